@@ -1,0 +1,432 @@
+"""Pins of the float64 oracle against facts fixed outside the oracle itself:
+library routines on special cases, closed forms, brute force on tiny inputs,
+invariants of the mathematics, and numbers the paper prints."""
+
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hga_oracle as O
+from paper_2606_30709_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden(name):
+    vals = {}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].strip()
+            if line:
+                k, v = (x.strip() for x in line.split("="))
+                vals[k] = float(v)
+    return vals
+
+
+def _rand_qkv(rng, B, Hq, Hkv, N, d, base, scale=1.0):
+    """Gaussian raw Q/K rotated (rotate-half) at positions 0..N-1, written
+    here with complex arithmetic, independently of the generator."""
+    half = d // 2
+    theta = base ** (-2.0 * np.arange(half) / d)
+    rot = np.exp(1j * np.arange(N)[:, None] * theta[None, :])
+
+    def rope(x):
+        z = (x[..., :half] + 1j * x[..., half:]) * rot
+        return np.concatenate([z.real, z.imag], axis=-1)
+
+    q = rope(rng.standard_normal((B, Hq, N, d)) * scale)
+    k = rope(rng.standard_normal((B, Hkv, N, d)) * scale)
+    v = rng.standard_normal((B, Hkv, N, d))
+    return q, k, v
+
+
+def _sdpa_dense(q, k, v):
+    """Dense causal attention (Eq. 1) by torch's own SDPA in float64 on CPU."""
+    r = q.shape[1] // k.shape[1]
+    qt = torch.from_numpy(q)
+    kt = torch.from_numpy(k).repeat_interleave(r, dim=1)
+    vt = torch.from_numpy(v).repeat_interleave(r, dim=1)
+    out = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True)
+    logits = (qt @ kt.transpose(-1, -2)) / math.sqrt(q.shape[-1])
+    n = q.shape[2]
+    logits = logits.masked_fill(torch.ones(n, n, dtype=torch.bool).triu(1), float("-inf"))
+    return out.numpy(), torch.logsumexp(logits, dim=-1).numpy()
+
+
+# ----------------------------------------------------------- dense pins ---
+
+@pytest.mark.parametrize("B,Hq,Hkv,N,d,base,F,L", [
+    (1, 1, 1, 1024, 64, 1e4, 1, 0),     # tiny preset shape
+    (2, 4, 4, 2048, 64, 1e4, 1, 0),     # MHA, d64
+    (1, 8, 1, 2048, 128, 1e6, 1, 2),    # GQA 8:1, d128
+    (1, 8, 2, 1024, 128, 1e6, 2, 8),    # decode-style windows
+])
+def test_full_coverage_is_dense_causal_attention(B, Hq, Hkv, N, d, base, F, L):
+    """Routing every chunk and group must reproduce dense causal attention
+    (Sec. 5.7 first correctness mode; Table 7)."""
+    rng = np.random.default_rng(7)
+    q, k, v = _rand_qkv(rng, B, Hq, Hkv, N, d, base)
+    C, G = 64, 16
+    nc = N // C
+    res = O.hga_forward(q, k, v, chunk=C, group=G, keep_first=F, keep_last=L, force_prev=1,
+                        topk_chunks=nc, topk_groups=nc * C // G, rope_base=base)
+    ref_out, ref_lse = _sdpa_dense(q, k, v)
+    assert np.max(np.abs(res["out"] - ref_out)) < 1e-12
+    assert np.max(np.abs(res["lse"] - ref_lse)) < 1e-12
+
+
+def test_attention_matches_scalar_loops_of_eq1():
+    """Tiny case against Eq. (1) written as scalar Python loops, with a
+    routing budget that actually drops chunks: the loops visit exactly the
+    tokens of the oracle's working set plus the causal current chunk."""
+    rng = np.random.default_rng(3)
+    B, Hq, Hkv, N, d, base = 1, 2, 1, 512, 8, 1e4
+    C, G, F, L, Kc, Kg = 64, 16, 1, 0, 2, 3
+    q, k, v = _rand_qkv(rng, B, Hq, Hkv, N, d, base)
+    res = O.hga_forward(q, k, v, chunk=C, group=G, keep_first=F, keep_last=L, force_prev=1,
+                        topk_chunks=Kc, topk_groups=Kg, rope_base=base)
+    gi = res["group_idx"]
+    for h in range(Hq):
+        for t in range(N):
+            c = t // C
+            allowed = set()
+            for cc in range(c):
+                if cc < F or cc >= c - max(L, 1):
+                    allowed.update(range(cc * C, (cc + 1) * C))
+            for g in gi[0, 0, c]:
+                if g >= 0:
+                    allowed.update(range(g * G, (g + 1) * G))
+            allowed.update(range(c * C, t + 1))
+            logits = {u: sum(q[0, h, t, x] * k[0, 0, u, x] for x in range(d)) / math.sqrt(d)
+                      for u in sorted(allowed)}
+            mx = max(logits.values())
+            den = sum(math.exp(s - mx) for s in logits.values())
+            for x in range(d):
+                num = sum(math.exp(logits[u] - mx) * v[0, 0, u, x] for u in logits)
+                assert abs(res["out"][0, h, t, x] - num / den) < 1e-12
+            assert abs(res["lse"][0, h, t] - (mx + math.log(den))) < 1e-12
+
+
+# --------------------------------------------------------- summary pins ---
+
+def test_high_freq_pair_counts_by_hand():
+    # wavelength 2*pi*base**(2p/d) <= span, solved for p by hand:
+    # d64/base1e4: span64 -> p <= 8.06 -> 9 pairs; span16 -> p <= 3.25 -> 4 pairs
+    # d128/base1e6: span64 -> p <= 10.75 -> 11 pairs; span16 -> p <= 4.33 -> 5 pairs
+    assert O.high_freq_pairs(64, 64, 1e4) == 9
+    assert O.high_freq_pairs(16, 64, 1e4) == 4
+    assert O.high_freq_pairs(64, 128, 1e6) == 11
+    assert O.high_freq_pairs(16, 128, 1e6) == 5
+
+
+@pytest.mark.parametrize("d,base,pos0", [(64, 1e4, 0), (128, 1e6, 0), (64, 1e4, 4096),
+                                          (128, 1e6, 65536)])
+def test_summary_phase_form_equals_literal_rule(d, base, pos0):
+    """Sec. 3.2: rotated-mean for high-frequency pairs and raw-mean rotated at
+    the middle for low-frequency pairs, computed literally through absolute
+    positions, equals the phase-adjusted form on rotated keys."""
+    rng = np.random.default_rng(11)
+    N = 512
+    half = d // 2
+    theta = base ** (-2.0 * np.arange(half) / d)
+    raw = rng.standard_normal((2, 3, N, d))
+    z = (raw[..., :half] + 1j * raw[..., half:]) * np.exp(1j * (pos0 + np.arange(N))[:, None] * theta)
+    k_rot = np.concatenate([z.real, z.imag], -1)
+    for span in (64, 16):
+        nhf = O.high_freq_pairs(span, d, base)
+        a = O.summaries(k_rot, span, base, nhf)
+        b = O.summaries_literal(k_rot, span, base, nhf, first_position=pos0)
+        tol = 1e-12 if pos0 < 10000 else 1e-9   # angle arguments near 6.5e4 rad
+        assert np.max(np.abs(a - b)) < tol
+
+
+@pytest.mark.parametrize("d,base", [(64, 1e4), (128, 1e6)])
+@pytest.mark.parametrize("span,start", [(64, 0), (64, 640), (16, 48), (16, 4096)])
+def test_summary_of_constant_raw_key_closed_form(d, base, span, start):
+    """A span whose raw key is the same vector w at every token.  Closed form:
+    low-frequency pair -> w rotated at the middle m = start + (span-1)/2;
+    high-frequency pair -> the mean of e^{i t theta} over the span times w,
+    i.e. the Dirichlet kernel sin(span*theta/2) / (span*sin(theta/2)) times
+    w rotated at m."""
+    rng = np.random.default_rng(5)
+    half = d // 2
+    theta = base ** (-2.0 * np.arange(half) / d)
+    w = rng.standard_normal(d)
+    wz = w[:half] + 1j * w[half:]
+    t = start + np.arange(span)
+    z = wz[None, :] * np.exp(1j * t[:, None] * theta[None, :])
+    k_rot = np.concatenate([z.real, z.imag], -1)[None, None]
+    nhf = O.high_freq_pairs(span, d, base)
+    got = O.summaries(k_rot, span, base, nhf)[0, 0, 0]
+    m = start + (span - 1) / 2.0
+    dirichlet = np.sin(span * theta / 2) / (span * np.sin(theta / 2))
+    gain = np.where(np.arange(half) < nhf, dirichlet, 1.0)
+    ez = gain * wz * np.exp(1j * m * theta)
+    exp = np.concatenate([ez.real, ez.imag])
+    assert np.max(np.abs(got - exp)) < 1e-12
+    # the Dirichlet gain of the fastest pair is far from 1, so the split matters
+    assert abs(dirichlet[0]) < 0.2
+
+
+def test_summary_all_high_frequency_is_plain_mean():
+    rng = np.random.default_rng(2)
+    k = rng.standard_normal((1, 2, 256, 64))
+    got = O.summaries(k, 64, 1e4, 32)
+    assert np.max(np.abs(got - k.reshape(1, 2, 4, 64, 64).mean(axis=3))) < 1e-15
+
+
+# ------------------------------------------------------------- query means ---
+
+def test_query_means_group_consecutive_heads():
+    """GQA (Sec. 2): query head h reads KV head h // r.  With q == h
+    everywhere, q_bar of KV head j is the mean of j*r .. j*r + r - 1."""
+    B, Hq, Hkv, T, d = 2, 8, 2, 128, 4
+    q = np.broadcast_to(np.arange(Hq, dtype=np.float64)[None, :, None, None], (B, Hq, T, d))
+    qb = O.query_means(q, Hkv, 64)
+    r = Hq // Hkv
+    for j in range(Hkv):
+        assert np.all(qb[:, j] == j * r + (r - 1) / 2)
+
+
+# --------------------------------------------------------------- routing ---
+
+def test_visibility_sets_by_hand():
+    # F=1, L=0 with force-include: D = {0, c-1}; M = [1, c-1)
+    assert O.visibility(0, 1, 0, 1) == ([], [])
+    assert O.visibility(1, 1, 0, 1) == ([0], [])
+    assert O.visibility(2, 1, 0, 1) == ([0, 1], [])
+    assert O.visibility(5, 1, 0, 1) == ([0, 4], [1, 2, 3])
+    # without force-include (literal "first chunk hot + current" wording)
+    assert O.visibility(5, 1, 0, 0) == ([0], [1, 2, 3, 4])
+    # F=2, L=8 (Sec. 4.1 table) at chunk 1024
+    D, M = O.visibility(1024, 2, 8, 1)
+    assert D == [0, 1] + list(range(1016, 1024)) and M == list(range(2, 1016))
+    # windows overlapping early on
+    assert O.visibility(6, 2, 8, 1) == ([0, 1, 2, 3, 4, 5], [])
+
+
+def test_topk_is_the_max_sum_subset():
+    """Brute force: with distinct scores the selected k-set is the unique
+    k-subset of largest total score."""
+    rng = np.random.default_rng(13)
+    for trial in range(30):
+        n = int(rng.integers(3, 9))
+        k = int(rng.integers(1, n + 1))
+        ids = np.sort(rng.choice(100, size=n, replace=False))
+        sc = rng.standard_normal(n)
+        best = max(itertools.combinations(range(n), k), key=lambda s: sum(sc[list(s)]))
+        assert list(O.topk_lowest_index(sc, ids, k)) == sorted(ids[list(best)])
+
+
+def test_ties_resolve_to_lowest_index():
+    B, H, d, N, C, G = 1, 2, 16, 1024, 64, 16
+    rng = np.random.default_rng(4)
+    k = rng.standard_normal((B, H, N, d))
+    q = np.zeros((B, H, N, d))
+    cs = O.summaries(k, C, 1e4, 2)
+    gs = O.summaries(k, G, 1e4, 1)
+    qb = O.query_means(q, H, C)
+    ids = list(range(N // C))
+    ci = O.route_chunks(qb, cs, ids, 1, 0, 1, 3)
+    # all scores are exactly zero: the three lowest middle chunks win
+    for c in ids:
+        _, M = O.visibility(c, 1, 0, 1)
+        exp = (M[:3] + [-1, -1, -1])[:3]
+        assert list(ci[0, 0, c]) == exp and list(ci[0, 1, c]) == exp
+    gi = O.route_groups(qb, ci, gs, C // G, 5)
+    for c in ids:
+        chunks = [x for x in ci[0, 0, c] if x >= 0]
+        cand = [4 * x + i for x in chunks for i in range(4)]
+        assert list(gi[0, 0, c]) == (cand[:5] + [-1] * 5)[:5]
+    # duplicated best summary: both copies beat the rest, the lower one wins at k=1
+    cs2 = cs.copy()
+    qb2 = rng.standard_normal(qb.shape)
+    cs2[:, :, 3] = qb2[:, :, -1] * 10
+    cs2[:, :, 9] = qb2[:, :, -1] * 10
+    ci1 = O.route_chunks(qb2, cs2, ids, 1, 0, 1, 1)
+    ci2 = O.route_chunks(qb2, cs2, ids, 1, 0, 1, 2)
+    assert ci1[0, 0, 15, 0] == 3 and list(ci2[0, 0, 15]) == [3, 9]
+
+
+def test_chunk_only_variant_opens_whole_chunks():
+    """With K_g >= (C/G) K_c every group of every selected chunk is opened:
+    the exact-token chunk variant of the Qwen3 wrapper (Sec. 3.3, Sec. 4.1)."""
+    rng = np.random.default_rng(8)
+    q, k, v = _rand_qkv(rng, 1, 4, 2, 2048, 64, 1e4)
+    res = O.hga_forward(q, k, v, chunk=64, group=16, keep_first=2, keep_last=8, force_prev=1,
+                        topk_chunks=5, topk_groups=20, rope_base=1e4)
+    ci, gi = res["chunk_idx"], res["group_idx"]
+    for b, j, i in itertools.product(range(1), range(2), range(32)):
+        chunks = [x for x in ci[b, j, i] if x >= 0]
+        groups = [x for x in gi[b, j, i] if x >= 0]
+        assert groups == [4 * c + t for c in chunks for t in range(4)]
+
+
+def test_planted_needles_are_routed():
+    w = W.preset("tiny")
+    inp = W.generate(w)
+    q, k, v = (W.storage_to_f64(inp[x], w.dtype) for x in "qkv")
+    res = O.hga_forward(q, k, v, chunk=w.chunk, group=w.group, keep_first=w.keep_first,
+                        keep_last=w.keep_last, force_prev=w.force_prev,
+                        topk_chunks=w.topk_chunks, topk_groups=w.topk_groups,
+                        rope_base=w.rope_base)
+    for kc, qc in inp["needles"]:
+        assert kc in res["chunk_idx"][0, 0, qc]
+    # SmallLM-shaped pairs, reduced to one sequence of 2048 tokens
+    w2 = W.preset("smalllm").with_(batch=1, seq_len=2048)
+    inp2 = W.generate(w2)
+    q, k, v = (W.storage_to_f64(inp2[x], w2.dtype) for x in "qkv")
+    res2 = O.hga_forward(q, k, v, chunk=64, group=16, keep_first=1, keep_last=0, force_prev=1,
+                         topk_chunks=w2.topk_chunks, topk_groups=w2.topk_groups,
+                         rope_base=w2.rope_base, attend_units=[])
+    hits = [all(kc in res2["chunk_idx"][b, j, qc] for j in range(w2.n_kv_heads))
+            for b, kc, qc in inp2["needles"]]
+    assert all(hits)
+
+
+# ---------------------------------------------------------------- budgets ---
+
+def _closed_form_fetch(c, C, G, F, L, Kc, Kg):
+    window = max(L, 1)
+    n_det = min(c, F + window)
+    n_mid = max(0, c - window - F)
+    kg = min(Kg, (C // G) * min(Kc, n_mid))
+    return C * n_det + G * kg, kg
+
+
+@pytest.mark.parametrize("key", list(W.PRESETS))
+def test_fetched_tokens_closed_form_and_budget(key):
+    w = W.preset(key)
+    C, G = w.chunk, w.group
+    for c in list(range(0, 40)) + [w.n_chunks - 1]:
+        exp, kg = _closed_form_fetch(c, C, G, w.keep_first, w.keep_last, w.topk_chunks,
+                                     w.topk_groups)
+        assert O.fetched_tokens(c, kg, C, G, w.keep_first, w.keep_last, w.force_prev) == exp
+    last = w.n_chunks - 1
+    exp, kg = _closed_form_fetch(last, C, G, w.keep_first, w.keep_last, w.topk_chunks,
+                                 w.topk_groups)
+    frac = (exp + C) / w.seq_len
+    budget = {"tiny": 0.25, "smalllm": 0.03125, "train12k": 0.03125, "qwen32k": 0.03125,
+              "decode64k": 1216 / 65600}[key]
+    assert frac == pytest.approx(budget, rel=1e-12)
+
+
+def test_routing_emits_the_closed_form_group_count():
+    rng = np.random.default_rng(21)
+    q, k, v = _rand_qkv(rng, 1, 2, 1, 4096, 64, 1e4)
+    res = O.hga_forward(q, k, v, chunk=64, group=16, keep_first=1, keep_last=2, force_prev=1,
+                        topk_chunks=3, topk_groups=7, rope_base=1e4, attend_units=[])
+    for c in range(64):
+        _, kg = _closed_form_fetch(c, 64, 16, 1, 2, 3, 7)
+        assert int(np.sum(res["group_idx"][0, 0, c] >= 0)) == kg
+
+
+def test_paper_budget_numbers():
+    g = _golden("paper_budgets.txt")
+    C = int(g["qwen_chunk"])
+    # Sec. 4.1 table: sink and recent windows in tokens
+    D, _ = O.visibility(100, int(g["qwen_keep_first_chunks"]), int(g["qwen_keep_last_chunks"]), 1)
+    assert sum(1 for c in D if c < 2) * C == g["qwen_sink_tokens"]
+    assert sum(1 for c in D if c >= 2) * C == g["qwen_recent_tokens"]
+    # Sec. 3.6: 16 opened chunks of 64 tokens = 1024 routed middle tokens
+    routed = O.fetched_tokens(100, int(g["qwen_topk_chunks"]) * 4, C, 16, 2, 8, 1) - 640
+    assert routed == g["qwen_routed_middle_tokens"]
+    # Sec. 5.3: 65,599 tokens in 1,025 chunks; K_g = 32 groups of 16 tokens
+    n = int(g["niah_prompt_tokens"])
+    assert math.ceil(n / C) == g["niah_chunks"]
+    last = n // C                     # the partial last chunk holds the final tokens
+    kg = min(int(g["niah_topk_groups"]), 4 * int(g["niah_topk_chunks"]))
+    hist = O.fetched_tokens(last, kg, C, int(g["niah_group"]), 2, 8, 1)
+    cur = n - last * C
+    assert round(100 * (hist + cur) / n, 1) == g["niah_sparsity_percent"]
+
+
+# ----------------------------------------------------------- invariants ---
+
+def _run(q, k, v, w, **kw):
+    return O.hga_forward(q, k, v, chunk=w.chunk, group=w.group, keep_first=w.keep_first,
+                         keep_last=w.keep_last, force_prev=w.force_prev,
+                         topk_chunks=w.topk_chunks, topk_groups=w.topk_groups,
+                         rope_base=w.rope_base, **kw)
+
+
+def test_causality_later_tokens_do_not_matter():
+    w = W.preset("smalllm").with_(batch=1, n_q_heads=2, n_kv_heads=2, seq_len=1536)
+    inp = W.generate(w)
+    q, k, v = (W.storage_to_f64(inp[x], w.dtype) for x in "qkv")
+    base = _run(q, k, v, w)
+    cut = 13 * 64
+    rng = np.random.default_rng(99)
+    q2, k2, v2 = q.copy(), k.copy(), v.copy()
+    for x in (q2, k2, v2):
+        x[:, :, cut:] += rng.standard_normal(x[:, :, cut:].shape)
+    pert = _run(q2, k2, v2, w)
+    assert np.array_equal(base["chunk_idx"][:, :, :13], pert["chunk_idx"][:, :, :13])
+    assert np.array_equal(base["group_idx"][:, :, :13], pert["group_idx"][:, :, :13])
+    assert np.array_equal(base["out"][:, :, :cut], pert["out"][:, :, :cut])
+
+
+def test_prefill_equals_block_sequential_decode():
+    """Sec. 5.7 second correctness mode: vectorised prefill and
+    chunk-by-chunk decode agree."""
+    w = W.preset("qwen32k").with_(n_q_heads=8, n_kv_heads=2, seq_len=1280, keep_last=2,
+                                   topk_chunks=4, topk_groups=6)
+    inp = W.generate(w)
+    q, k, v = (W.storage_to_f64(inp[x], w.dtype) for x in "qkv")
+    full = _run(q, k, v, w)
+    C = w.chunk
+    for c in range(w.n_chunks):
+        blk = _run(q[:, :, c * C:(c + 1) * C], k[:, :, :(c + 1) * C], v[:, :, :(c + 1) * C], w,
+                   q_chunk0=c)
+        assert np.array_equal(blk["chunk_idx"][:, :, 0], full["chunk_idx"][:, :, c])
+        assert np.array_equal(blk["group_idx"][:, :, 0], full["group_idx"][:, :, c])
+        assert np.max(np.abs(blk["out"] - full["out"][:, :, c * C:(c + 1) * C])) < 1e-12
+        assert np.max(np.abs(blk["qbar"][:, :, 0] - full["qbar"][:, :, c])) < 1e-15
+
+
+@pytest.mark.parametrize("shift", [4096, 12345])
+def test_rope_translation_invariance(shift):
+    """Shifting every absolute position leaves scores, selections and outputs
+    unchanged: summaries are built consistently with the queries' RoPE."""
+    # no needles: they are planted on rotated values, which a shift would not rotate
+    w = W.preset("qwen32k").with_(n_q_heads=8, n_kv_heads=2, seq_len=2048, topk_chunks=4,
+                                   topk_groups=6, needle_mode="none")
+    a = W.generate(w, unrounded=True)
+    b = W.generate(w, position_offset=shift, unrounded=True)
+    ra = _run(a["q"], a["k"], a["v"], w)
+    rb = _run(b["q"], b["k"], b["v"], w)
+    assert np.array_equal(ra["chunk_idx"], rb["chunk_idx"])
+    assert np.array_equal(ra["group_idx"], rb["group_idx"])
+    assert np.max(np.abs(ra["out"] - rb["out"])) < 1e-9
+    ids = list(range(w.n_chunks))
+    _, ia = O.route_chunks(ra["qbar"], ra["chunk_sum"], ids, 1, 2, 1, 4, details=True)
+    _, ib = O.route_chunks(rb["qbar"], rb["chunk_sum"], ids, 1, 2, 1, 4, details=True)
+    for x, y in zip(ia, ib):
+        assert np.max(np.abs(x[4] - y[4])) < 1e-9
+
+
+def test_gather_copies_the_named_tokens():
+    """Each token row encodes its own (head, position); the gathered rows must
+    name exactly the tokens of the listed groups, zero for padding."""
+    B, H, N, d, G = 2, 3, 512, 8, 16
+    pos = np.arange(N, dtype=np.float64)
+    k = np.broadcast_to(pos[None, None, :, None] + 1000 * np.arange(H)[None, :, None, None]
+                        + 1e6 * np.arange(B)[:, None, None, None], (B, H, N, d)).copy()
+    v = -k
+    gi = np.full((B, H, 3, 4), -1, dtype=np.int32)
+    gi[0, 1, 2, :3] = [1, 7, 30]
+    gi[1, 2, 0, :4] = [0, 2, 4, 31]
+    ko, vo = O.gather(gi, k, v, G)
+    for b, h, i in itertools.product(range(B), range(H), range(3)):
+        for s in range(4):
+            g = gi[b, h, i, s]
+            rows = ko[b, h, i, s * G:(s + 1) * G, 0]
+            if g < 0:
+                assert np.all(rows == 0) and np.all(vo[b, h, i, s * G:(s + 1) * G] == 0)
+            else:
+                assert np.array_equal(rows, 1e6 * b + 1000 * h + np.arange(g * G, (g + 1) * G))
+                assert np.array_equal(vo[b, h, i, s * G:(s + 1) * G, 0], -rows)
