@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Routed-attention throughput of one layer on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input: chunk and
+group summaries, chunk routing, group refinement, gather of the routed K/V,
+and exact attention (five C-ABI calls, inputs already resident in HBM).  The
+default workload is the SmallLM-shaped prefill (B4, 8/8 heads, d64, 8192
+tokens, bf16, C64 G16, first chunk hot, K_c 3, K_g 4 -> 3.125% of the
+context fetched by the last chunk).
+
+Prints one JSON line.  Per-kernel durations come from HIP events recorded
+around every call on the launch stream during the timed steps; the dominant
+kernel's algorithmic bytes over its mean duration give the roofline entry.
+The float64 oracle timed on the host cores over a bounded sample of the same
+workload gives the CPU baseline.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
+
+STAGES = ("build_summaries", "route_chunks", "route_groups", "gather_kv", "attend")
+
+
+def algorithmic_bytes(w, n_valid_rows: int) -> dict:
+    """Bytes each kernel must move at least once per step (compulsory
+    traffic).  n_valid_rows = routed token rows (all heads, all chunks)."""
+    B, Hq, Hkv, d, N, C, G = (w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.seq_len,
+                              w.chunk, w.group)
+    e = w.elem_bytes
+    nc = w.n_chunks
+    gpc = C // G
+    kv_tok = B * Hkv * N * d * e          # one of K or V
+    q_tok = B * Hq * N * d * e
+    table_c = B * Hkv * nc * d * 4
+    table_g = B * Hkv * nc * gpc * d * 4
+    routed = n_valid_rows * d * e         # one of K or V
+    return {
+        "build_summaries": kv_tok + table_c + table_g,
+        "route_chunks": q_tok + table_c + table_c + B * Hkv * nc * w.topk_chunks * 4,
+        "route_groups": table_c + table_g + B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4,
+        "gather_kv": 4 * routed + B * Hkv * nc * w.topk_groups * 4,
+        "attend": q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4,
+    }
+
+
+def attention_flops(w, group_idx: np.ndarray) -> float:
+    """Exact-attention FLOPs of a step: 4*d per (query, key) pair (QK^T and PV)."""
+    C, G, d, r = w.chunk, w.group, w.head_dim, w.gqa_ratio
+    F, W = w.keep_first, max(w.keep_last, 1 if w.force_prev else 0)
+    valid = (group_idx >= 0).sum(axis=-1)             # [B, Hkv, nq]
+    pairs = 0
+    for i in range(group_idx.shape[2]):
+        c = w.q_chunk0 + i
+        a = min(F, c)
+        nd = a + (c - max(a, max(0, c - W)))
+        hist = nd * C
+        pairs += r * (C * hist * group_idx.shape[0] * group_idx.shape[1]
+                      + C * G * int(valid[:, :, i].sum()) + group_idx.shape[0] *
+                      group_idx.shape[1] * C * (C + 1) // 2)
+    return 4.0 * d * pairs
+
+
+def cpu_baseline(w, inp, max_seconds: float) -> dict:
+    """The float64 oracle, as it stands, over the (batch, KV head) units of the
+    same workload in order (wrapping around) until max_seconds of CPU work."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import hga_oracle as O
+    from paper_2606_30709_amd import workloads as W
+
+    r = w.gqa_ratio
+    units = [(b, j) for b in range(w.batch) for j in range(w.n_kv_heads)]
+    done = 0
+    t0 = time.perf_counter()
+    while True:
+        b, j = units[done % len(units)]
+        q = W.storage_to_f64(inp["q"][b:b + 1, j * r:(j + 1) * r], w.dtype)
+        k = W.storage_to_f64(inp["k"][b:b + 1, j:j + 1], w.dtype)
+        v = W.storage_to_f64(inp["v"][b:b + 1, j:j + 1], w.dtype)
+        O.hga_forward(q, k, v, chunk=w.chunk, group=w.group, keep_first=w.keep_first,
+                      keep_last=w.keep_last, force_prev=w.force_prev, topk_chunks=w.topk_chunks,
+                      topk_groups=w.topk_groups, rope_base=w.rope_base, with_gather=True)
+        done += 1
+        if time.perf_counter() - t0 > max_seconds:
+            break
+    dt = time.perf_counter() - t0
+    frac = done / len(units)           # may exceed 1: the layer is swept repeatedly
+    tokens = frac * w.batch * w.seq_len
+    threads = 1
+    for pool in threadpool_info():
+        threads = max(threads, int(pool.get("num_threads", 1)))
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} (batch, KV head) units of {len(units)} in the layer, all "
+                      f"{w.n_chunks} chunks each, five stages, float64 NumPy, {dt:.1f} s",
+            "cpu": platform.processor() or platform.machine(), "host_cpus": os.cpu_count()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="smalllm",
+                    help="workload preset (default smalllm, the SmallLM-shaped prefill)")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="CPU budget of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for "
+              f"--gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_30709_amd import hga
+    from paper_2606_30709_amd import workloads as W
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+
+    w = W.preset(args.workload)
+    if w.decode_block:
+        print("bench.py times the prefill workloads; the decode block is covered by the tests",
+              file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    p = pipe.plan
+
+    calls = (
+        lambda: hga.hga_build_summaries(p, pipe.k, 0, w.n_chunks, pipe.chunk_sum, pipe.group_sum,
+                                        stream=sh),
+        lambda: hga.hga_route_chunks(p, pipe.q, 0, pipe.chunk_sum, pipe.qbar, pipe.chunk_idx,
+                                     stream=sh),
+        lambda: hga.hga_route_groups(p, pipe.qbar, pipe.chunk_idx, 0, pipe.group_sum,
+                                     pipe.group_idx, stream=sh),
+        lambda: hga.hga_gather_kv(p, pipe.group_idx, 0, pipe.k, pipe.v, pipe.k_routed,
+                                  pipe.v_routed, stream=sh),
+        lambda: hga.hga_attend(p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
+                               pipe.group_idx, pipe.out, pipe.lse, stream=sh),
+    )
+
+    for _ in range(args.warmup):
+        for f in calls:
+            f()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(K):
+        row = ev[s]
+        row[0].record(stream)
+        for n, f in enumerate(calls):
+            f()
+            row[n + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    stage_ms = {name: float(np.mean([ev[s][n].elapsed_time(ev[s][n + 1]) for s in range(K)]))
+                for n, name in enumerate(STAGES)}
+    gpu_step_ms = float(np.mean([ev[s][0].elapsed_time(ev[s][-1]) for s in range(K)]))
+    wall_ms = (t1 - t0) * 1e3 / K
+    tokens = w.batch * w.seq_len
+    gi = pipe.group_idx.cpu().numpy()
+    n_valid_rows = int((gi >= 0).sum()) * w.group
+    abytes = algorithmic_bytes(w, n_valid_rows)
+    flops = attention_flops(w, gi)
+
+    dominant = max(STAGES, key=lambda s: stage_ms[s])
+    stages = {}
+    for sname in STAGES:
+        sec = stage_ms[sname] * 1e-3
+        ent = {"us": round(stage_ms[sname] * 1e3, 2),
+               "alg_bytes": abytes[sname], "GB_s": round(abytes[sname] / sec / 1e9, 1),
+               "hbm_frac": round(abytes[sname] / sec / 1e9 / HBM_PEAK_GBS, 4)}
+        if sname == "attend":
+            ent["TFLOP_s"] = round(flops / sec / 1e12, 2)
+            ent["mfma_frac"] = round(flops / sec / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+        stages[sname] = ent
+    dsec = stage_ms[dominant] * 1e-3
+    achieved = abytes[dominant] / dsec / 1e9
+    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": None, "alg_bytes_per_launch": abytes[dominant],
+                "mean_launch_us": round(stage_ms[dominant] * 1e3, 2)}
+
+    res = {
+        "metric": "routed-attn tokens/s per layer",
+        "value": round(tokens * K / (t1 - t0), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{w.key}: prefill B{w.batch} H{w.n_q_heads}/{w.n_kv_heads} "
+                         f"d{w.head_dim} N{w.seq_len} {w.dtype} C{w.chunk} G{w.group} "
+                         f"F{w.keep_first} L{w.keep_last} Kc{w.topk_chunks} Kg{w.topk_groups}"),
+            "batch": w.batch, "seq_len": w.seq_len, "tokens_per_step": tokens,
+            "seed": inp["seed"],
+        },
+        "gpu_ms_per_step_events": round(gpu_step_ms, 4),
+        "stages": stages,
+        "roofline": roofline,
+        "device": torch.cuda.get_device_properties(0).gcnArchName,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

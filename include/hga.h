@@ -1,0 +1,233 @@
+/*
+ * hga.h -- C ABI of the MI355X (gfx950) routed-attention path of
+ * Hierarchical Global Attention (HGA).
+ *
+ * The five calls follow the paper's statement of the problem.  Its tiered
+ * K/V store (Sec. 4.3) exposes four operations -- append a closed chunk,
+ * read chunk summaries, fetch group summaries, gather exact token K/V --
+ * and the routed module then runs exact-token attention (Sec. 3.4):
+ *
+ *   hga_build_summaries  mixed-RoPE chunk and group key summaries (Sec. 3.1, 3.2)
+ *   hga_route_chunks     query-chunk -> chunk scoring, top-K_c (Sec. 3.3)
+ *   hga_route_groups     group refinement inside the chosen chunks, top-K_g (Sec. 3.3)
+ *   hga_gather_kv        copy the routed groups' exact token K/V (Sec. 4.3)
+ *   hga_attend           exact causal softmax attention, Eq. (1), over the
+ *                        current chunk, the always-visible chunks and the
+ *                        routed groups (Sec. 3.3, 3.4)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are row-major "BHND": [batch, heads, tokens, head_dim] with
+ *   head_dim contiguous.  Q and K arrive already rotated by RoPE at their
+ *   absolute positions (rotate-half pairing: dimension p pairs with
+ *   p + head_dim/2).  Chunk c is tokens [c*chunk, (c+1)*chunk).
+ * - Query head h reads KV head h / (n_q_heads / n_kv_heads) (GQA, Sec. 2);
+ *   routing is per KV head and shared by its query heads.
+ * - Element type of Q, K, V, the routed buffers and the output: the plan's
+ *   dtype (fp32 or bf16).  Summaries and query means are fp32; indices are
+ *   int32, ascending, padded with -1.
+ * - Every buffer is owned by the caller; the calls allocate nothing.
+ *   Pointers are device pointers unless stated otherwise.  Tensor pointers
+ *   must be 16-byte aligned, index pointers 4-byte aligned.
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the
+ *   legacy default stream) and must run with the plan's device current.
+ *   All argument checks happen on the host before anything is launched; a
+ *   failing check launches nothing and returns a negative hga_status.
+ * - Error strings: hga_last_error() returns the message of the last failing
+ *   call on the calling thread.  No C++ exception crosses this interface.
+ * - The library keeps no state between calls besides the plan, so calls on
+ *   different streams may overlap as long as their buffers do not.
+ */
+#ifndef HGA_H
+#define HGA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HGA_OK = 0,
+    HGA_EINVAL = -1,        /* invalid argument: null pointer, size or id out of range */
+    HGA_EUNSUPPORTED = -2,  /* valid by the method but outside what the kernels cover  */
+    HGA_EALIGN = -3,        /* misaligned pointer                                       */
+    HGA_EHIP = -4           /* a HIP runtime call failed (no device, launch failure...) */
+} hga_status;
+
+typedef enum { HGA_F32 = 0, HGA_BF16 = 1 } hga_dtype;
+
+/* Routing configuration (Sec. 3.1-3.3).  Field meaning and accepted values:
+ *   batch, n_q_heads, n_kv_heads  >= 1, n_q_heads % n_kv_heads == 0,
+ *                                 n_q_heads / n_kv_heads <= 16
+ *   head_dim        64 or 128
+ *   chunk           C, the chunk length: 64 (Sec. 3.1)
+ *   group           g_s, the group length: 8, 16 or 32 (divides chunk)
+ *   keep_first      F: the first F chunks are always visible (attention sinks)
+ *   keep_last       L: the last L closed chunks are always visible
+ *   force_prev      1: the preceding chunk is force-included when L == 0
+ *                   (Sec. 3.3 "Deterministic visibility"); 0: not included
+ *   topk_chunks     K_c in [1, 512]: chunks kept by chunk routing
+ *   topk_groups     K_g in [1, 512]: groups opened by group refinement
+ *   hf_pairs_chunk  number of high-frequency RoPE pairs for chunk summaries;
+ *   hf_pairs_group  ... for group summaries.  -1 selects the rule "pair p is
+ *                   high-frequency when its wavelength 2*pi*base^(2p/d) is at
+ *                   most the span" (Sec. 3.2 gives no threshold).
+ *   dtype           hga_dtype of Q/K/V/routed buffers/output
+ *   rope_base       RoPE base (> 1), theta_p = base^(-2p/head_dim)
+ *
+ * Visible closed chunks of query chunk c ("D_c"): chunks [0, min(F, c)) and
+ * [max(0, c - W), c) with W = max(L, force_prev ? 1 : 0).  Routable middle
+ * ("M_c"): chunks [F, c - W).  Chunk routing keeps min(K_c, |M_c|) chunks;
+ * group refinement opens min(K_g, (chunk/group) * that) groups. */
+typedef struct {
+    int32_t batch;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t chunk;
+    int32_t group;
+    int32_t keep_first;
+    int32_t keep_last;
+    int32_t force_prev;
+    int32_t topk_chunks;
+    int32_t topk_groups;
+    int32_t hf_pairs_chunk;
+    int32_t hf_pairs_group;
+    int32_t dtype;
+    double rope_base;
+} hga_params;
+
+typedef struct hga_plan hga_plan;
+
+/* Validate `params`, compute the summary phase tables in double precision on
+ * the host (stored as fp32) and upload them to the current device.  The plan
+ * owns that device memory (a few tens of KiB) and is bound to the device
+ * current at creation.  *plan is set only on HGA_OK.  Returns HGA_EINVAL /
+ * HGA_EUNSUPPORTED for bad params before touching the device, HGA_EHIP if
+ * there is no usable device. */
+hga_status hga_plan_create(const hga_params* params, hga_plan** plan);
+
+/* Release the plan's device memory.  NULL is accepted.  The caller must not
+ * destroy a plan while work that uses it is still queued. */
+hga_status hga_plan_destroy(hga_plan* plan);
+
+/* Copy the plan's resolved parameters (hf_pairs_* filled in) to *out. */
+hga_status hga_plan_params(const hga_plan* plan, hga_params* out);
+
+/* Mixed-RoPE chunk and group key summaries (Sec. 3.2), the store's "append
+ * a newly closed chunk" (Sec. 4.3).
+ *
+ * For each chunk c in [chunk_begin, chunk_end) and each (batch, KV head):
+ *   chunk_sum[c]  = mean over the chunk's tokens of R(phi_p(o)) k_rot[t]
+ *   group_sum[g]  = the same over each of the chunk/group groups g of c
+ * where o = t - span start, phi_p(o) = 0 for the high-frequency pairs
+ * (rotated keys are averaged) and ((span-1)/2 - o) * theta_p for the others
+ * (which equals averaging the raw keys and rotating at the span's middle).
+ *
+ *   k_rot        [batch, n_kv_heads, k_tokens, head_dim] plan dtype; its
+ *                token 0 is the first token of chunk k_chunk0
+ *   chunk_sum    fp32 [batch, n_kv_heads, table_chunks, head_dim]
+ *   group_sum    fp32 [batch, n_kv_heads, table_chunks * chunk/group, head_dim]
+ * Requires k_chunk0 <= chunk_begin <= chunk_end <= table_chunks and
+ * (chunk_end - k_chunk0) * chunk <= k_tokens.  Rows of other chunks are not
+ * written.  An empty range is a no-op. */
+hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
+                               int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
+                               float* chunk_sum, float* group_sum, int32_t table_chunks,
+                               void* stream);
+
+/* Chunk-level content routing (Sec. 3.3), the store's "read chunk
+ * summaries".  For query chunk c = q_chunk0 + i and KV head j:
+ *   qbar[i]       = mean of q_rot over the chunk's tokens and the query
+ *                   heads of KV head j (chunk-shared routing, Sec. 1)
+ *   chunk_idx[i]  = the min(K_c, |M_c|) chunks of M_c with the largest
+ *                   qbar . chunk_sum[c'] (unscaled dot product), lowest
+ *                   chunk id first among equal scores; ascending, -1 padded
+ *
+ *   q_rot      [batch, n_q_heads, n_q_chunks * chunk, head_dim] plan dtype:
+ *              the tokens of chunks q_chunk0 .. q_chunk0 + n_q_chunks - 1
+ *   chunk_sum  fp32 [batch, n_kv_heads, table_chunks, head_dim]; only rows of
+ *              middle chunks are read
+ *   qbar       fp32 out [batch, n_kv_heads, n_q_chunks, head_dim]
+ *   chunk_idx  int32 out [batch, n_kv_heads, n_q_chunks, topk_chunks]
+ * Requires q_chunk0 >= 0, n_q_chunks >= 0 and q_chunk0 + n_q_chunks - 1 <=
+ * table_chunks.  HGA_EUNSUPPORTED when a query chunk has more than 16384
+ * middle chunks. */
+hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
+                            float* qbar, int32_t* chunk_idx, void* stream);
+
+/* Group refinement (Sec. 3.3), the store's "fetch group summaries".  The
+ * candidates of query chunk c are the groups (chunk/group) * c' + i of every
+ * chunk c' listed in chunk_idx[i]; the min(K_g, #candidates) groups with the
+ * largest qbar . group_sum are kept, globally across the chunks, lowest group
+ * id first among equal scores; ascending, -1 padded.
+ *
+ *   qbar, chunk_idx  as written by hga_route_chunks (chunk ids distinct)
+ *   group_sum        fp32 [batch, n_kv_heads, table_chunks * chunk/group, head_dim]
+ *   group_idx        int32 out [batch, n_kv_heads, n_q_chunks, topk_groups]
+ * chunk_idx entries outside [0, min(c, table_chunks)) are ignored like -1. */
+hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32_t* chunk_idx,
+                            int32_t q_chunk0, int32_t n_q_chunks, const float* group_sum,
+                            int32_t table_chunks, int32_t* group_idx, void* stream);
+
+/* Gather the exact token K/V of the routed groups (Sec. 4.3, "gathering
+ * exact token K/V for the selected chunks or groups").  Slot s of query chunk
+ * c = q_chunk0 + i receives tokens [g*group, (g+1)*group) of group
+ * g = group_idx[i][s]; slots with g outside [0, c*chunk/group) or beyond
+ * src_tokens are zero-filled.
+ *
+ *   k_src, v_src  [batch, n_kv_heads, src_tokens, head_dim] plan dtype.  With
+ *                 src_on_host == 0 they are device pointers.  With
+ *                 src_on_host == 1 they are pinned host allocations made with
+ *                 hipHostMalloc (mapped); the kernel reads them directly over
+ *                 the host link (the paper's RAM-backed cold tier) -- only the
+ *                 routed groups cross it.
+ *   k_routed, v_routed  out [batch, n_kv_heads, n_q_chunks, topk_groups*group,
+ *                 head_dim] plan dtype (device) */
+hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t q_chunk0,
+                         int32_t n_q_chunks, const void* k_src, const void* v_src,
+                         int64_t src_tokens, int32_t src_on_host, void* k_routed,
+                         void* v_routed, void* stream);
+
+/* Exact-token attention (Sec. 3.4) with the causal softmax of Eq. (1).  For
+ * query head h, KV head j = h / (n_q_heads / n_kv_heads), and token t of
+ * query chunk c = q_chunk0 + i, the softmax of q.k / sqrt(head_dim) runs over
+ *   - the tokens of the visible closed chunks D_c (sinks and recent window),
+ *   - the valid rows of the routed buffers (slots s with group_idx[i][s] in
+ *     [0, c*chunk/group)),
+ *   - the tokens u <= t of the current chunk c,
+ * and out = sum_u p_u v_u.  lse = natural-log log-sum-exp of the logits.
+ *
+ *   q_rot       [batch, n_q_heads, n_q_chunks*chunk, head_dim] plan dtype
+ *   k_res,v_res resident K/V [batch, n_kv_heads, res_tokens, head_dim].
+ *               res_slot == NULL: chunk c' is at tokens [c'*chunk, ...) and
+ *               (q_chunk0 + n_q_chunks) * chunk <= res_tokens is required.
+ *               res_slot != NULL: device int32 [q_chunk0 + n_q_chunks]; chunk
+ *               c' is at tokens [res_slot[c']*chunk, ...).  Only the entries
+ *               of chunks in D_c and of c itself are read; if one is outside
+ *               [0, res_tokens/chunk) the rows of that query chunk are NaN.
+ *   k_routed, v_routed, group_idx  as produced by hga_gather_kv/route_groups
+ *   out         [batch, n_q_heads, n_q_chunks*chunk, head_dim] plan dtype
+ *   lse         fp32 [batch, n_q_heads, n_q_chunks*chunk] or NULL */
+hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                      int32_t n_q_chunks, const void* k_res, const void* v_res,
+                      int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                      const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                      void* stream);
+
+/* Static description of a status code (never NULL). */
+const char* hga_status_string(int32_t status);
+
+/* Message of the last failing call on the calling thread ("" if none). */
+const char* hga_last_error(void);
+
+/* Library ABI version: (major << 16) | minor. */
+int32_t hga_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HGA_H */

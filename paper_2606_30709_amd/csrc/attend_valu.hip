@@ -1,0 +1,165 @@
+// Exact-token attention (Sec. 3.4, Eq. (1)) in fp32 on the vector ALUs.
+//
+// Used for fp32 inputs, where the dense-matrix cores would need fp32 MFMA
+// with no gain at these sizes.  One wavefront per (batch, query head, query
+// chunk): lane t owns query token t of the chunk and keeps q and the output
+// accumulator in registers.  Key tiles of 16 rows are staged in LDS as fp32
+// (read as broadcasts), and the softmax is the online (running max / running
+// sum) form, rescaled once per tile.
+#include <math.h>
+
+#include "attend_common.hpp"
+#include "hga_internal.hpp"
+
+namespace hga {
+namespace {
+
+constexpr int kTile = 16;
+
+template <int D>
+__global__ __launch_bounds__(64) void attend_valu_kernel(
+    const float* __restrict__ q_rot, int q_chunk0, int n_q_chunks, const float* __restrict__ k_res,
+    const float* __restrict__ v_res, int64_t res_tokens, const int32_t* __restrict__ res_slot,
+    const float* __restrict__ k_routed, const float* __restrict__ v_routed,
+    const int32_t* __restrict__ group_idx, float* __restrict__ out, float* __restrict__ lse,
+    int n_q_heads, int n_kv, int chunk, int group, int keep_first, int window, int topk_groups) {
+    __shared__ float s_k[kTile][D];
+    __shared__ float s_v[kTile][D];
+    __shared__ int s_valid[kTile];
+
+    const int lane = threadIdx.x;
+    const int r = n_q_heads / n_kv;
+    const int i = blockIdx.x / r, hh = blockIdx.x % r;
+    const int bh = blockIdx.y;
+    const int b = bh / n_kv, j = bh % n_kv;
+    const int c = q_chunk0 + i;
+    const int gpc = chunk / group;
+    const int64_t qtok = static_cast<int64_t>(n_q_chunks) * chunk;
+    const int64_t qrow = (static_cast<int64_t>(b) * n_q_heads + j * r + hh) * qtok +
+                         static_cast<int64_t>(i) * chunk + lane;
+    const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
+    const int64_t res_chunks = res_tokens / chunk;
+
+    float q[D], acc[D];
+#pragma unroll
+    for (int e = 0; e < D; ++e) {
+        q[e] = q_rot[qrow * D + e] * scale;
+        acc[e] = 0.f;
+    }
+    float m_run = -INFINITY, l_run = 0.f;
+    bool bad = false;
+
+    const VisibleChunks vis(c, keep_first, window);
+    const int64_t unit = static_cast<int64_t>(bh) * n_q_chunks + i;
+    const int32_t* gi = group_idx + unit * topk_groups;
+    const int routed_rows = topk_groups * group;
+    const int n_vis_tiles = vis.count * (chunk / kTile);
+    const int n_rt_tiles = (routed_rows + kTile - 1) / kTile;
+    const int n_tiles = n_vis_tiles + n_rt_tiles + chunk / kTile;
+
+    for (int tile = 0; tile < n_tiles; ++tile) {
+        // locate this tile's rows
+        const float* ksrc = nullptr;
+        const float* vsrc = nullptr;
+        int kind, row0 = 0;
+        if (tile < n_vis_tiles) {
+            kind = kTileVisible;
+            const int cc = vis.chunk(tile / (chunk / kTile));
+            int64_t slot = res_slot ? res_slot[cc] : cc;
+            if (slot < 0 || slot >= res_chunks) { bad = true; slot = 0; }
+            const int64_t off = (static_cast<int64_t>(bh) * res_tokens + slot * chunk +
+                                 (tile % (chunk / kTile)) * kTile) * D;
+            ksrc = k_res + off;
+            vsrc = v_res + off;
+        } else if (tile < n_vis_tiles + n_rt_tiles) {
+            kind = kTileRouted;
+            row0 = (tile - n_vis_tiles) * kTile;
+            const int64_t off = (unit * routed_rows + row0) * D;
+            ksrc = k_routed + off;
+            vsrc = v_routed + off;
+        } else {
+            kind = kTileCurrent;
+            row0 = (tile - n_vis_tiles - n_rt_tiles) * kTile;
+            int64_t slot = res_slot ? res_slot[c] : c;
+            if (slot < 0 || slot >= res_chunks) { bad = true; slot = 0; }
+            const int64_t off = (static_cast<int64_t>(bh) * res_tokens + slot * chunk + row0) * D;
+            ksrc = k_res + off;
+            vsrc = v_res + off;
+        }
+        __syncthreads();
+        for (int x = lane; x < kTile * D; x += 64) {
+            const int rr = x / D, e = x % D;
+            bool ok = true;
+            if (kind == kTileRouted) {
+                const int row = row0 + rr;
+                ok = row < routed_rows;
+                if (ok) {
+                    const int g = gi[row / group];
+                    ok = g >= 0 && g < c * gpc;
+                }
+            }
+            s_k[rr][e] = ok ? ksrc[rr * D + e] : 0.f;
+            s_v[rr][e] = ok ? vsrc[rr * D + e] : 0.f;
+            if (e == 0) s_valid[rr] = ok;
+        }
+        __syncthreads();
+
+        float s[kTile];
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int kk = 0; kk < kTile; ++kk) {
+            float dot = 0.f;
+#pragma unroll
+            for (int e = 0; e < D; ++e) dot = fmaf(q[e], s_k[kk][e], dot);
+            bool ok = s_valid[kk];
+            if (kind == kTileCurrent) ok = (row0 + kk) <= lane;
+            s[kk] = ok ? dot : -INFINITY;
+            tmax = fmaxf(tmax, s[kk]);
+        }
+        const float m_new = fmaxf(m_run, tmax);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(m_run - m_use);
+        l_run *= alpha;
+#pragma unroll
+        for (int e = 0; e < D; ++e) acc[e] *= alpha;
+#pragma unroll
+        for (int kk = 0; kk < kTile; ++kk) {
+            const float pk = exp2f(s[kk] - m_use);
+            l_run += pk;
+#pragma unroll
+            for (int e = 0; e < D; ++e) acc[e] = fmaf(pk, s_v[kk][e], acc[e]);
+        }
+        m_run = m_new;
+    }
+
+    const float inv = 1.0f / l_run;
+    float* orow = out + qrow * D;
+#pragma unroll
+    for (int e = 0; e < D; ++e) orow[e] = bad ? NAN : acc[e] * inv;
+    if (lse) lse[qrow] = bad ? NAN : (m_run + log2f(l_run)) * 0.6931471805599453f;
+}
+
+}  // namespace
+
+hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                              int n_q_chunks, const void* k_res, const void* v_res,
+                              int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                              const void* v_routed, const int32_t* group_idx, void* out,
+                              float* lse, hipStream_t stream) {
+    const hga_params& p = plan.p;
+    const int r = p.n_q_heads / p.n_kv_heads;
+    dim3 grid(n_q_chunks * r, p.batch * p.n_kv_heads);
+#define HGA_VALU(DD)                                                                            \
+    hipLaunchKernelGGL((attend_valu_kernel<DD>), grid, dim3(64), 0, stream,                     \
+                       static_cast<const float*>(q_rot), q_chunk0, n_q_chunks,                  \
+                       static_cast<const float*>(k_res), static_cast<const float*>(v_res),      \
+                       res_tokens, res_slot, static_cast<const float*>(k_routed),               \
+                       static_cast<const float*>(v_routed), group_idx,                          \
+                       static_cast<float*>(out), lse, p.n_q_heads, p.n_kv_heads, p.chunk,       \
+                       p.group, p.keep_first, recent_window(p), p.topk_groups)
+    if (p.head_dim == 64) HGA_VALU(64); else HGA_VALU(128);
+#undef HGA_VALU
+    return hipGetLastError();
+}
+
+}  // namespace hga

@@ -1,0 +1,346 @@
+// Host side of the C ABI: plan creation, argument validation before any
+// launch, status codes and the per-thread error message.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "hga.h"
+#include "hga_internal.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hga_status fail(hga_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+hga_status hip_fail(hipError_t e, const char* what) {
+    return fail(HGA_EHIP, "%s: %s (%d)", what, hipGetErrorString(e), static_cast<int>(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Pair p is high-frequency for a span when its wavelength 2*pi/theta_p is at
+// most the span (Sec. 3.2 leaves the split open; this is the rule used).
+int high_freq_pairs(int span, int head_dim, double base) {
+    int n = 0;
+    for (int p = 0; p < head_dim / 2; ++p) {
+        const double theta = std::pow(base, -2.0 * p / head_dim);
+        if (2.0 * M_PI / theta <= static_cast<double>(span)) ++n;
+    }
+    return n;
+}
+
+// cos and sin of phi_p(o) = ((span - 1)/2 - o) * theta_p for low-frequency
+// pairs and 0 for high-frequency ones, in double, stored as fp32
+// [2][span][head_dim/2].
+std::vector<float> phase_table(int span, int head_dim, double base, int n_hf) {
+    const int half = head_dim / 2;
+    std::vector<float> t(2 * static_cast<size_t>(span) * half);
+    for (int o = 0; o < span; ++o)
+        for (int p = 0; p < half; ++p) {
+            double phi = 0.0;
+            if (p >= n_hf) phi = ((span - 1) / 2.0 - o) * std::pow(base, -2.0 * p / head_dim);
+            t[static_cast<size_t>(o) * half + p] = static_cast<float>(std::cos(phi));
+            t[static_cast<size_t>(span + o) * half + p] = static_cast<float>(std::sin(phi));
+        }
+    return t;
+}
+
+hga_status validate_params(const hga_params* p) {
+    if (!p) return fail(HGA_EINVAL, "params is NULL");
+    if (p->batch < 1 || p->n_q_heads < 1 || p->n_kv_heads < 1)
+        return fail(HGA_EINVAL, "batch, n_q_heads and n_kv_heads must be >= 1");
+    if (p->n_q_heads % p->n_kv_heads != 0)
+        return fail(HGA_EINVAL, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)",
+                    p->n_q_heads, p->n_kv_heads);
+    if (p->n_q_heads / p->n_kv_heads > 64)
+        return fail(HGA_EUNSUPPORTED, "GQA ratio above 64 is not supported");
+    if (static_cast<int64_t>(p->batch) * p->n_kv_heads > 65535)
+        return fail(HGA_EUNSUPPORTED, "batch * n_kv_heads above 65535 is not supported");
+    if (p->head_dim != 64 && p->head_dim != 128)
+        return fail(HGA_EUNSUPPORTED, "head_dim %d not supported (64 or 128)", p->head_dim);
+    if (p->chunk != 64) return fail(HGA_EUNSUPPORTED, "chunk %d not supported (64)", p->chunk);
+    if (p->group != 8 && p->group != 16 && p->group != 32)
+        return fail(HGA_EUNSUPPORTED, "group %d not supported (8, 16 or 32)", p->group);
+    if (p->keep_first < 0 || p->keep_last < 0)
+        return fail(HGA_EINVAL, "keep_first and keep_last must be >= 0");
+    if (p->force_prev != 0 && p->force_prev != 1)
+        return fail(HGA_EINVAL, "force_prev must be 0 or 1");
+    if (p->topk_chunks < 1 || p->topk_chunks > hga::kMaxTopK)
+        return fail(HGA_EINVAL, "topk_chunks must be in [1, %d]", hga::kMaxTopK);
+    if (p->topk_groups < 1 || p->topk_groups > hga::kMaxTopK)
+        return fail(HGA_EINVAL, "topk_groups must be in [1, %d]", hga::kMaxTopK);
+    if (p->hf_pairs_chunk < -1 || p->hf_pairs_chunk > p->head_dim / 2 ||
+        p->hf_pairs_group < -1 || p->hf_pairs_group > p->head_dim / 2)
+        return fail(HGA_EINVAL, "hf_pairs_* must be -1 or in [0, head_dim/2]");
+    if (p->dtype != HGA_F32 && p->dtype != HGA_BF16)
+        return fail(HGA_EINVAL, "dtype must be HGA_F32 or HGA_BF16");
+    if (!(p->rope_base > 1.0) || !std::isfinite(p->rope_base))
+        return fail(HGA_EINVAL, "rope_base must be finite and > 1");
+    return HGA_OK;
+}
+
+hga_status check_plan(const hga_plan* plan) {
+    if (!plan) return fail(HGA_EINVAL, "plan is NULL");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != plan->device)
+        return fail(HGA_EINVAL, "current device %d is not the plan's device %d", dev, plan->device);
+    return HGA_OK;
+}
+
+hga_status check_tensor(const void* p, const char* name) {
+    if (!p) return fail(HGA_EINVAL, "%s is NULL", name);
+    if (!aligned(p, 16)) return fail(HGA_EALIGN, "%s is not 16-byte aligned", name);
+    return HGA_OK;
+}
+
+hga_status check_index(const void* p, const char* name) {
+    if (!p) return fail(HGA_EINVAL, "%s is NULL", name);
+    if (!aligned(p, 4)) return fail(HGA_EALIGN, "%s is not 4-byte aligned", name);
+    return HGA_OK;
+}
+
+hga_status launched(hipError_t e, const char* what) {
+    if (e != hipSuccess) return hip_fail(e, what);
+    return HGA_OK;
+}
+
+#define HGA_TRY(x)                      \
+    do {                                \
+        hga_status st_ = (x);           \
+        if (st_ != HGA_OK) return st_;  \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int32_t hga_version(void) { return (1 << 16) | 0; }
+
+const char* hga_status_string(int32_t status) {
+    switch (status) {
+        case HGA_OK: return "HGA_OK: success";
+        case HGA_EINVAL: return "HGA_EINVAL: invalid argument";
+        case HGA_EUNSUPPORTED: return "HGA_EUNSUPPORTED: valid but not supported by the kernels";
+        case HGA_EALIGN: return "HGA_EALIGN: misaligned pointer";
+        case HGA_EHIP: return "HGA_EHIP: HIP runtime error";
+        default: return "unknown hga_status";
+    }
+}
+
+const char* hga_last_error(void) { return g_last_error.c_str(); }
+
+hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
+    if (!plan) return fail(HGA_EINVAL, "plan out-pointer is NULL");
+    HGA_TRY(validate_params(params));
+    hga_params p = *params;
+    if (p.hf_pairs_chunk < 0) p.hf_pairs_chunk = high_freq_pairs(p.chunk, p.head_dim, p.rope_base);
+    if (p.hf_pairs_group < 0) p.hf_pairs_group = high_freq_pairs(p.group, p.head_dim, p.rope_base);
+    const std::vector<float> tc = phase_table(p.chunk, p.head_dim, p.rope_base, p.hf_pairs_chunk);
+    const std::vector<float> tg = phase_table(p.group, p.head_dim, p.rope_base, p.hf_pairs_group);
+
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    int max_lds = 0;
+    e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    hga_plan* pl = new (std::nothrow) hga_plan();
+    if (!pl) return fail(HGA_EINVAL, "out of host memory");
+    pl->p = p;
+    pl->device = dev;
+    pl->max_lds = max_lds;
+    float* buf = nullptr;
+    const size_t bytes = (tc.size() + tg.size()) * sizeof(float);
+    e = hipMalloc(&buf, bytes);
+    if (e != hipSuccess) {
+        delete pl;
+        return hip_fail(e, "hipMalloc (phase tables)");
+    }
+    e = hipMemcpy(buf, tc.data(), tc.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(buf + tc.size(), tg.data(), tg.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(buf);
+        delete pl;
+        return hip_fail(e, "hipMemcpy (phase tables)");
+    }
+    pl->phase_chunk = buf;
+    pl->phase_group = buf + tc.size();
+    *plan = pl;
+    return HGA_OK;
+}
+
+hga_status hga_plan_destroy(hga_plan* plan) {
+    if (!plan) return HGA_OK;
+    hipError_t e = hipFree(plan->phase_chunk);
+    delete plan;
+    if (e != hipSuccess) return hip_fail(e, "hipFree (phase tables)");
+    return HGA_OK;
+}
+
+hga_status hga_plan_params(const hga_plan* plan, hga_params* out) {
+    if (!plan || !out) return fail(HGA_EINVAL, "plan or out is NULL");
+    *out = plan->p;
+    return HGA_OK;
+}
+
+hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
+                               int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
+                               float* chunk_sum, float* group_sum, int32_t table_chunks,
+                               void* stream) {
+    HGA_TRY(check_plan(plan));
+    const hga_params& p = plan->p;
+    if (k_tokens < 0 || k_chunk0 < 0 || table_chunks < 0)
+        return fail(HGA_EINVAL, "k_tokens, k_chunk0 and table_chunks must be >= 0");
+    if (chunk_begin < k_chunk0 || chunk_end < chunk_begin || chunk_end > table_chunks)
+        return fail(HGA_EINVAL, "need k_chunk0 <= chunk_begin <= chunk_end <= table_chunks "
+                    "(got %d, %d, %d, %d)", k_chunk0, chunk_begin, chunk_end, table_chunks);
+    if (static_cast<int64_t>(chunk_end - k_chunk0) * p.chunk > k_tokens)
+        return fail(HGA_EINVAL, "chunks up to %d need %lld tokens of k_rot, have %lld", chunk_end,
+                    static_cast<long long>(static_cast<int64_t>(chunk_end - k_chunk0) * p.chunk),
+                    static_cast<long long>(k_tokens));
+    if (chunk_end == chunk_begin) return HGA_OK;
+    HGA_TRY(check_tensor(k_rot, "k_rot"));
+    HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
+    HGA_TRY(check_tensor(group_sum, "group_sum"));
+    return launched(hga::launch_build_summaries(*plan, k_rot, k_tokens, k_chunk0, chunk_begin,
+                                                chunk_end, chunk_sum, group_sum, table_chunks,
+                                                static_cast<hipStream_t>(stream)),
+                    "hga_build_summaries launch");
+}
+
+hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
+                            float* qbar, int32_t* chunk_idx, void* stream) {
+    HGA_TRY(check_plan(plan));
+    const hga_params& p = plan->p;
+    if (q_chunk0 < 0 || n_q_chunks < 0 || table_chunks < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and table_chunks must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    if (static_cast<int64_t>(q_chunk0) + n_q_chunks - 1 > table_chunks)
+        return fail(HGA_EINVAL, "query chunk %d needs summaries of earlier chunks but "
+                    "table_chunks is %d", q_chunk0 + n_q_chunks - 1, table_chunks);
+    const int n_max = hga::middle_count(p, q_chunk0 + n_q_chunks - 1);
+    if (n_max > hga::kMaxChunkCandidates)
+        return fail(HGA_EUNSUPPORTED, "%d middle chunks exceed the %d-candidate limit", n_max,
+                    hga::kMaxChunkCandidates);
+    const int vec = p.dtype == HGA_F32 ? 4 : 8;
+    const size_t head = (sizeof(float) * ((256 / (p.head_dim / vec)) * p.head_dim + p.head_dim) +
+                         sizeof(int) * 2 * p.topk_chunks + 15) & ~size_t(15);
+    if (head + sizeof(uint64_t) * n_max > static_cast<size_t>(plan->max_lds))
+        return fail(HGA_EUNSUPPORTED, "%d middle chunks do not fit the device's %d-byte LDS",
+                    n_max, plan->max_lds);
+    HGA_TRY(check_tensor(q_rot, "q_rot"));
+    HGA_TRY(check_tensor(qbar, "qbar"));
+    HGA_TRY(check_index(chunk_idx, "chunk_idx"));
+    if (n_max > 0) HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
+    return launched(hga::launch_route_chunks(*plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+                                             table_chunks, qbar, chunk_idx,
+                                             static_cast<hipStream_t>(stream)),
+                    "hga_route_chunks launch");
+}
+
+hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32_t* chunk_idx,
+                            int32_t q_chunk0, int32_t n_q_chunks, const float* group_sum,
+                            int32_t table_chunks, int32_t* group_idx, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || table_chunks < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and table_chunks must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_tensor(qbar, "qbar"));
+    HGA_TRY(check_index(chunk_idx, "chunk_idx"));
+    HGA_TRY(check_tensor(group_sum, "group_sum"));
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    return launched(hga::launch_route_groups(*plan, qbar, chunk_idx, q_chunk0, n_q_chunks,
+                                             group_sum, table_chunks, group_idx,
+                                             static_cast<hipStream_t>(stream)),
+                    "hga_route_groups launch");
+}
+
+hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t q_chunk0,
+                         int32_t n_q_chunks, const void* k_src, const void* v_src,
+                         int64_t src_tokens, int32_t src_on_host, void* k_routed,
+                         void* v_routed, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || src_tokens < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and src_tokens must be >= 0");
+    if (src_on_host != 0 && src_on_host != 1) return fail(HGA_EINVAL, "src_on_host must be 0 or 1");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    HGA_TRY(check_tensor(k_src, "k_src"));
+    HGA_TRY(check_tensor(v_src, "v_src"));
+    HGA_TRY(check_tensor(k_routed, "k_routed"));
+    HGA_TRY(check_tensor(v_routed, "v_routed"));
+    const void* ks = k_src;
+    const void* vs = v_src;
+    if (src_on_host) {
+        void* dk = nullptr;
+        void* dv = nullptr;
+        hipError_t e = hipHostGetDevicePointer(&dk, const_cast<void*>(k_src), 0);
+        if (e != hipSuccess)
+            return fail(HGA_EINVAL, "k_src is not a mapped pinned host allocation (%s)",
+                        hipGetErrorString(e));
+        e = hipHostGetDevicePointer(&dv, const_cast<void*>(v_src), 0);
+        if (e != hipSuccess)
+            return fail(HGA_EINVAL, "v_src is not a mapped pinned host allocation (%s)",
+                        hipGetErrorString(e));
+        if (!aligned(dk, 16) || !aligned(dv, 16))
+            return fail(HGA_EALIGN, "mapped host sources are not 16-byte aligned");
+        ks = dk;
+        vs = dv;
+    }
+    return launched(hga::launch_gather_kv(*plan, group_idx, q_chunk0, n_q_chunks, ks, vs,
+                                          src_tokens, k_routed, v_routed,
+                                          static_cast<hipStream_t>(stream)),
+                    "hga_gather_kv launch");
+}
+
+hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                      int32_t n_q_chunks, const void* k_res, const void* v_res,
+                      int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                      const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                      void* stream) {
+    HGA_TRY(check_plan(plan));
+    const hga_params& p = plan->p;
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    if (!res_slot && (static_cast<int64_t>(q_chunk0) + n_q_chunks) * p.chunk > res_tokens)
+        return fail(HGA_EINVAL, "without res_slot the resident K/V must cover chunks up to %d "
+                    "(%lld tokens), have %lld", q_chunk0 + n_q_chunks - 1,
+                    static_cast<long long>((static_cast<int64_t>(q_chunk0) + n_q_chunks) * p.chunk),
+                    static_cast<long long>(res_tokens));
+    if (res_slot && res_tokens < p.chunk)
+        return fail(HGA_EINVAL, "resident buffer holds no full chunk");
+    if (res_slot) HGA_TRY(check_index(res_slot, "res_slot"));
+    HGA_TRY(check_tensor(q_rot, "q_rot"));
+    HGA_TRY(check_tensor(k_res, "k_res"));
+    HGA_TRY(check_tensor(v_res, "v_res"));
+    HGA_TRY(check_tensor(k_routed, "k_routed"));
+    HGA_TRY(check_tensor(v_routed, "v_routed"));
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    HGA_TRY(check_tensor(out, "out"));
+    if (lse && !aligned(lse, 4)) return fail(HGA_EALIGN, "lse is not 4-byte aligned");
+    return launched(hga::launch_attend(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+                                       res_tokens, res_slot, k_routed, v_routed, group_idx, out,
+                                       lse, static_cast<hipStream_t>(stream)),
+                    "hga_attend launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,130 @@
+// Device-side helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hga {
+
+typedef uint16_t bf16_t;  // bfloat16 storage
+
+struct alignas(16) vec16 {  // one 16-byte load/store
+    uint32_t w[4];
+};
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t x) {
+    return __uint_as_float(static_cast<uint32_t>(x) << 16);
+}
+
+// Round-to-nearest-even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<bf16_t>(u >> 16);
+}
+
+// Element type traits: how many elements one 16-byte vector holds and how
+// to widen them to fp32.
+template <typename T> struct elem;
+
+template <> struct elem<float> {
+    static constexpr int kVec = 4;
+    __device__ static __forceinline__ void unpack(const vec16& v, float* out) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) out[e] = __uint_as_float(v.w[e]);
+    }
+    __device__ static __forceinline__ float to_f32(float x) { return x; }
+    __device__ static __forceinline__ float from_f32(float x) { return x; }
+};
+
+template <> struct elem<bf16_t> {
+    static constexpr int kVec = 8;
+    __device__ static __forceinline__ void unpack(const vec16& v, float* out) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            out[2 * e] = __uint_as_float(v.w[e] << 16);
+            out[2 * e + 1] = __uint_as_float(v.w[e] & 0xffff0000u);
+        }
+    }
+    __device__ static __forceinline__ float to_f32(bf16_t x) { return bf16_to_f32(x); }
+    __device__ static __forceinline__ bf16_t from_f32(float x) { return f32_to_bf16(x); }
+};
+
+__device__ __forceinline__ vec16 load16(const void* p) {
+    return *reinterpret_cast<const vec16*>(p);
+}
+
+__device__ __forceinline__ void store16(void* p, const vec16& v) {
+    *reinterpret_cast<vec16*>(p) = v;
+}
+
+// Total order on fp32 scores as unsigned keys; -0 is folded into +0 by the
+// caller (score + 0.0f) so equal scores compare equal.
+__device__ __forceinline__ uint32_t orderable(float s) {
+    uint32_t u = __float_as_uint(s);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Packed selection key: larger score first, then smaller index.
+__device__ __forceinline__ uint64_t select_key(float score, int idx) {
+    return (static_cast<uint64_t>(orderable(score + 0.0f)) << 32) |
+           static_cast<uint64_t>(0xffffffffu - static_cast<uint32_t>(idx));
+}
+
+__device__ __forceinline__ int key_index(uint64_t key) {
+    return static_cast<int>(0xffffffffu - static_cast<uint32_t>(key & 0xffffffffu));
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int mask) {
+    uint32_t lo = __shfl_xor(static_cast<uint32_t>(x), mask, 64);
+    uint32_t hi = __shfl_xor(static_cast<uint32_t>(x >> 32), mask, 64);
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) {
+        uint64_t o = shfl_xor_u64(x, m);
+        x = o > x ? o : x;
+    }
+    return x;
+}
+
+// Top-k selection by one wavefront over `n` packed keys in LDS (keys are
+// never zero; zero marks a taken key).  Writes the k selected indices, in
+// ascending order, to sel[0..k) (LDS).  All 64 lanes of the wave must call.
+__device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, int* scratch) {
+    const int lane = threadIdx.x & 63;
+    uint64_t best = 0;
+    int best_pos = -1;
+    for (int i = lane; i < n; i += 64) {
+        uint64_t v = keys[i];
+        if (v > best) { best = v; best_pos = i; }
+    }
+    for (int round = 0; round < k; ++round) {
+        uint64_t top = wave_max_u64(best);
+        if (best == top && best_pos >= 0) {
+            scratch[round] = key_index(top);
+            keys[best_pos] = 0;
+            best = 0;
+            best_pos = -1;
+            for (int i = lane; i < n; i += 64) {
+                uint64_t v = keys[i];
+                if (v > best) { best = v; best_pos = i; }
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // ascending order: rank of each winner among the k winners
+    for (int i = lane; i < k; i += 64) {
+        int v = scratch[i];
+        int rank = 0;
+        for (int j = 0; j < k; ++j) rank += scratch[j] < v;
+        sel[rank] = v;
+    }
+}
+
+}  // namespace hga

@@ -1,0 +1,57 @@
+// Internal declarations shared by the host ABI and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hga.h"
+
+struct hga_plan {
+    hga_params p;         // resolved: hf_pairs_* filled in
+    int device;
+    int max_lds;          // device limit on LDS bytes per workgroup
+    float* phase_chunk;   // device [2][chunk][head_dim/2]: cos then sin of phi_p(o), span = chunk
+    float* phase_group;   // device [2][group][head_dim/2]: same for span = group
+};
+
+namespace hga {
+
+// Largest candidate lists the routing kernels keep in LDS.
+constexpr int kMaxChunkCandidates = 16384;
+constexpr int kMaxTopK = 512;
+
+// visible-window length W = max(L, force_prev ? 1 : 0)
+inline int recent_window(const hga_params& p) {
+    return p.keep_last > (p.force_prev ? 1 : 0) ? p.keep_last : (p.force_prev ? 1 : 0);
+}
+
+// Number of routable middle chunks of query chunk c: |[F, c - W)|.
+inline int middle_count(const hga_params& p, int c) {
+    int n = c - recent_window(p) - p.keep_first;
+    return n > 0 ? n : 0;
+}
+
+// Kernel launchers; each returns hipSuccess or the launch error.
+hipError_t launch_build_summaries(const hga_plan& plan, const void* k_rot, int64_t k_tokens,
+                                  int k_chunk0, int chunk_begin, int chunk_end, float* chunk_sum,
+                                  float* group_sum, int table_chunks, hipStream_t stream);
+
+hipError_t launch_route_chunks(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                               int n_q_chunks, const float* chunk_sum, int table_chunks,
+                               float* qbar, int32_t* chunk_idx, hipStream_t stream);
+
+hipError_t launch_route_groups(const hga_plan& plan, const float* qbar, const int32_t* chunk_idx,
+                               int q_chunk0, int n_q_chunks, const float* group_sum,
+                               int table_chunks, int32_t* group_idx, hipStream_t stream);
+
+hipError_t launch_gather_kv(const hga_plan& plan, const int32_t* group_idx, int q_chunk0,
+                            int n_q_chunks, const void* k_src, const void* v_src,
+                            int64_t src_tokens, void* k_routed, void* v_routed,
+                            hipStream_t stream);
+
+hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
+                         const void* k_res, const void* v_res, int64_t res_tokens,
+                         const int32_t* res_slot, const void* k_routed, const void* v_routed,
+                         const int32_t* group_idx, void* out, float* lse, hipStream_t stream);
+
+}  // namespace hga

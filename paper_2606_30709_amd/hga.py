@@ -1,0 +1,223 @@
+"""Thin ctypes binding of libhga.so (include/hga.h).
+
+Argument marshalling only: tensors are passed as raw device pointers with the
+sizes read from their shapes, and the stream is torch's current stream unless
+one is given.  Every step of the routed-attention path runs in the library's
+HIP kernels; there is no fallback.  If the library is missing, importing the
+binding's functions raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
+    "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_gather_kv",
+    "hga_attend", "hga_status_string", "hga_last_error", "hga_version",
+    "EXPORTED_SYMBOLS",
+]
+
+F32, BF16 = 0, 1
+_TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
+
+EXPORTED_SYMBOLS = (
+    "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
+    "hga_route_chunks", "hga_route_groups", "hga_gather_kv", "hga_attend",
+    "hga_status_string", "hga_last_error", "hga_version",
+)
+
+
+class HgaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} [status {status}]")
+        self.status = status
+
+
+class HgaParams(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("chunk", ctypes.c_int32), ("group", ctypes.c_int32),
+        ("keep_first", ctypes.c_int32), ("keep_last", ctypes.c_int32),
+        ("force_prev", ctypes.c_int32), ("topk_chunks", ctypes.c_int32),
+        ("topk_groups", ctypes.c_int32), ("hf_pairs_chunk", ctypes.c_int32),
+        ("hf_pairs_group", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("rope_base", ctypes.c_double),
+    ]
+
+
+def library_path() -> str:
+    return os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhga.so")
+
+
+_LIB = None
+
+
+def library() -> ctypes.CDLL:
+    """Load libhga.so (after torch, so both share torch's HIP runtime)."""
+    global _LIB
+    if _LIB is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise ImportError(f"{path} is not built; run `python -m paper_2606_30709_amd.build`")
+        lib = ctypes.CDLL(path)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        sigs = {
+            "hga_plan_create": [ctypes.POINTER(HgaParams), ctypes.POINTER(vp)],
+            "hga_plan_destroy": [vp],
+            "hga_plan_params": [vp, ctypes.POINTER(HgaParams)],
+            "hga_build_summaries": [vp, vp, i64, i32, i32, i32, vp, vp, i32, vp],
+            "hga_route_chunks": [vp, vp, i32, i32, vp, i32, vp, vp, vp],
+            "hga_route_groups": [vp, vp, vp, i32, i32, vp, i32, vp, vp],
+            "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
+            "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
+        }
+        for name, args in sigs.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = i32
+        lib.hga_status_string.argtypes = [i32]
+        lib.hga_status_string.restype = ctypes.c_char_p
+        lib.hga_last_error.argtypes = []
+        lib.hga_last_error.restype = ctypes.c_char_p
+        lib.hga_version.argtypes = []
+        lib.hga_version.restype = i32
+        _LIB = lib
+    return _LIB
+
+
+def hga_status_string(status: int) -> str:
+    return library().hga_status_string(status).decode()
+
+
+def hga_last_error() -> str:
+    return library().hga_last_error().decode()
+
+
+def hga_version() -> int:
+    return library().hga_version()
+
+
+def _check(status: int):
+    if status != 0:
+        raise HgaError(status, f"{hga_status_string(status)}: {hga_last_error()}")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Plan:
+    """Owns an hga_plan (the resolved routing configuration and the summary
+    phase tables on the current device)."""
+
+    def __init__(self, *, batch, n_q_heads, n_kv_heads, head_dim, chunk=64, group=16,
+                 keep_first=1, keep_last=0, force_prev=1, topk_chunks, topk_groups,
+                 hf_pairs_chunk=-1, hf_pairs_group=-1, dtype=BF16, rope_base=10000.0):
+        self._handle = None
+        p = HgaParams(batch, n_q_heads, n_kv_heads, head_dim, chunk, group, keep_first,
+                      keep_last, force_prev, topk_chunks, topk_groups, hf_pairs_chunk,
+                      hf_pairs_group, dtype, float(rope_base))
+        h = ctypes.c_void_p()
+        _check(library().hga_plan_create(ctypes.byref(p), ctypes.byref(h)))
+        self._handle = h
+        out = HgaParams()
+        _check(library().hga_plan_params(h, ctypes.byref(out)))
+        self.params = out
+
+    @classmethod
+    def for_workload(cls, w, **overrides):
+        kw = dict(batch=w.batch, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads,
+                  head_dim=w.head_dim, chunk=w.chunk, group=w.group, keep_first=w.keep_first,
+                  keep_last=w.keep_last, force_prev=w.force_prev, topk_chunks=w.topk_chunks,
+                  topk_groups=w.topk_groups, dtype=F32 if w.dtype == "f32" else BF16,
+                  rope_base=w.rope_base)
+        kw.update(overrides)
+        return cls(**kw)
+
+    @property
+    def handle(self):
+        if self._handle is None:
+            raise RuntimeError("plan is closed")
+        return self._handle
+
+    @property
+    def torch_dtype(self):
+        return _TORCH_DTYPE[self.params.dtype]
+
+    def close(self):
+        if self._handle is not None:
+            h, self._handle = self._handle, None
+            _check(library().hga_plan_destroy(h))
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---------------------------------------------------------------- calls ---
+
+def hga_build_summaries(plan: Plan, k_rot, chunk_begin: int, chunk_end: int, chunk_sum,
+                        group_sum, k_chunk0: int = 0, stream=None):
+    """k_rot [B, Hkv, k_tokens, d]; chunk_sum [B, Hkv, table_chunks, d] fp32;
+    group_sum [B, Hkv, table_chunks*C/G, d] fp32."""
+    _check(library().hga_build_summaries(
+        plan.handle, _ptr(k_rot), k_rot.shape[2], k_chunk0, chunk_begin, chunk_end,
+        _ptr(chunk_sum), _ptr(group_sum), chunk_sum.shape[2], _stream(stream)))
+
+
+def hga_route_chunks(plan: Plan, q_rot, q_chunk0: int, chunk_sum, qbar, chunk_idx, stream=None):
+    """q_rot [B, Hq, n_q_chunks*C, d]; qbar [B, Hkv, n_q_chunks, d] fp32;
+    chunk_idx [B, Hkv, n_q_chunks, K_c] int32."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_route_chunks(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(chunk_sum), chunk_sum.shape[2],
+        _ptr(qbar), _ptr(chunk_idx), _stream(stream)))
+
+
+def hga_route_groups(plan: Plan, qbar, chunk_idx, q_chunk0: int, group_sum, group_idx,
+                     stream=None):
+    """group_sum [B, Hkv, table_chunks*C/G, d] fp32; group_idx [B, Hkv, n_q_chunks, K_g]."""
+    gpc = plan.params.chunk // plan.params.group
+    _check(library().hga_route_groups(
+        plan.handle, _ptr(qbar), _ptr(chunk_idx), q_chunk0, qbar.shape[2], _ptr(group_sum),
+        group_sum.shape[2] // gpc, _ptr(group_idx), _stream(stream)))
+
+
+def hga_gather_kv(plan: Plan, group_idx, q_chunk0: int, k_src, v_src, k_routed, v_routed,
+                  src_on_host: bool = False, stream=None):
+    """k_src/v_src [B, Hkv, src_tokens, d] (device, or pinned host with
+    src_on_host); k_routed/v_routed [B, Hkv, n_q_chunks, K_g*G, d]."""
+    _check(library().hga_gather_kv(
+        plan.handle, _ptr(group_idx), q_chunk0, group_idx.shape[2], _ptr(k_src), _ptr(v_src),
+        k_src.shape[2], int(bool(src_on_host)), _ptr(k_routed), _ptr(v_routed),
+        _stream(stream)))
+
+
+def hga_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v_routed, group_idx,
+               out, lse=None, res_slot=None, stream=None):
+    """q_rot/out [B, Hq, n_q_chunks*C, d]; k_res/v_res [B, Hkv, res_tokens, d];
+    lse [B, Hq, n_q_chunks*C] fp32 or None; res_slot int32 or None."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_attend(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
+        _stream(stream)))

@@ -1,0 +1,163 @@
+"""Device buffers and the five-call sequence for one workload.
+
+``PrefillPipeline``: every token's K/V is resident in device memory; one step
+summarises every chunk, routes every query chunk, gathers the routed groups
+(device to device) and attends.
+
+``DecodePipeline``: the history K/V lives in pinned host memory (the paper's
+RAM-backed cold tier, Sec. 4.3); the device holds the summary tables, the
+always-visible first and recent chunks and the current 64-token block.  One
+step routes the block, gathers only its routed groups over the host link,
+attends, and appends the block's summaries (the store's "append").
+
+Both only allocate with torch and call the binding; all arithmetic runs in
+the HIP library.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import hga
+
+__all__ = ["PrefillPipeline", "DecodePipeline", "to_device"]
+
+
+def to_device(arr: np.ndarray, dtype: str, device="cuda", pin=False) -> torch.Tensor:
+    """Storage array from the workload generator -> torch tensor with the same bytes."""
+    t = torch.from_numpy(np.ascontiguousarray(arr))
+    if dtype == "bf16":
+        t = t.view(torch.bfloat16)
+    if pin:
+        return t.pin_memory()
+    return t.to(device)
+
+
+class PrefillPipeline:
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None):
+        assert not w.decode_block
+        self.w = w
+        self.plan = plan or hga.Plan.for_workload(w)
+        B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
+        nc = w.n_chunks
+        f32, i32 = torch.float32, torch.int32
+        self.q = to_device(inputs["q"], w.dtype, device)
+        self.k = to_device(inputs["k"], w.dtype, device)
+        self.v = to_device(inputs["v"], w.dtype, device)
+        dt = self.q.dtype
+        self.chunk_sum = torch.empty(B, Hkv, nc, d, dtype=f32, device=device)
+        self.group_sum = torch.empty(B, Hkv, nc * (C // G), d, dtype=f32, device=device)
+        self.qbar = torch.empty(B, Hkv, nc, d, dtype=f32, device=device)
+        self.chunk_idx = torch.empty(B, Hkv, nc, w.topk_chunks, dtype=i32, device=device)
+        self.group_idx = torch.empty(B, Hkv, nc, w.topk_groups, dtype=i32, device=device)
+        self.k_routed = torch.empty(B, Hkv, nc, w.topk_groups * G, d, dtype=dt, device=device)
+        self.v_routed = torch.empty_like(self.k_routed)
+        self.out = torch.empty_like(self.q)
+        self.lse = torch.empty(B, w.n_q_heads, w.seq_len, dtype=f32, device=device)
+
+    def summaries(self, stream=None):
+        hga.hga_build_summaries(self.plan, self.k, 0, self.w.n_chunks, self.chunk_sum,
+                                self.group_sum, stream=stream)
+
+    def route(self, stream=None):
+        hga.hga_route_chunks(self.plan, self.q, 0, self.chunk_sum, self.qbar, self.chunk_idx,
+                             stream=stream)
+        hga.hga_route_groups(self.plan, self.qbar, self.chunk_idx, 0, self.group_sum,
+                             self.group_idx, stream=stream)
+
+    def gather(self, stream=None):
+        hga.hga_gather_kv(self.plan, self.group_idx, 0, self.k, self.v, self.k_routed,
+                          self.v_routed, stream=stream)
+
+    def attend(self, stream=None):
+        hga.hga_attend(self.plan, self.q, 0, self.k, self.v, self.k_routed, self.v_routed,
+                       self.group_idx, self.out, self.lse, stream=stream)
+
+    def step(self, stream=None):
+        self.summaries(stream)
+        self.route(stream)
+        self.gather(stream)
+        self.attend(stream)
+
+
+class DecodePipeline:
+    """One query block (the last chunk of the workload) after a host-resident history."""
+
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None):
+        assert w.decode_block
+        self.w = w
+        self.plan = plan or hga.Plan.for_workload(w)
+        B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
+        f32, i32 = torch.float32, torch.int32
+        c = w.q_chunk0                      # the block's chunk id
+        self.c = c
+        hist = c * C
+        k_all = to_device(inputs["k"], w.dtype, "cpu")
+        v_all = to_device(inputs["v"], w.dtype, "cpu")
+        # cold tier: the history in pinned host memory
+        self.k_hist = k_all[:, :, :hist].contiguous().pin_memory()
+        self.v_hist = v_all[:, :, :hist].contiguous().pin_memory()
+        # hot tier: first F chunks, the recent window, then the current block
+        window = max(w.keep_last, 1 if w.force_prev else 0)
+        hot = sorted(set(range(min(w.keep_first, c))) | set(range(max(0, c - window), c)))
+        self.hot_chunks = hot + [c]
+        slot = np.full(c + 1, -1, dtype=np.int32)
+        for s, cc in enumerate(self.hot_chunks):
+            slot[cc] = s
+        self.res_slot = torch.from_numpy(slot).to(device)
+        idx = torch.tensor([t for cc in self.hot_chunks for t in range(cc * C, (cc + 1) * C)])
+        self.k_res = k_all[:, :, idx].contiguous().to(device)
+        self.v_res = v_all[:, :, idx].contiguous().to(device)
+        self.cur_slot = len(hot)
+        dt = self.k_res.dtype
+        self.q = to_device(inputs["q"], w.dtype, device)           # [B, Hq, 64, d]
+        self.table_chunks = c + 1
+        self.chunk_sum = torch.zeros(B, Hkv, c + 1, d, dtype=f32, device=device)
+        self.group_sum = torch.zeros(B, Hkv, (c + 1) * (C // G), d, dtype=f32, device=device)
+        self.qbar = torch.empty(B, Hkv, 1, d, dtype=f32, device=device)
+        self.chunk_idx = torch.empty(B, Hkv, 1, w.topk_chunks, dtype=i32, device=device)
+        self.group_idx = torch.empty(B, Hkv, 1, w.topk_groups, dtype=i32, device=device)
+        self.k_routed = torch.empty(B, Hkv, 1, w.topk_groups * G, d, dtype=dt, device=device)
+        self.v_routed = torch.empty_like(self.k_routed)
+        self.out = torch.empty_like(self.q)
+        self.lse = torch.empty(B, w.n_q_heads, C, dtype=f32, device=device)
+        # The history's summaries were appended as its chunks closed; build
+        # them once here from a transient device copy of the history keys.
+        k_dev = self.k_hist.to(device)
+        hga.hga_build_summaries(self.plan, k_dev, 0, c, self.chunk_sum, self.group_sum)
+        torch.cuda.synchronize()
+        del k_dev
+
+    def pcie_bytes_per_step(self) -> int:
+        """Bytes the gather pulls across the host link: K and V of every valid routed group."""
+        n = int((self.group_idx >= 0).sum().item())
+        return 2 * n * self.w.group * self.w.head_dim * self.w.elem_bytes
+
+    def route(self, stream=None):
+        hga.hga_route_chunks(self.plan, self.q, self.c, self.chunk_sum, self.qbar,
+                             self.chunk_idx, stream=stream)
+        hga.hga_route_groups(self.plan, self.qbar, self.chunk_idx, self.c, self.group_sum,
+                             self.group_idx, stream=stream)
+
+    def gather(self, stream=None):
+        hga.hga_gather_kv(self.plan, self.group_idx, self.c, self.k_hist, self.v_hist,
+                          self.k_routed, self.v_routed, src_on_host=True, stream=stream)
+
+    def attend(self, stream=None):
+        hga.hga_attend(self.plan, self.q, self.c, self.k_res, self.v_res, self.k_routed,
+                       self.v_routed, self.group_idx, self.out, self.lse,
+                       res_slot=self.res_slot, stream=stream)
+
+    def append(self, stream=None):
+        """Summaries of the block's chunk once it closes (store "append")."""
+        # k_res row cur_slot*C is the block's first token: chunk c sits at
+        # chunk offset cur_slot of the resident buffer.
+        hga.hga_build_summaries(self.plan, self.k_res, self.c, self.c + 1, self.chunk_sum,
+                                self.group_sum, k_chunk0=self.c - self.cur_slot, stream=stream)
+
+    def step(self, stream=None):
+        self.route(stream)
+        self.gather(stream)
+        self.attend(stream)
+        self.append(stream)

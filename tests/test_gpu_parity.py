@@ -1,0 +1,413 @@
+"""GPU parity of the HIP path against the float64 oracle, called through the
+C ABI (ctypes binding).  Every stage is compared on the GPU's own upstream
+results (stage isolation): selections bit-exact with lowest-index ties unless
+two candidates are within the fp32 error bound of each other; gathers
+bit-exact; summaries and query means within their fp32 error bounds; outputs
+within max-abs 1e-5 (fp32) / 2e-2 (bf16)."""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import hga_oracle as O  # noqa: E402
+from paper_2606_30709_amd import workloads as W  # noqa: E402
+
+from parity_util import (LSE_TOL, OUT_TOL, SelectionReport, check_selection, f64,  # noqa: E402
+                         score_bounds, summary_bound, tensor_to_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def hga():
+    _need_gpu()
+    from paper_2606_30709_amd import hga as H
+    H.library()
+    return H
+
+
+# ------------------------------------------------------------ workloads ---
+
+def W_(key, **kw):
+    return W.preset(key).with_(**kw)
+
+
+SMALL = {
+    "tiny": W_("tiny"),
+    "smalllm_2k": W_("smalllm", batch=2, seq_len=2048),
+    "train_3k": W_("train12k", batch=2, n_q_heads=4, n_kv_heads=4, seq_len=3072),
+    "qwen_4k": W_("qwen32k", seq_len=4096),
+    "qwen_4k_ragged": W_("qwen32k", seq_len=4096, topk_groups=45, keep_last=3),
+    "qwen_g8": W_("qwen32k", seq_len=2048, n_q_heads=8, n_kv_heads=2, group=8, topk_chunks=6,
+                  topk_groups=21),
+    "qwen_g32": W_("qwen32k", seq_len=2048, n_q_heads=8, n_kv_heads=2, group=32, topk_chunks=6,
+                   topk_groups=7),
+    "mha_d128": W_("qwen32k", seq_len=2048, n_q_heads=4, n_kv_heads=4, topk_chunks=5,
+                   topk_groups=9),
+    "gqa3_d64": W_("smalllm", batch=1, seq_len=2048, n_q_heads=6, n_kv_heads=2, topk_chunks=4,
+                   topk_groups=7, keep_first=2, keep_last=1),
+    "tiny_noforce": W_("tiny", force_prev=0),
+    "f32_d128_gqa": W_("tiny", seq_len=1024, n_q_heads=4, n_kv_heads=2, head_dim=128,
+                       rope_base=1e6, topk_chunks=3, topk_groups=5, keep_last=2),
+}
+
+
+def _oracle_stage_checks(w, inp, pipe, units=None, chunk_ids=None):
+    """Compare every stage of a finished PrefillPipeline with the oracle."""
+    C, G, d = w.chunk, w.group, w.head_dim
+    r = w.gqa_ratio
+    q, k, v = (f64(inp[x], w.dtype) for x in "qkv")
+    nc = w.n_chunks
+    ids = list(range(nc)) if chunk_ids is None else chunk_ids
+    nhc = O.high_freq_pairs(C, d, w.rope_base)
+    nhg = O.high_freq_pairs(G, d, w.rope_base)
+    assert pipe.plan.params.hf_pairs_chunk == nhc and pipe.plan.params.hf_pairs_group == nhg
+
+    # summaries
+    cs = O.summaries(k, C, w.rope_base, nhc)
+    gs = O.summaries(k, G, w.rope_base, nhg)
+    cmag = O.summary_magnitudes(k, C, w.rope_base, nhc)
+    gmag = O.summary_magnitudes(k, G, w.rope_base, nhg)
+    g_cs = tensor_to_f64(pipe.chunk_sum)
+    g_gs = tensor_to_f64(pipe.group_sum)
+    assert np.all(np.abs(g_cs - cs) <= summary_bound(cmag, C) + 1e-30), \
+        f"chunk summaries: max err {np.max(np.abs(g_cs - cs)):.3g}"
+    assert np.all(np.abs(g_gs - gs) <= summary_bound(gmag, G) + 1e-30), \
+        f"group summaries: max err {np.max(np.abs(g_gs - gs)):.3g}"
+
+    # query means
+    qb = O.query_means(q, w.n_kv_heads, C)
+    qmag = O.query_magnitudes(q, w.n_kv_heads, C)
+    g_qb = tensor_to_f64(pipe.qbar)
+    assert np.all(np.abs(g_qb - qb) <= 2 * (r * C + 8) * 2.0 ** -24 * qmag + 1e-30), \
+        f"qbar: max err {np.max(np.abs(g_qb - qb)):.3g}"
+
+    # chunk routing (oracle on exact inputs; near-tie rule)
+    g_ci = pipe.chunk_idx.cpu().numpy()
+    rep_c = SelectionReport()
+    for c in ids:
+        _, M = O.visibility(c, w.keep_first, w.keep_last, w.force_prev)
+        for b in range(w.batch):
+            for j in range(w.n_kv_heads):
+                if not M:
+                    assert np.all(g_ci[b, j, c] == -1)
+                    continue
+                sc = cs[b, j, M] @ qb[b, j, c]
+                eps = score_bounds(qb[b, j, c], cs[b, j, M], qmag[b, j, c], cmag[b, j, M],
+                                   C, r * C, d)
+                check_selection(g_ci[b, j, c], M, sc, eps, w.topk_chunks, rep_c,
+                                f"chunk_idx[{b},{j},{c}]")
+    # group routing on the GPU's chunk selection
+    g_gi = pipe.group_idx.cpu().numpy()
+    rep_g = SelectionReport()
+    gpc = C // G
+    for c in ids:
+        for b in range(w.batch):
+            for j in range(w.n_kv_heads):
+                chunks = [int(x) for x in g_ci[b, j, c] if x >= 0]
+                if not chunks:
+                    assert np.all(g_gi[b, j, c] == -1)
+                    continue
+                cand = np.array([cc * gpc + t for cc in chunks for t in range(gpc)])
+                sc = gs[b, j, cand] @ qb[b, j, c]
+                eps = score_bounds(qb[b, j, c], gs[b, j, cand], qmag[b, j, c], gmag[b, j, cand],
+                                   G, r * C, d)
+                check_selection(g_gi[b, j, c], cand, sc, eps, w.topk_groups, rep_g,
+                                f"group_idx[{b},{j},{c}]")
+    _say(f"  {w.key}: chunk selections {rep_c}, group selections {rep_g}")
+
+    # gather: bit-exact on the GPU's group selection
+    kb = inp["k"]
+    vb = inp["v"]
+    sel = [(b, j, c) for b in range(w.batch) for j in range(w.n_kv_heads) for c in ids]
+    gk = pipe.k_routed.cpu()
+    gv = pipe.v_routed.cpu()
+    if w.dtype == "bf16":
+        gk, gv = gk.view(torch.int16).numpy().view(np.uint16), gv.view(torch.int16).numpy().view(np.uint16)
+    else:
+        gk, gv = gk.numpy(), gv.numpy()
+    for (b, j, c) in sel:
+        for s, g in enumerate(g_gi[b, j, c]):
+            rows_k = gk[b, j, c, s * G:(s + 1) * G]
+            rows_v = gv[b, j, c, s * G:(s + 1) * G]
+            if g < 0:
+                assert not np.any(rows_k) and not np.any(rows_v)
+            else:
+                assert np.array_equal(rows_k, kb[b, j, g * G:(g + 1) * G])
+                assert np.array_equal(rows_v, vb[b, j, g * G:(g + 1) * G])
+
+    # attention on the GPU's group selection
+    if units is None:
+        units = [(b, j, c) for b in range(w.batch) for j in range(w.n_kv_heads) for c in ids]
+    out, lse = O.attend(q, k, v, g_gi, list(range(nc)), C, G, w.keep_first, w.keep_last,
+                        w.force_prev, units=units)
+    g_out = tensor_to_f64(pipe.out)
+    g_lse = tensor_to_f64(pipe.lse)
+    worst_o = worst_l = 0.0
+    for (b, j, c) in units:
+        hs = slice(j * r, (j + 1) * r)
+        ts = slice(c * C, (c + 1) * C)
+        eo = np.max(np.abs(g_out[b, hs, ts] - out[b, hs, ts]))
+        el = np.max(np.abs(g_lse[b, hs, ts] - lse[b, hs, ts]))
+        worst_o, worst_l = max(worst_o, eo), max(worst_l, el)
+    _say(f"  {w.key}: out max-abs {worst_o:.3g} (tol {OUT_TOL[w.dtype]}), "
+         f"lse max-abs {worst_l:.3g} (tol {LSE_TOL[w.dtype]})")
+    assert worst_o <= OUT_TOL[w.dtype]
+    assert worst_l <= LSE_TOL[w.dtype]
+    return rep_c, rep_g
+
+
+@pytest.mark.parametrize("key", list(SMALL))
+def test_prefill_parity_small(hga, key):
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SMALL[key]
+    _say(f"[parity] {key}: B{w.batch} H{w.n_q_heads}/{w.n_kv_heads} d{w.head_dim} N{w.seq_len} "
+         f"{w.dtype} G{w.group} Kc{w.topk_chunks} Kg{w.topk_groups} F{w.keep_first} L{w.keep_last}")
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    for t in (pipe.out, pipe.lse, pipe.chunk_sum, pipe.group_sum, pipe.qbar):
+        t.fill_(float("nan"))
+    pipe.chunk_idx.fill_(-7)
+    pipe.group_idx.fill_(-7)
+    pipe.step()
+    torch.cuda.synchronize()
+    assert not torch.isnan(pipe.out).any() and not torch.isnan(pipe.lse).any()
+    _oracle_stage_checks(w, inp, pipe)
+
+
+def test_planted_needles_routed_on_gpu(hga):
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SMALL["smalllm_2k"]
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    pipe.step()
+    ci = pipe.chunk_idx.cpu().numpy()
+    for b, kc, qc in inp["needles"]:
+        assert all(kc in ci[b, j, qc] for j in range(w.n_kv_heads))
+
+
+def test_determinism_bitwise(hga):
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SMALL["qwen_4k"]
+    pipe = PrefillPipeline(w, W.generate(w))
+    pipe.step()
+    first = [t.clone() for t in (pipe.chunk_sum, pipe.group_sum, pipe.qbar, pipe.chunk_idx,
+                                 pipe.group_idx, pipe.k_routed, pipe.v_routed, pipe.out, pipe.lse)]
+    pipe.step()
+    second = (pipe.chunk_sum, pipe.group_sum, pipe.qbar, pipe.chunk_idx, pipe.group_idx,
+              pipe.k_routed, pipe.v_routed, pipe.out, pipe.lse)
+    for a, b in zip(first, second):
+        assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
+
+
+# ----------------------------------------------------------------- decode ---
+
+def _decode_check(hga, w):
+    from paper_2606_30709_amd.pipeline import DecodePipeline
+    inp = W.generate(w)
+    pipe = DecodePipeline(w, inp)
+    pipe.out.fill_(float("nan"))
+    pipe.step()
+    torch.cuda.synchronize()
+    C, G, d, r = w.chunk, w.group, w.head_dim, w.gqa_ratio
+    c = w.q_chunk0
+    q, k, v = (f64(inp[x], w.dtype) for x in "qkv")
+    nhc = O.high_freq_pairs(C, d, w.rope_base)
+    nhg = O.high_freq_pairs(G, d, w.rope_base)
+    cs = O.summaries(k, C, w.rope_base, nhc)
+    gs = O.summaries(k, G, w.rope_base, nhg)
+    cmag = O.summary_magnitudes(k, C, w.rope_base, nhc)
+    gmag = O.summary_magnitudes(k, G, w.rope_base, nhg)
+    qb = O.query_means(q, w.n_kv_heads, C)
+    qmag = O.query_magnitudes(q, w.n_kv_heads, C)
+    # summaries of the history and of the appended block
+    g_cs = tensor_to_f64(pipe.chunk_sum)
+    assert np.all(np.abs(g_cs - cs) <= summary_bound(cmag, C) + 1e-30)
+    g_gs = tensor_to_f64(pipe.group_sum)
+    assert np.all(np.abs(g_gs - gs) <= summary_bound(gmag, G) + 1e-30)
+    _, M = O.visibility(c, w.keep_first, w.keep_last, w.force_prev)
+    g_ci = pipe.chunk_idx.cpu().numpy()
+    g_gi = pipe.group_idx.cpu().numpy()
+    rc, rg = SelectionReport(), SelectionReport()
+    gpc = C // G
+    for b in range(w.batch):
+        for j in range(w.n_kv_heads):
+            sc = cs[b, j, M] @ qb[b, j, 0]
+            eps = score_bounds(qb[b, j, 0], cs[b, j, M], qmag[b, j, 0], cmag[b, j, M], C, r * C, d)
+            check_selection(g_ci[b, j, 0], M, sc, eps, w.topk_chunks, rc, f"decode chunk {b},{j}")
+            chunks = [int(x) for x in g_ci[b, j, 0] if x >= 0]
+            cand = np.array([cc * gpc + t for cc in chunks for t in range(gpc)])
+            sc = gs[b, j, cand] @ qb[b, j, 0]
+            eps = score_bounds(qb[b, j, 0], gs[b, j, cand], qmag[b, j, 0], gmag[b, j, cand],
+                               G, r * C, d)
+            check_selection(g_gi[b, j, 0], cand, sc, eps, w.topk_groups, rg, f"decode group {b},{j}")
+    out, lse = O.attend(q, k, v, g_gi, [c], C, G, w.keep_first, w.keep_last, w.force_prev)
+    eo = np.max(np.abs(tensor_to_f64(pipe.out) - out))
+    el = np.max(np.abs(tensor_to_f64(pipe.lse) - lse))
+    _say(f"  decode {w.key} N{w.seq_len}: {rc} {rg} out {eo:.3g} lse {el:.3g} "
+         f"pcie bytes {pipe.pcie_bytes_per_step()}")
+    assert eo <= OUT_TOL[w.dtype] and el <= LSE_TOL[w.dtype]
+    # needles at the configured depths are routed for every KV head
+    for kc, _ in inp["needles"]:
+        if kc in M:
+            assert all(kc in g_ci[0, j, 0] for j in range(w.n_kv_heads)), f"needle {kc} missed"
+    return pipe
+
+
+def test_decode_block_parity_reduced(hga):
+    w = W_("decode64k", seq_len=8192 + 64, needle_depths=(12, 64, 115))
+    _decode_check(hga, w)
+
+
+def test_decode_block_parity_full(hga):
+    pipe = _decode_check(hga, W.preset("decode64k"))
+    # host-sourced gather equals a device-sourced gather of the same history
+    kd, vd = pipe.k_hist.to("cuda"), pipe.v_hist.to("cuda")
+    k2, v2 = torch.empty_like(pipe.k_routed), torch.empty_like(pipe.v_routed)
+    hga.hga_gather_kv(pipe.plan, pipe.group_idx, pipe.c, kd, vd, k2, v2)
+    torch.cuda.synchronize()
+    assert torch.equal(k2.view(torch.int16), pipe.k_routed.view(torch.int16))
+    assert torch.equal(v2.view(torch.int16), pipe.v_routed.view(torch.int16))
+
+
+# -------------------------------------------------------------- full size ---
+
+@pytest.mark.parametrize("key", ["smalllm", "train12k", "qwen32k"])
+def test_prefill_parity_full_size_sampled(hga, key):
+    """Full sizes, launched exactly as the benchmark does; the oracle checks
+    every summary and query mean, the routing of sampled query chunks, and
+    the attention of sampled units."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = W.preset(key)
+    _say(f"[full] {key}")
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    pipe.out.fill_(float("nan"))
+    pipe.step()
+    torch.cuda.synchronize()
+    assert not torch.isnan(pipe.out).any()
+    rng = np.random.default_rng(5)
+    nc = w.n_chunks
+    chunk_ids = sorted(set([0, 1, 2, 3, nc - 1] + list(rng.choice(nc, 6, replace=False))))
+    units = [(int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads)), c) for c in chunk_ids]
+    _oracle_stage_checks(w, inp, pipe, units=units, chunk_ids=chunk_ids)
+
+
+# ------------------------------------------------------------- edge cases ---
+
+def test_argument_errors_launch_nothing(hga):
+    w = SMALL["tiny"]
+    plan = hga.Plan.for_workload(w)
+    dev = "cuda"
+    k = torch.zeros(1, 1, 1024, 64, device=dev)
+    cs = torch.zeros(1, 1, 16, 64, device=dev)
+    gs = torch.zeros(1, 1, 64, 64, device=dev)
+    with pytest.raises(hga.HgaError) as e:
+        hga.hga_build_summaries(plan, k, 0, 17, cs, gs)          # beyond table
+    assert e.value.status == -1
+    with pytest.raises(hga.HgaError):
+        hga.hga_build_summaries(plan, k[:, :, :512], 0, 16, cs, gs)   # K too short
+    lib = hga.library()
+    st = lib.hga_build_summaries(plan.handle, k.data_ptr() + 4, 1024, 0, 0, 16, cs.data_ptr(),
+                                 gs.data_ptr(), 16, None)
+    assert st == -3                                              # misaligned
+    st = lib.hga_route_chunks(plan.handle, None, 0, 16, cs.data_ptr(), 16, cs.data_ptr(),
+                              cs.data_ptr(), None)
+    assert st == -1
+    q = torch.zeros(1, 1, 1024, 64, device=dev)
+    st = lib.hga_route_chunks(plan.handle, q.data_ptr(), 5, 16, cs.data_ptr(), 16,
+                              cs.data_ptr(), cs.data_ptr(), None)
+    assert st == -1                                              # needs table of 20 chunks
+    st = lib.hga_attend(plan.handle, q.data_ptr(), 0, 16, k.data_ptr(), k.data_ptr(), 512, None,
+                        k.data_ptr(), k.data_ptr(), cs.data_ptr(), q.data_ptr(), None, None)
+    assert st == -1                                              # resident K/V too short
+    host = torch.zeros(1, 1, 1024, 64)                           # pageable host memory
+    gi = torch.zeros(1, 1, 16, 4, dtype=torch.int32, device=dev)
+    kr = torch.zeros(1, 1, 16, 64, 64, device=dev)
+    st = lib.hga_gather_kv(plan.handle, gi.data_ptr(), 0, 16, host.data_ptr(), host.data_ptr(),
+                           1024, 1, kr.data_ptr(), kr.data_ptr(), None)
+    assert st == -1
+    assert "pinned" in hga.hga_last_error()
+    # empty ranges are no-ops
+    hga.hga_build_summaries(plan, k, 3, 3, cs, gs)
+    torch.cuda.synchronize()
+
+
+def test_gather_and_attend_handle_invalid_slots(hga):
+    """-1 and out-of-range group ids give zero rows in the gather and are
+    skipped by attention; an invalid resident slot poisons its rows."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SMALL["qwen_g8"]
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    pipe.step()
+    gi = pipe.group_idx.clone()
+    c = w.n_chunks - 1
+    gi[0, 0, c, 3] = -1
+    gi[0, 1, c, 5] = 10 ** 6         # beyond the causal past
+    pipe.group_idx.copy_(gi)
+    pipe.gather()
+    pipe.attend()
+    torch.cuda.synchronize()
+    G = w.group
+    assert not pipe.k_routed[0, 0, c, 3 * G:4 * G].any()
+    assert not pipe.v_routed[0, 1, c, 5 * G:6 * G].any()
+    q, k, v = (f64(inp[x], w.dtype) for x in "qkv")
+    gnp = gi.cpu().numpy()
+    units = [(0, 0, c), (0, 1, c)]
+    out, _ = O.attend(q, k, v, gnp, list(range(w.n_chunks)), w.chunk, G, w.keep_first,
+                      w.keep_last, w.force_prev, units=units)
+    g_out = tensor_to_f64(pipe.out)
+    r = w.gqa_ratio
+    for (b, j, cc) in units:
+        sl = (b, slice(j * r, (j + 1) * r), slice(cc * 64, (cc + 1) * 64))
+        assert np.max(np.abs(g_out[sl] - out[sl])) <= OUT_TOL[w.dtype]
+    # resident-slot indirection: identity map equals no map; an invalid slot gives NaN rows
+    slot = torch.arange(w.n_chunks, dtype=torch.int32, device="cuda")
+    out2 = torch.empty_like(pipe.out)
+    hga.hga_attend(pipe.plan, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
+                   pipe.group_idx, out2, None, res_slot=slot)
+    torch.cuda.synchronize()
+    assert torch.equal(out2.view(torch.int16), pipe.out.view(torch.int16))
+    slot[c] = 999
+    hga.hga_attend(pipe.plan, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
+                   pipe.group_idx, out2, None, res_slot=slot)
+    torch.cuda.synchronize()
+    assert torch.isnan(out2[:, :, c * 64:(c + 1) * 64]).all()
+    assert not torch.isnan(out2[:, :, :c * 64]).any()
+
+
+def test_incremental_summaries_equal_bulk(hga):
+    """Appending chunk by chunk (the store's append) equals one bulk build."""
+    w = SMALL["qwen_4k"]
+    inp = W.generate(w)
+    from paper_2606_30709_amd.pipeline import to_device
+    k = to_device(inp["k"], w.dtype)
+    plan = hga.Plan.for_workload(w)
+    nc = w.n_chunks
+    shape_c = (w.batch, w.n_kv_heads, nc, w.head_dim)
+    shape_g = (w.batch, w.n_kv_heads, nc * 4, w.head_dim)
+    a_c, a_g = torch.zeros(shape_c, device="cuda"), torch.zeros(shape_g, device="cuda")
+    b_c, b_g = torch.zeros(shape_c, device="cuda"), torch.zeros(shape_g, device="cuda")
+    hga.hga_build_summaries(plan, k, 0, nc, a_c, a_g)
+    for c in range(nc):
+        blk = k[:, :, c * 64:(c + 1) * 64].contiguous()
+        hga.hga_build_summaries(plan, blk, c, c + 1, b_c, b_g, k_chunk0=c)
+    torch.cuda.synchronize()
+    assert torch.equal(a_c, b_c) and torch.equal(a_g, b_g)
