@@ -47,9 +47,11 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + \
-        sorted(glob.glob(os.path.join(CSRC, "*.cpp")))
+def build(verbose: bool = False, src_dir: str = CSRC, out: str = LIB,
+          defines: tuple = ()) -> str:
+    """Compile every source of ``src_dir`` and link ``out``."""
+    srcs = sorted(glob.glob(os.path.join(src_dir, "*.hip"))) + \
+        sorted(glob.glob(os.path.join(src_dir, "*.cpp")))
     tlib = torch_lib_dir()
     hip_rt = os.path.join(tlib, "libamdhip64.so")
     if not os.path.exists(hip_rt):
@@ -61,24 +63,25 @@ def build(verbose: bool = False) -> str:
         for s in srcs:
             o = os.path.join(tmp, os.path.basename(s) + ".o")
             lang = ["-x", "hip"] if s.endswith(".hip") else []
-            cmd = [HIPCC] + CXXFLAGS + lang + ["-c", s, "-o", o]
+            cmd = [HIPCC] + CXXFLAGS + ["-I", src_dir] + [f"-D{d}" for d in defines] + \
+                lang + ["-c", s, "-o", o]
             procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE,
                                                 stderr=subprocess.STDOUT, text=True)))
             objs.append(o)
         for cmd, p in procs:
-            out, _ = p.communicate()
-            out = "\n".join(l for l in out.splitlines() if "packed-fp32-ops" not in l)
+            log, _ = p.communicate()
+            log = "\n".join(l for l in log.splitlines() if "packed-fp32-ops" not in l)
             if p.returncode != 0:
-                raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{out}")
-            if verbose and out.strip():
-                print(out)
-        tmp_lib = LIB + ".tmp"
+                raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{log}")
+            if verbose and log.strip():
+                print(log)
+        tmp_lib = out + ".tmp"
         _run(["g++", "-shared", "-o", tmp_lib] + objs +
              [hip_rt, f"-Wl,-rpath,{tlib}", "-Wl,--no-undefined", "-Wl,-z,defs"])
-        os.replace(tmp_lib, LIB)
+        os.replace(tmp_lib, out)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":

@@ -120,6 +120,11 @@ hga_status launched(hipError_t e, const char* what) {
     return HGA_OK;
 }
 
+// A launch reports its error through hipGetLastError(), which also returns
+// errors that earlier, unrelated runtime calls on this thread left behind;
+// clear those first so a launch is charged only with its own failure.
+void clear_stale_error() { (void)hipGetLastError(); }
+
 #define HGA_TRY(x)                      \
     do {                                \
         hga_status st_ = (x);           \
@@ -219,6 +224,7 @@ hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t 
     HGA_TRY(check_tensor(k_rot, "k_rot"));
     HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
     HGA_TRY(check_tensor(group_sum, "group_sum"));
+    clear_stale_error();
     return launched(hga::launch_build_summaries(*plan, k_rot, k_tokens, k_chunk0, chunk_begin,
                                                 chunk_end, chunk_sum, group_sum, table_chunks,
                                                 static_cast<hipStream_t>(stream)),
@@ -250,6 +256,7 @@ hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_c
     HGA_TRY(check_tensor(qbar, "qbar"));
     HGA_TRY(check_index(chunk_idx, "chunk_idx"));
     if (n_max > 0) HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
+    clear_stale_error();
     return launched(hga::launch_route_chunks(*plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
                                              table_chunks, qbar, chunk_idx,
                                              static_cast<hipStream_t>(stream)),
@@ -267,6 +274,7 @@ hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32
     HGA_TRY(check_index(chunk_idx, "chunk_idx"));
     HGA_TRY(check_tensor(group_sum, "group_sum"));
     HGA_TRY(check_index(group_idx, "group_idx"));
+    clear_stale_error();
     return launched(hga::launch_route_groups(*plan, qbar, chunk_idx, q_chunk0, n_q_chunks,
                                              group_sum, table_chunks, group_idx,
                                              static_cast<hipStream_t>(stream)),
@@ -293,18 +301,23 @@ hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t
         void* dk = nullptr;
         void* dv = nullptr;
         hipError_t e = hipHostGetDevicePointer(&dk, const_cast<void*>(k_src), 0);
-        if (e != hipSuccess)
+        if (e != hipSuccess) {
+            (void)hipGetLastError();  // the failed lookup must not surface at a later launch
             return fail(HGA_EINVAL, "k_src is not a mapped pinned host allocation (%s)",
                         hipGetErrorString(e));
+        }
         e = hipHostGetDevicePointer(&dv, const_cast<void*>(v_src), 0);
-        if (e != hipSuccess)
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
             return fail(HGA_EINVAL, "v_src is not a mapped pinned host allocation (%s)",
                         hipGetErrorString(e));
+        }
         if (!aligned(dk, 16) || !aligned(dv, 16))
             return fail(HGA_EALIGN, "mapped host sources are not 16-byte aligned");
         ks = dk;
         vs = dv;
     }
+    clear_stale_error();
     return launched(hga::launch_gather_kv(*plan, group_idx, q_chunk0, n_q_chunks, ks, vs,
                                           src_tokens, k_routed, v_routed,
                                           static_cast<hipStream_t>(stream)),
@@ -337,6 +350,7 @@ hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
     HGA_TRY(check_index(group_idx, "group_idx"));
     HGA_TRY(check_tensor(out, "out"));
     if (lse && !aligned(lse, 4)) return fail(HGA_EALIGN, "lse is not 4-byte aligned");
+    clear_stale_error();
     return launched(hga::launch_attend(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
                                        res_tokens, res_slot, k_routed, v_routed, group_idx, out,
                                        lse, static_cast<hipStream_t>(stream)),

@@ -59,6 +59,24 @@ __device__ __forceinline__ void store16(void* p, const vec16& v) {
     *reinterpret_cast<vec16*>(p) = v;
 }
 
+// Raw buffer access: a resource descriptor covers [base, base + bytes); a load
+// whose offset falls outside returns zeros without touching memory.  Loads
+// through it never need a branch, so their wait counts stay exact.
+typedef __amdgpu_buffer_rsrc_t buf_rsrc;
+
+__device__ __forceinline__ buf_rsrc make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                             0x00020000);
+}
+
+__device__ __forceinline__ vec16 buf_load16(buf_rsrc r, uint32_t offset) {
+    return __builtin_bit_cast(vec16, __builtin_amdgcn_raw_buffer_load_b128(r, offset, 0, 0));
+}
+
+__device__ __forceinline__ int buf_load_i32(buf_rsrc r, uint32_t offset) {
+    return static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(r, offset, 0, 0));
+}
+
 // Total order on fp32 scores as unsigned keys; -0 is folded into +0 by the
 // caller (score + 0.0f) so equal scores compare equal.
 __device__ __forceinline__ uint32_t orderable(float s) {

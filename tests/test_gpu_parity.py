@@ -370,6 +370,11 @@ def test_gather_and_attend_handle_invalid_slots(hga):
     assert not pipe.v_routed[0, 1, c, 5 * G:6 * G].any()
     q, k, v = (f64(inp[x], w.dtype) for x in "qkv")
     gnp = gi.cpu().numpy()
+    # the C ABI ignores ids outside [0, c * chunk/group) like -1: tell the oracle so
+    gpc = w.chunk // G
+    for cc in range(w.n_chunks):
+        sl = gnp[:, :, cc]
+        sl[(sl < 0) | (sl >= cc * gpc)] = -1
     units = [(0, 0, c), (0, 1, c)]
     out, _ = O.attend(q, k, v, gnp, list(range(w.n_chunks)), w.chunk, G, w.keep_first,
                       w.keep_last, w.force_prev, units=units)
