@@ -72,7 +72,9 @@ typedef enum { HGA_F32 = 0, HGA_BF16 = 1 } hga_dtype;
  *   hf_pairs_chunk  number of high-frequency RoPE pairs for chunk summaries;
  *   hf_pairs_group  ... for group summaries.  -1 selects the rule "pair p is
  *                   high-frequency when its wavelength 2*pi*base^(2p/d) is at
- *                   most the span" (Sec. 3.2 gives no threshold).
+ *                   most the span" (Sec. 3.2 gives no threshold).  The resolved
+ *                   values must satisfy hf_pairs_chunk >= hf_pairs_group (the
+ *                   rule always does; HGA_EUNSUPPORTED otherwise).
  *   dtype           hga_dtype of Q/K/V/routed buffers/output
  *   rope_base       RoPE base (> 1), theta_p = base^(-2p/head_dim)
  *

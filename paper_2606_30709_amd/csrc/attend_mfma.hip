@@ -39,7 +39,6 @@ typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
 constexpr int KT = 64;  // keys per LDS tile (= chunk)
 constexpr int kXcds = 8;
 
@@ -67,9 +66,10 @@ __device__ __forceinline__ i16x4_t lds_read_tr16(const bf16_t* p) {
 }
 
 // D: head dim; KS: wavefronts sharing one query tile (each takes one 32-key
-// half of every key tile); P: key tiles kept in flight in registers.
-template <int D, int KS, int P>
-__global__ __launch_bounds__(kThreads, 2) void attend_mfma_kernel(
+// half of every key tile); P: key tiles kept in flight in registers; NW:
+// wavefronts per workgroup (NW / KS query tiles per workgroup).
+template <int D, int KS, int P, int NW>
+__global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const bf16_t* __restrict__ q_rot, int q_chunk0, int n_q_chunks,
     const bf16_t* __restrict__ k_res, const bf16_t* __restrict__ v_res, int64_t res_tokens,
     const int32_t* __restrict__ res_slot, const bf16_t* __restrict__ k_routed,
@@ -80,8 +80,9 @@ __global__ __launch_bounds__(kThreads, 2) void attend_mfma_kernel(
     constexpr int KSTR = S::KSTR, VSTR = S::VSTR, NDT = S::NDT;
     constexpr int NKS = D / 16;                  // k-steps of Q.K^T
     constexpr int VPR = D / 8;                   // 16-byte vectors per row
+    constexpr int kThreads = NW * 64;
     constexpr int NVEC = KT * VPR / kThreads;    // K (and V) vectors per thread per tile
-    constexpr int QT = 4 / KS;                   // query tiles per workgroup
+    constexpr int QT = NW / KS;                  // query tiles per workgroup
     constexpr int NST = 2 / KS;                  // 32-key sub-tiles per wave per tile
     constexpr uint32_t kRowBytes = D * 2;
 
@@ -127,8 +128,10 @@ __global__ __launch_bounds__(kThreads, 2) void attend_mfma_kernel(
 
     // group ids first: their validity is needed only when routed tiles are staged
     const buf_rsrc g_rsrc = make_rsrc(group_idx + unit * topk_groups, topk_groups * 4);
-    const int gval0 = buf_load_i32(g_rsrc, tid * 4);
-    const int gval1 = buf_load_i32(g_rsrc, (tid + kThreads) * 4);
+    constexpr int NG = 512 / kThreads;           // group-id slots per thread
+    int gval[NG];
+#pragma unroll
+    for (int u = 0; u < NG; ++u) gval[u] = buf_load_i32(g_rsrc, (tid + kThreads * u) * 4);
 
     // this lane's query row and its Q fragments (B operand of S^T = K.Q^T)
     const int qrow_in_unit = qtile * 32 + col;
@@ -189,8 +192,12 @@ __global__ __launch_bounds__(kThreads, 2) void attend_mfma_kernel(
 #pragma unroll
     for (int s = 0; s < P; ++s) fetch(s, kreg[s], vreg[s]);
 
-    if (tid < topk_groups) s_gvalid[tid] = gval0 >= 0 && gval0 < c * gpc;
-    if (tid + kThreads < topk_groups) s_gvalid[tid + kThreads] = gval1 >= 0 && gval1 < c * gpc;
+#pragma unroll
+    for (int u = 0; u < NG; ++u) {
+        const int slot = tid + kThreads * u;
+        if (slot < topk_groups) s_gvalid[slot] = gval[u] >= 0 && gval[u] < c * gpc;
+    }
+
 
     const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
     f32x16_t oacc[NDT];
@@ -329,23 +336,18 @@ __global__ __launch_bounds__(kThreads, 2) void attend_mfma_kernel(
     }
     if (!qactive || ksplit != 0) return;
 
-    const float inv = 1.0f / l_tot;
+    const float inv = bad ? NAN : 1.0f / l_tot;
     bf16_t* orow = out + qrow * D;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             const int d0 = dt * 32 + g4 * 8 + half * 4;
-            uint32_t w0, w1;
-            if (bad) {
-                w0 = w1 = 0x7fc07fc0u;
-            } else {
-                w0 = f32_to_bf16(oacc[dt][g4 * 4 + 0] * inv) |
-                     (static_cast<uint32_t>(f32_to_bf16(oacc[dt][g4 * 4 + 1] * inv)) << 16);
-                w1 = f32_to_bf16(oacc[dt][g4 * 4 + 2] * inv) |
-                     (static_cast<uint32_t>(f32_to_bf16(oacc[dt][g4 * 4 + 3] * inv)) << 16);
-            }
-            *reinterpret_cast<uint2*>(orow + d0) = make_uint2(w0, w1);
+            typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+            bf16x4_t o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(oacc[dt][g4 * 4 + e] * inv);
+            *reinterpret_cast<bf16x4_t*>(orow + d0) = o;
         }
     if (lse && half == 0) lse[qrow] = bad ? NAN : (m_run + log2f(l_tot)) * 0.6931471805599453f;
 }
@@ -360,17 +362,19 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int nqt = 2 * r;
-    const bool split = nqt <= 2;                 // one head: two waves per query tile
-    const int wg_per_unit = split ? 1 : (nqt + 3) / 4;
+    // One head per KV head (two query tiles): a workgroup of two wavefronts,
+    // each with every key of its tile; otherwise four query tiles per group.
+    const bool one_head = nqt <= 2;
+    const int wg_per_unit = one_head ? 1 : (nqt + 3) / 4;
     const int64_t n_blocks64 =
         static_cast<int64_t>(p.batch) * p.n_kv_heads * n_q_chunks * wg_per_unit;
     if (n_blocks64 > (int64_t(1) << 30)) return hipErrorInvalidConfiguration;
     const int n_blocks = static_cast<int>(n_blocks64);
     const int grid = (n_blocks + kXcds - 1) / kXcds * kXcds;
     const int group_shift = p.group == 8 ? 3 : (p.group == 16 ? 4 : 5);
-#define HGA_MFMA(DD, KSV, PV)                                                                    \
-    hipLaunchKernelGGL((attend_mfma_kernel<DD, KSV, PV>), dim3(grid), dim3(kThreads), 0, stream, \
-                       static_cast<const bf16_t*>(q_rot), q_chunk0, n_q_chunks,                  \
+#define HGA_MFMA(DD, KSV, PV, NWV)                                                               \
+    hipLaunchKernelGGL((attend_mfma_kernel<DD, KSV, PV, NWV>), dim3(grid), dim3(NWV * 64), 0,    \
+                       stream, static_cast<const bf16_t*>(q_rot), q_chunk0, n_q_chunks,          \
                        static_cast<const bf16_t*>(k_res), static_cast<const bf16_t*>(v_res),     \
                        res_tokens, res_slot, static_cast<const bf16_t*>(k_routed),               \
                        static_cast<const bf16_t*>(v_routed), group_idx,                          \
@@ -379,9 +383,9 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     // One tile in flight per workgroup: measured faster than deeper register
     // rings, whose extra VGPRs cost more occupancy than they hide latency.
     if (p.head_dim == 64) {
-        if (split) HGA_MFMA(64, 2, 1); else HGA_MFMA(64, 1, 1);
+        if (one_head) HGA_MFMA(64, 2, 1, 4); else HGA_MFMA(64, 1, 1, 4);
     } else {
-        if (split) HGA_MFMA(128, 2, 1); else HGA_MFMA(128, 1, 1);
+        if (one_head) HGA_MFMA(128, 2, 1, 4); else HGA_MFMA(128, 1, 1, 4);
     }
 #undef HGA_MFMA
     return hipGetLastError();

@@ -59,6 +59,21 @@ std::vector<float> phase_table(int span, int head_dim, double base, int n_hf) {
     return t;
 }
 
+// cos and sin of psi_g theta_p, psi_g = (chunk - group)/2 - g*group: the
+// rotation taking group g's middle position to the chunk's middle position
+// (used for the low-frequency chunk pairs), [2][chunk/group][head_dim/2].
+std::vector<float> psi_table(int chunk, int group, int head_dim, double base) {
+    const int half = head_dim / 2, gpc = chunk / group;
+    std::vector<float> t(2 * static_cast<size_t>(gpc) * half);
+    for (int g = 0; g < gpc; ++g)
+        for (int p = 0; p < half; ++p) {
+            const double psi = ((chunk - group) / 2.0 - g * group) * std::pow(base, -2.0 * p / head_dim);
+            t[static_cast<size_t>(g) * half + p] = static_cast<float>(std::cos(psi));
+            t[static_cast<size_t>(gpc + g) * half + p] = static_cast<float>(std::sin(psi));
+        }
+    return t;
+}
+
 hga_status validate_params(const hga_params* p) {
     if (!p) return fail(HGA_EINVAL, "params is NULL");
     if (p->batch < 1 || p->n_q_heads < 1 || p->n_kv_heads < 1)
@@ -156,8 +171,12 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
     hga_params p = *params;
     if (p.hf_pairs_chunk < 0) p.hf_pairs_chunk = high_freq_pairs(p.chunk, p.head_dim, p.rope_base);
     if (p.hf_pairs_group < 0) p.hf_pairs_group = high_freq_pairs(p.group, p.head_dim, p.rope_base);
-    const std::vector<float> tc = phase_table(p.chunk, p.head_dim, p.rope_base, p.hf_pairs_chunk);
+    if (p.hf_pairs_chunk < p.hf_pairs_group)
+        return fail(HGA_EUNSUPPORTED, "hf_pairs_chunk (%d) below hf_pairs_group (%d) is not "
+                    "supported: a high-frequency group pair must be high-frequency for the chunk",
+                    p.hf_pairs_chunk, p.hf_pairs_group);
     const std::vector<float> tg = phase_table(p.group, p.head_dim, p.rope_base, p.hf_pairs_group);
+    const std::vector<float> tc = psi_table(p.chunk, p.group, p.head_dim, p.rope_base);
 
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
@@ -177,23 +196,23 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
         delete pl;
         return hip_fail(e, "hipMalloc (phase tables)");
     }
-    e = hipMemcpy(buf, tc.data(), tc.size() * sizeof(float), hipMemcpyHostToDevice);
+    e = hipMemcpy(buf, tg.data(), tg.size() * sizeof(float), hipMemcpyHostToDevice);
     if (e == hipSuccess)
-        e = hipMemcpy(buf + tc.size(), tg.data(), tg.size() * sizeof(float), hipMemcpyHostToDevice);
+        e = hipMemcpy(buf + tg.size(), tc.data(), tc.size() * sizeof(float), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(buf);
         delete pl;
         return hip_fail(e, "hipMemcpy (phase tables)");
     }
-    pl->phase_chunk = buf;
-    pl->phase_group = buf + tc.size();
+    pl->phase_group = buf;
+    pl->phase_psi = buf + tg.size();
     *plan = pl;
     return HGA_OK;
 }
 
 hga_status hga_plan_destroy(hga_plan* plan) {
     if (!plan) return HGA_OK;
-    hipError_t e = hipFree(plan->phase_chunk);
+    hipError_t e = hipFree(plan->phase_group);
     delete plan;
     if (e != hipSuccess) return hip_fail(e, "hipFree (phase tables)");
     return HGA_OK;
@@ -246,10 +265,7 @@ hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_c
     if (n_max > hga::kMaxChunkCandidates)
         return fail(HGA_EUNSUPPORTED, "%d middle chunks exceed the %d-candidate limit", n_max,
                     hga::kMaxChunkCandidates);
-    const int vec = p.dtype == HGA_F32 ? 4 : 8;
-    const size_t head = (sizeof(float) * ((256 / (p.head_dim / vec)) * p.head_dim + p.head_dim) +
-                         sizeof(int) * 2 * p.topk_chunks + 15) & ~size_t(15);
-    if (head + sizeof(uint64_t) * n_max > static_cast<size_t>(plan->max_lds))
+    if (hga::route_chunks_lds_bytes(*plan, n_max) > static_cast<size_t>(plan->max_lds))
         return fail(HGA_EUNSUPPORTED, "%d middle chunks do not fit the device's %d-byte LDS",
                     n_max, plan->max_lds);
     HGA_TRY(check_tensor(q_rot, "q_rot"));

@@ -10,8 +10,8 @@ struct hga_plan {
     hga_params p;         // resolved: hf_pairs_* filled in
     int device;
     int max_lds;          // device limit on LDS bytes per workgroup
-    float* phase_chunk;   // device [2][chunk][head_dim/2]: cos then sin of phi_p(o), span = chunk
-    float* phase_group;   // device [2][group][head_dim/2]: same for span = group
+    float* phase_group;   // device [2][group][head_dim/2]: cos then sin of phi_p(o), span = group
+    float* phase_psi;     // device [2][chunk/group][head_dim/2]: cos, sin of psi_g theta_p
 };
 
 namespace hga {
@@ -30,6 +30,9 @@ inline int middle_count(const hga_params& p, int c) {
     int n = c - recent_window(p) - p.keep_first;
     return n > 0 ? n : 0;
 }
+
+// LDS one routing wavefront needs for `n_max` middle-chunk candidates.
+size_t route_chunks_lds_bytes(const hga_plan& plan, int n_max);
 
 // Kernel launchers; each returns hipSuccess or the launch error.
 hipError_t launch_build_summaries(const hga_plan& plan, const void* k_rot, int64_t k_tokens,

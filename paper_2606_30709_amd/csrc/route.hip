@@ -1,168 +1,247 @@
 // Content-based routing (Sec. 3.3): query-chunk -> chunk scoring with top-K_c
 // selection, then group refinement with top-K_g selection.
 //
-// One workgroup per (batch, KV head, query chunk).  Scores are fp32 dot
-// products reduced in a fixed order, packed with their candidate id into
-// 64-bit keys (larger score first, then lower id) held in LDS, and one
-// wavefront extracts the top k by repeated wave-wide maxima.  Each lane keeps
-// the best key of its own strided share, so a round costs one wave reduction
-// plus one rescan of the winning lane's share.
+// One wavefront per (batch, KV head, query chunk) unit and up to four units
+// per workgroup, each wave with its own LDS region and no workgroup barrier.
+// Scores are fp32 dot products (coalesced row reads, a fixed DPP row sum),
+// packed with their candidate id into 64-bit keys
+// (larger score first, then lower id) held in LDS, and the wave extracts the top k by repeated wave-wide maxima: each lane
+// keeps the best key of its own strided share, so a round costs one wave
+// reduction plus one rescan of the winning lane's share.
 #include "hga_device.hpp"
 #include "hga_internal.hpp"
 
 namespace hga {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kLanesPerCand = 16;  // lanes cooperating on one dot product
+__device__ __forceinline__ void wave_sync_lds() {
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
 
-// Dot product of the LDS query mean with a global fp32 row of length D, by the
-// 16 lanes of a lane group; every lane of the group returns the sum.
-template <int D>
-__device__ __forceinline__ float group_dot(const float* s_q, const float* row, int part) {
-    constexpr int PER = D / kLanesPerCand;  // 4 or 8 floats per lane
-    float acc = 0.f;
+// x + x from the lane n below within each 16-lane row (lanes below n add 0).
+template <int kCtrl>
+__device__ __forceinline__ float add_row_shr(float x) {
+    return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, true));
+}
+
+// Scores of 64 candidates by one wavefront, coalesced: the 16 lanes of row
+// g = lane/16 read the rows of candidates 16g .. 16g+15, one table row per
+// instruction (lane p takes float4 p, and p+16 for D = 128), form partial
+// dot products with q_bar (broadcast from LDS), and a DPP prefix sum over the
+// row (shifts 1, 2, 4, 8) leaves each candidate's complete score in lane 15
+// of the row.  The summation order is fixed, so scores are bit-reproducible.
+// Lane 15 of each row writes the keys of its 16 candidates; row_of(k) gives
+// the table row (and candidate id) of the batch's k-th candidate, valid(k)
+// whether it exists.
+template <int D, typename RowOf>
+__device__ __forceinline__ void batch_keys(const float* s_q, const float* table, RowOf row_of,
+                                           int n_valid, uint64_t* keys) {
+    constexpr int F4 = D / 64;  // float4 per lane per row
+    const int lane = threadIdx.x & 63;
+    const int grp = lane >> 4, p = lane & 15;
+    float4 qv[F4];
 #pragma unroll
-    for (int v = 0; v < PER / 4; ++v) {
-        const float4 x = *reinterpret_cast<const float4*>(row + part * PER + v * 4);
-        const float* q = s_q + part * PER + v * 4;
-        acc = fmaf(q[0], x.x, acc);
-        acc = fmaf(q[1], x.y, acc);
-        acc = fmaf(q[2], x.z, acc);
-        acc = fmaf(q[3], x.w, acc);
+    for (int f = 0; f < F4; ++f) qv[f] = *reinterpret_cast<const float4*>(s_q + (p + 16 * f) * 4);
+    float part[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        const float* row = table + static_cast<int64_t>(row_of(grp * 16 + k)) * D;
+        float a = 0.f;
+#pragma unroll
+        for (int f = 0; f < F4; ++f) {
+            const float4 x = *reinterpret_cast<const float4*>(row + (p + 16 * f) * 4);
+            a = fmaf(qv[f].x, x.x, a);
+            a = fmaf(qv[f].y, x.y, a);
+            a = fmaf(qv[f].z, x.z, a);
+            a = fmaf(qv[f].w, x.w, a);
+        }
+        part[k] = a;
     }
 #pragma unroll
-    for (int m = kLanesPerCand / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
-    return acc;
+    for (int k = 0; k < 16; ++k) {
+        float x = part[k];
+        x = add_row_shr<0x111>(x);  // row_shr:1
+        x = add_row_shr<0x112>(x);  // row_shr:2
+        x = add_row_shr<0x114>(x);  // row_shr:4
+        x = add_row_shr<0x118>(x);  // row_shr:8
+        part[k] = x;
+    }
+    if (p == 15) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const int m = grp * 16 + k;
+            if (m < n_valid) keys[m] = select_key(part[k], row_of(m));
+        }
+    }
+}
+
+// Per-wave LDS carve-up, 16-byte aligned pieces.
+struct WaveLds {
+    float* q;        // [D]
+    int* list;       // [n_list]
+    int* sel;        // [topk]
+    int* scr;        // [topk]
+    uint64_t* keys;  // [n_keys]
+};
+
+__host__ __device__ inline size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
+
+__host__ __device__ inline size_t wave_lds_bytes(int d, int n_list, int topk, int n_keys) {
+    return align16(sizeof(float) * d) + align16(sizeof(int) * n_list) +
+           2 * align16(sizeof(int) * topk) + align16(sizeof(uint64_t) * (n_keys > 0 ? n_keys : 1));
+}
+
+__device__ inline WaveLds carve(unsigned char* base, int d, int n_list, int topk) {
+    WaveLds w;
+    size_t off = 0;
+    w.q = reinterpret_cast<float*>(base + off);
+    off += align16(sizeof(float) * d);
+    w.list = reinterpret_cast<int*>(base + off);
+    off += align16(sizeof(int) * n_list);
+    w.sel = reinterpret_cast<int*>(base + off);
+    off += align16(sizeof(int) * topk);
+    w.scr = reinterpret_cast<int*>(base + off);
+    off += align16(sizeof(int) * topk);
+    w.keys = reinterpret_cast<uint64_t*>(base + off);
+    return w;
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void route_chunks_kernel(
+__global__ __launch_bounds__(256) void route_chunks_kernel(
     const T* __restrict__ q_rot, int q_chunk0, int n_q_chunks, const float* __restrict__ chunk_sum,
     int table_chunks, float* __restrict__ qbar, int32_t* __restrict__ chunk_idx, int n_q_heads,
-    int n_kv, int chunk, int keep_first, int window, int topk) {
+    int n_kv, int n_units, int keep_first, int window, int topk, size_t wave_bytes) {
+    constexpr int chunk = 64;
     constexpr int V = elem<T>::kVec;
     constexpr int VPR = D / V;              // 16-byte vectors per row
-    constexpr int NRS = kThreads / VPR;     // row slots
+    constexpr int NRS = 64 / VPR;           // row slots per wave
+    constexpr int UNROLL = 8;
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    float* s_part = reinterpret_cast<float*>(smem_raw);   // [NRS][D]
-    float* s_q = s_part + NRS * D;                        // [D]
-    int* s_sel = reinterpret_cast<int*>(s_q + D);         // [topk]
-    int* s_scr = s_sel + topk;                            // [topk]
-    uint64_t* s_keys = reinterpret_cast<uint64_t*>(
-        smem_raw + ((sizeof(float) * (NRS * D + D) + sizeof(int) * 2 * topk + 15) & ~size_t(15)));
-
-    const int i = blockIdx.x;
-    const int bh = blockIdx.y;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int unit = blockIdx.x * (blockDim.x >> 6) + wave;
+    if (unit >= n_units) return;
+    WaveLds L = carve(smem_raw + wave * wave_bytes, D, 0, topk);
+    const int i = unit % n_q_chunks;
+    const int bh = unit / n_q_chunks;
     const int b = bh / n_kv, j = bh % n_kv;
     const int r = n_q_heads / n_kv;
-    const int tid = threadIdx.x;
     const int c = q_chunk0 + i;
 
     // 1. q_bar: mean over the r heads x chunk tokens, fixed summation order.
-    {
-        const int cv = tid % VPR, rs = tid / VPR;
-        float acc[V];
+    const int cv = lane % VPR, rs = lane / VPR;
+    float acc[V];
 #pragma unroll
-        for (int e = 0; e < V; ++e) acc[e] = 0.f;
-        const int rows = r * chunk;
-        const int64_t qtok = static_cast<int64_t>(n_q_chunks) * chunk;
-        for (int row = rs; row < rows; row += NRS) {
-            const int hh = row / chunk, tt = row % chunk;
-            const T* src = q_rot + ((static_cast<int64_t>(b) * n_q_heads + j * r + hh) * qtok +
-                                    static_cast<int64_t>(i) * chunk + tt) * D + cv * V;
-            float x[V];
-            elem<T>::unpack(load16(src), x);
+    for (int e = 0; e < V; ++e) acc[e] = 0.f;
+    const int rows = r * chunk;
+    const int64_t qtok = static_cast<int64_t>(n_q_chunks) * chunk;
+    const T* qbase = q_rot + ((static_cast<int64_t>(b) * n_q_heads + j * r) * qtok +
+                              static_cast<int64_t>(i) * chunk) * D + cv * V;
+    for (int row0 = rs; row0 < rows; row0 += NRS * UNROLL) {
+        vec16 x[UNROLL];
 #pragma unroll
-            for (int e = 0; e < V; ++e) acc[e] += x[e];
+        for (int u = 0; u < UNROLL; ++u) {
+            const int row = row0 + u * NRS;
+            const int hh = row >> 6, tt = row & 63;
+            x[u] = row < rows ? load16(qbase + (hh * qtok + tt) * D) : vec16{{0u, 0u, 0u, 0u}};
         }
 #pragma unroll
-        for (int e = 0; e < V; ++e) s_part[rs * D + cv * V + e] = acc[e];
+        for (int u = 0; u < UNROLL; ++u) {
+            float f[V];
+            elem<T>::unpack(x[u], f);
+#pragma unroll
+            for (int e = 0; e < V; ++e) acc[e] += f[e];
+        }
     }
-    __syncthreads();
-    if (tid < D) {
-        float s = 0.f;
-        for (int rs = 0; rs < NRS; ++rs) s += s_part[rs * D + tid];
-        s *= 1.0f / static_cast<float>(r * chunk);
-        s_q[tid] = s;
-        qbar[(static_cast<int64_t>(bh) * n_q_chunks + i) * D + tid] = s;
+#pragma unroll
+    for (int m = VPR; m < 64; m <<= 1)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[e] += __shfl_xor(acc[e], m, 64);
+    const float inv = 1.0f / static_cast<float>(rows);
+    if (rs == 0) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) L.q[cv * V + e] = acc[e] * inv;
     }
-    __syncthreads();
+    wave_sync_lds();
+    if (lane < VPR) {
+        float* out = qbar + static_cast<int64_t>(unit) * D + cv * V;
+#pragma unroll
+        for (int e = 0; e < V; ++e) out[e] = L.q[cv * V + e];
+    }
 
     // 2. score the middle chunks [keep_first, c - window).
     int n = c - window - keep_first;
     if (n < 0) n = 0;
     const float* table = chunk_sum + static_cast<int64_t>(bh) * table_chunks * D;
-    {
-        const int part = tid % kLanesPerCand;
-        for (int m = tid / kLanesPerCand; m < n; m += kThreads / kLanesPerCand) {
-            const int cand = keep_first + m;
-            const float s = group_dot<D>(s_q, table + static_cast<int64_t>(cand) * D, part);
-            if (part == 0) s_keys[m] = select_key(s, cand);
-        }
+    for (int m0 = 0; m0 < n; m0 += 64) {
+        const int last = n - 1 - m0;
+        batch_keys<D>(L.q, table, [&](int k) { return keep_first + m0 + min(k, last); }, n - m0,
+                      L.keys + m0);
     }
-    __syncthreads();
+    wave_sync_lds();
 
-    // 3. top-k by wave 0, ascending, -1 padded.
-    if (tid < 64) {
-        const int k = n < topk ? n : topk;
-        wave_select_topk(s_keys, n, k, s_sel, s_scr);
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        int32_t* out = chunk_idx + (static_cast<int64_t>(bh) * n_q_chunks + i) * topk;
-        for (int t = tid; t < topk; t += 64) out[t] = t < k ? s_sel[t] : -1;
-    }
+    // 3. top-k, ascending, -1 padded.
+    const int k = n < topk ? n : topk;
+    wave_select_topk(L.keys, n, k, L.sel, L.scr);
+    wave_sync_lds();
+    int32_t* out = chunk_idx + static_cast<int64_t>(unit) * topk;
+    for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void route_groups_kernel(
+__global__ __launch_bounds__(256) void route_groups_kernel(
     const float* __restrict__ qbar, const int32_t* __restrict__ chunk_idx, int q_chunk0,
     int n_q_chunks, const float* __restrict__ group_sum, int table_chunks,
-    int32_t* __restrict__ group_idx, int topk_chunks, int topk_groups, int gpc) {
+    int32_t* __restrict__ group_idx, int n_units, int topk_chunks, int topk_groups, int gpc_shift,
+    size_t wave_bytes) {
+    const int gpc = 1 << gpc_shift;
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    float* s_q = reinterpret_cast<float*>(smem_raw);      // [D]
-    int* s_chunks = reinterpret_cast<int*>(s_q + D);      // [topk_chunks]
-    int* s_sel = s_chunks + topk_chunks;                  // [topk_groups]
-    int* s_scr = s_sel + topk_groups;                     // [topk_groups]
-    int* s_nvalid = s_scr + topk_groups;                  // [1]
-    uint64_t* s_keys = reinterpret_cast<uint64_t*>(
-        smem_raw + ((sizeof(float) * D + sizeof(int) * (topk_chunks + 2 * topk_groups + 1) + 15) &
-                    ~size_t(15)));
-
-    const int i = blockIdx.x;
-    const int bh = blockIdx.y;
-    const int tid = threadIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int unit = blockIdx.x * (blockDim.x >> 6) + wave;
+    if (unit >= n_units) return;
+    WaveLds L = carve(smem_raw + wave * wave_bytes, D, topk_chunks, topk_groups);
+    const int i = unit % n_q_chunks;
+    const int bh = unit / n_q_chunks;
     const int c = q_chunk0 + i;
     const int limit = c < table_chunks ? c : table_chunks;
 
-    if (tid < D) s_q[tid] = qbar[(static_cast<int64_t>(bh) * n_q_chunks + i) * D + tid];
-    if (tid == 0) {
-        const int32_t* row = chunk_idx + (static_cast<int64_t>(bh) * n_q_chunks + i) * topk_chunks;
-        int nv = 0;
-        for (int t = 0; t < topk_chunks; ++t) {
-            const int cc = row[t];
-            if (cc >= 0 && cc < limit) s_chunks[nv++] = cc;
-        }
-        *s_nvalid = nv;
+    for (int x = lane; x < D; x += 64) L.q[x] = qbar[static_cast<int64_t>(unit) * D + x];
+    // valid chunk ids in order (a wave-wide compaction by ballot)
+    const int32_t* row = chunk_idx + static_cast<int64_t>(unit) * topk_chunks;
+    int nv = 0;
+    for (int t0 = 0; t0 < topk_chunks; t0 += 64) {
+        const int t = t0 + lane;
+        const int cc = t < topk_chunks ? row[t] : -1;
+        const bool ok = cc >= 0 && cc < limit;
+        const uint64_t mask = __ballot(ok);
+        const int pos = nv + __popcll(mask & ((uint64_t(1) << lane) - 1));
+        if (ok) L.list[pos] = cc;
+        nv += __popcll(mask);
     }
-    __syncthreads();
-    const int n = *s_nvalid * gpc;
+    wave_sync_lds();
+
+    const int n = nv * gpc;
     const float* table = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
-    {
-        const int part = tid % kLanesPerCand;
-        for (int m = tid / kLanesPerCand; m < n; m += kThreads / kLanesPerCand) {
-            const int g = s_chunks[m / gpc] * gpc + m % gpc;
-            const float s = group_dot<D>(s_q, table + static_cast<int64_t>(g) * D, part);
-            if (part == 0) s_keys[m] = select_key(s, g);
-        }
+    for (int m0 = 0; m0 < n; m0 += 64) {
+        const int last = n - 1 - m0;
+        auto row_of = [&](int k) {
+            const int mm = m0 + min(k, last);
+            return L.list[mm >> gpc_shift] * gpc + (mm & (gpc - 1));
+        };
+        batch_keys<D>(L.q, table, row_of, n - m0, L.keys + m0);
     }
-    __syncthreads();
-    if (tid < 64) {
-        const int k = n < topk_groups ? n : topk_groups;
-        wave_select_topk(s_keys, n, k, s_sel, s_scr);
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        int32_t* out = group_idx + (static_cast<int64_t>(bh) * n_q_chunks + i) * topk_groups;
-        for (int t = tid; t < topk_groups; t += 64) out[t] = t < k ? s_sel[t] : -1;
-    }
+    wave_sync_lds();
+    const int k = n < topk_groups ? n : topk_groups;
+    wave_select_topk(L.keys, n, k, L.sel, L.scr);
+    wave_sync_lds();
+    int32_t* out = group_idx + static_cast<int64_t>(unit) * topk_groups;
+    for (int t = lane; t < topk_groups; t += 64) out[t] = t < k ? L.sel[t] : -1;
+}
+
+// Up to four waves per workgroup, as many as the LDS budget allows.
+int waves_per_block(size_t wave_bytes, int max_lds) {
+    int w = static_cast<int>(static_cast<size_t>(max_lds) / wave_bytes);
+    return w < 1 ? 1 : (w > 4 ? 4 : w);
 }
 
 template <typename T, int D>
@@ -170,18 +249,15 @@ hipError_t launch_chunks_t(const hga_plan& plan, const void* q_rot, int q_chunk0
                            const float* chunk_sum, int table_chunks, float* qbar,
                            int32_t* chunk_idx, hipStream_t stream) {
     const hga_params& p = plan.p;
-    constexpr int V = elem<T>::kVec;
-    constexpr int NRS = kThreads / (D / V);
-    const int window = recent_window(p);
     const int n_max = middle_count(p, q_chunk0 + n_q_chunks - 1);
-    const size_t head = (sizeof(float) * (NRS * D + D) + sizeof(int) * 2 * p.topk_chunks + 15) &
-                        ~size_t(15);
-    const size_t lds = head + sizeof(uint64_t) * (n_max > 0 ? n_max : 1);
-    dim3 grid(n_q_chunks, p.batch * p.n_kv_heads);
-    hipLaunchKernelGGL((route_chunks_kernel<T, D>), grid, dim3(kThreads), lds, stream,
+    const size_t wb = wave_lds_bytes(D, 0, p.topk_chunks, n_max);
+    const int wpb = waves_per_block(wb, plan.max_lds);
+    const int n_units = p.batch * p.n_kv_heads * n_q_chunks;
+    const int blocks = (n_units + wpb - 1) / wpb;
+    hipLaunchKernelGGL((route_chunks_kernel<T, D>), dim3(blocks), dim3(64 * wpb), wb * wpb, stream,
                        static_cast<const T*>(q_rot), q_chunk0, n_q_chunks, chunk_sum,
-                       table_chunks, qbar, chunk_idx, p.n_q_heads, p.n_kv_heads, p.chunk,
-                       p.keep_first, window, p.topk_chunks);
+                       table_chunks, qbar, chunk_idx, p.n_q_heads, p.n_kv_heads, n_units,
+                       p.keep_first, recent_window(p), p.topk_chunks, wb);
     return hipGetLastError();
 }
 
@@ -191,17 +267,21 @@ hipError_t launch_groups_t(const hga_plan& plan, const float* qbar, const int32_
                            int32_t* group_idx, hipStream_t stream) {
     const hga_params& p = plan.p;
     const int gpc = p.chunk / p.group;
-    const size_t head = (sizeof(float) * D + sizeof(int) * (p.topk_chunks + 2 * p.topk_groups + 1) +
-                         15) & ~size_t(15);
-    const size_t lds = head + sizeof(uint64_t) * p.topk_chunks * gpc;
-    dim3 grid(n_q_chunks, p.batch * p.n_kv_heads);
-    hipLaunchKernelGGL((route_groups_kernel<D>), grid, dim3(kThreads), lds, stream, qbar,
-                       chunk_idx, q_chunk0, n_q_chunks, group_sum, table_chunks, group_idx,
-                       p.topk_chunks, p.topk_groups, gpc);
+    const size_t wb = wave_lds_bytes(D, p.topk_chunks, p.topk_groups, p.topk_chunks * gpc);
+    const int wpb = waves_per_block(wb, plan.max_lds);
+    const int n_units = p.batch * p.n_kv_heads * n_q_chunks;
+    const int blocks = (n_units + wpb - 1) / wpb;
+    hipLaunchKernelGGL((route_groups_kernel<D>), dim3(blocks), dim3(64 * wpb), wb * wpb, stream,
+                       qbar, chunk_idx, q_chunk0, n_q_chunks, group_sum, table_chunks, group_idx,
+                       n_units, p.topk_chunks, p.topk_groups, gpc == 8 ? 3 : (gpc == 4 ? 2 : 1), wb);
     return hipGetLastError();
 }
 
 }  // namespace
+
+size_t route_chunks_lds_bytes(const hga_plan& plan, int n_max) {
+    return wave_lds_bytes(plan.p.head_dim, 0, plan.p.topk_chunks, n_max);
+}
 
 hipError_t launch_route_chunks(const hga_plan& plan, const void* q_rot, int q_chunk0,
                                int n_q_chunks, const float* chunk_sum, int table_chunks,

@@ -1,15 +1,24 @@
 // Mixed-RoPE chunk and group key summaries (Sec. 3.2).
 //
-// One thread owns one (chunk, group, pair-block): a pair-block is the
-// 16 bytes of dimensions [pb*V, pb*V + V) together with their rotate-half
-// partners [D/2 + pb*V, ...), V = 16 / sizeof(element).  It walks the
-// group's tokens in order, accumulating in fp32 both the group summary and
-// its share of the chunk summary:
-//   first half  += cos(phi) a - sin(phi) b
-//   second half += sin(phi) a + cos(phi) b
-// with the span's phase phi_p(o) read from LDS copies of the plan's tables.
-// The group share is final; the chunk shares of the chunk's groups are added
-// in group order through LDS.  The kernel is bound by the single read of K.
+// For a pair p of a span starting at token s, the summary adds
+// R(phi_p(o)) k_rot[s + o] over the span (then divides by its length), with
+// phi_p(o) = 0 for high-frequency pairs and ((span-1)/2 - o) theta_p for the
+// others.  With C = chunk and G = group, a chunk is gpc = C/G groups, and for
+// a low-frequency pair the chunk phase of token o = g*G + o' splits as
+//   ((C-1)/2 - o) theta_p = psi_g theta_p + ((G-1)/2 - o') theta_p,
+//   psi_g = (C - G)/2 - g*G,
+// so the chunk sum is the sum over its groups of R(psi_g theta_p) times the
+// group sum (an identity of rotations).  High-frequency chunk pairs are plain
+// sums of the rotated keys.  This needs every high-frequency group pair to be
+// a high-frequency chunk pair, which the wavelength rule guarantees (the plan
+// rejects other settings).
+//
+// Layout of the work: one wavefront per chunk.  Lane (pb, ts) owns the
+// pair-block pb (eight dimensions [8 pb, 8 pb + 8) and their rotate-half
+// partners) of the consecutive tokens of slice ts.  Every lane issues all
+// its loads at once, accumulates its slice, pre-rotates the chunk share by its
+// group's psi_g, and the slices are added in a fixed order through LDS.  The
+// group phase table and the psi table live in LDS.
 #include "hga_device.hpp"
 #include "hga_internal.hpp"
 
@@ -17,90 +26,128 @@ namespace hga {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+template <typename T, int D>
+struct SumGeom {
+    static constexpr int V = 8;                     // pairs per lane (a pair-block)
+    static constexpr int LV = elem<T>::kVec;        // elements per 16-byte load
+    static constexpr int VPH = V / LV;              // loads per half pair-block
+    static constexpr int HALF = D / 2;
+    static constexpr int NPB = HALF / V;            // pair-blocks per token
+    static constexpr int TPL = NPB;                 // tokens per lane (64 lanes per chunk)
+    static constexpr int SLICES = 64 / NPB;         // token slices per chunk
+};
 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void build_summaries_kernel(
     const T* __restrict__ k_rot, int64_t k_tokens, int k_chunk0, int chunk_begin, int n_chunks,
-    float* __restrict__ chunk_sum, float* __restrict__ group_sum, int table_chunks, int n_kv,
-    const float* __restrict__ phase_chunk, const float* __restrict__ phase_group, int chunk,
-    int group) {
-    constexpr int V = elem<T>::kVec;
-    constexpr int HALF = D / 2;
-    constexpr int NPB = HALF / V;  // pair-blocks per token
-    extern __shared__ float smem[];
-    float* s_pc = smem;                       // [2][chunk][HALF]
-    float* s_pg = s_pc + 2 * chunk * HALF;    // [2][group][HALF]
-    float* s_red = s_pg + 2 * group * HALF;   // [chunks_per_block][gpc][D]
+    float* __restrict__ chunk_sum, float* __restrict__ group_sum, int table_chunks, int n_bh,
+    const float* __restrict__ phase_group, const float* __restrict__ phase_psi, int group,
+    int hf_chunk) {
+    using Gm = SumGeom<T, D>;
+    constexpr int V = Gm::V, LV = Gm::LV, VPH = Gm::VPH, HALF = Gm::HALF, NPB = Gm::NPB,
+                  TPL = Gm::TPL, SLICES = Gm::SLICES;
+    constexpr int C = 64;
+    // LDS rows padded by 4 words so lanes reading or writing the same column
+    // of different rows hit different banks.
+    constexpr int PH = HALF + 4;                   // phase-table row stride
+    constexpr int RD = D + 4;                      // reduction row stride
+    extern __shared__ __align__(16) float smem[];
+    const int gpc = C / group;
+    float* s_pg = smem;                            // [2][group][PH]
+    float* s_psi = s_pg + 2 * group * PH;          // [2][gpc][PH]
+    float* s_red = s_psi + 2 * gpc * PH;           // [kWaves][2][SLICES][RD]
 
-    const int gpc = chunk / group;
-    const int tpc = NPB * gpc;              // threads per chunk
-    const int cpb = kThreads / tpc;         // chunks per block
-    const int bh = blockIdx.y;              // b * n_kv + j
     const int tid = threadIdx.x;
-
-    for (int i = tid; i < 2 * chunk * HALF; i += kThreads) s_pc[i] = phase_chunk[i];
-    for (int i = tid; i < 2 * group * HALF; i += kThreads) s_pg[i] = phase_group[i];
+    for (int x = tid; x < 2 * group * HALF; x += kThreads) s_pg[(x / HALF) * PH + x % HALF] = phase_group[x];
+    for (int x = tid; x < 2 * gpc * HALF; x += kThreads) s_psi[(x / HALF) * PH + x % HALF] = phase_psi[x];
     __syncthreads();
 
-    const int local = tid / tpc;
-    const int grp = (tid % tpc) / NPB;
-    const int pb = tid % NPB;
-    const int c_rel = blockIdx.x * cpb + local;   // chunk index within the range
-    const bool active = local < cpb && c_rel < n_chunks;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int pb = lane % NPB, ts = lane / NPB;
+    const int o0 = ts * TPL;                       // first token of the slice
+    const int g = o0 / group;                      // its group (a slice lies in one group)
+    float* red = s_red + wave * 2 * SLICES * RD;
+    const int64_t total = static_cast<int64_t>(n_bh) * n_chunks;
 
-    float ca[V], cb[V], ga[V], gb[V];
+    for (int64_t item0 = static_cast<int64_t>(blockIdx.x) * kWaves; item0 < total;
+         item0 += static_cast<int64_t>(gridDim.x) * kWaves) {
+        const int64_t item = item0 + wave;
+        const bool active = item < total;
+        const int bh = active ? static_cast<int>(item / n_chunks) : 0;
+        const int c = chunk_begin + (active ? static_cast<int>(item % n_chunks) : 0);
+        const T* src = k_rot + (static_cast<int64_t>(bh) * k_tokens +
+                                static_cast<int64_t>(c - k_chunk0) * C + o0) * D;
+        vec16 ra[TPL][VPH], rb[TPL][VPH];
+        if (active) {
 #pragma unroll
-    for (int e = 0; e < V; ++e) ca[e] = cb[e] = ga[e] = gb[e] = 0.f;
-
-    const int c = chunk_begin + c_rel;
-    if (active) {
-        const T* base = k_rot + (static_cast<int64_t>(bh) * k_tokens +
-                                 static_cast<int64_t>(c - k_chunk0) * chunk + grp * group) * D;
-        for (int o2 = 0; o2 < group; ++o2) {
-            const int o = grp * group + o2;
-            float a[V], b[V];
-            elem<T>::unpack(load16(base + o2 * D + pb * V), a);
-            elem<T>::unpack(load16(base + o2 * D + HALF + pb * V), b);
-            const float* pcc = s_pc + o * HALF + pb * V;
-            const float* pcs = s_pc + chunk * HALF + o * HALF + pb * V;
-            const float* pgc = s_pg + o2 * HALF + pb * V;
-            const float* pgs = s_pg + group * HALF + o2 * HALF + pb * V;
+            for (int u = 0; u < TPL; ++u)
 #pragma unroll
-            for (int e = 0; e < V; ++e) {
-                ca[e] += pcc[e] * a[e] - pcs[e] * b[e];
-                cb[e] += pcs[e] * a[e] + pcc[e] * b[e];
-                ga[e] += pgc[e] * a[e] - pgs[e] * b[e];
-                gb[e] += pgs[e] * a[e] + pgc[e] * b[e];
+                for (int h = 0; h < VPH; ++h) {
+                    ra[u][h] = load16(src + u * D + pb * V + h * LV);
+                    rb[u][h] = load16(src + u * D + HALF + pb * V + h * LV);
+                }
+        }
+        float ga[V], gb[V], pa[V], pbv[V];
+#pragma unroll
+        for (int e = 0; e < V; ++e) ga[e] = gb[e] = pa[e] = pbv[e] = 0.f;
+        if (active) {
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                float a[V], b[V];
+#pragma unroll
+                for (int h = 0; h < VPH; ++h) {
+                    elem<T>::unpack(ra[u][h], a + h * LV);
+                    elem<T>::unpack(rb[u][h], b + h * LV);
+                }
+                const int o2 = (o0 + u) & (group - 1);
+                const float* pc = s_pg + o2 * PH + pb * V;
+                const float* ps = s_pg + (group + o2) * PH + pb * V;
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    ga[e] += pc[e] * a[e] - ps[e] * b[e];
+                    gb[e] += ps[e] * a[e] + pc[e] * b[e];
+                    pa[e] += a[e];
+                    pbv[e] += b[e];
+                }
             }
         }
-        const float inv_g = 1.0f / static_cast<float>(group);
-        float* gout = group_sum + (static_cast<int64_t>(bh) * table_chunks * gpc +
-                                   static_cast<int64_t>(c) * gpc + grp) * D;
+        // slice shares: [0] group sum, [1] chunk sum (rotated by psi_g, or plain
+        // for high-frequency chunk pairs)
+        const float* qc = s_psi + g * PH + pb * V;
+        const float* qs = s_psi + (gpc + g) * PH + pb * V;
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-            gout[pb * V + e] = ga[e] * inv_g;
-            gout[HALF + pb * V + e] = gb[e] * inv_g;
+            const int p = pb * V + e;
+            red[ts * RD + p] = ga[e];
+            red[ts * RD + HALF + p] = gb[e];
+            const bool hf = p < hf_chunk;
+            red[(SLICES + ts) * RD + p] = hf ? pa[e] : qc[e] * ga[e] - qs[e] * gb[e];
+            red[(SLICES + ts) * RD + HALF + p] = hf ? pbv[e] : qs[e] * ga[e] + qc[e] * gb[e];
         }
-        float* red = s_red + (local * gpc + grp) * D;
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-            red[pb * V + e] = ca[e];
-            red[HALF + pb * V + e] = cb[e];
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        if (active) {
+            const int spg = group / TPL;  // slices per group
+            const float inv_g = 1.0f / static_cast<float>(group);
+            float* gout = group_sum + (static_cast<int64_t>(bh) * table_chunks + c) * gpc * D;
+            for (int x = lane; x < gpc * D; x += 64) {
+                const int gg = x / D, dim = x % D;
+                float s = 0.f;
+                for (int k = 0; k < spg; ++k) s += red[(gg * spg + k) * RD + dim];
+                gout[x] = s * inv_g;
+            }
+            const float inv_c = 1.0f / static_cast<float>(C);
+            float* cout_ = chunk_sum + (static_cast<int64_t>(bh) * table_chunks + c) * D;
+            for (int dim = lane; dim < D; dim += 64) {
+                float s = 0.f;
+                for (int k = 0; k < SLICES; ++k) s += red[(SLICES + k) * RD + dim];
+                cout_[dim] = s * inv_c;
+            }
         }
-    }
-    __syncthreads();
-    // chunk summary: add the groups' shares in group order, one thread per
-    // (chunk, dimension).
-    const float inv_c = 1.0f / static_cast<float>(chunk);
-    for (int i = tid; i < cpb * D; i += kThreads) {
-        const int l = i / D, dim = i % D;
-        const int cr = blockIdx.x * cpb + l;
-        if (cr >= n_chunks) continue;
-        const float* red = s_red + l * gpc * D + dim;
-        float s = 0.f;
-        for (int g = 0; g < gpc; ++g) s += red[g * D];
-        chunk_sum[(static_cast<int64_t>(bh) * table_chunks + chunk_begin + cr) * D + dim] =
-            s * inv_c;
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
 }
 
@@ -108,20 +155,20 @@ template <typename T, int D>
 hipError_t launch_t(const hga_plan& plan, const void* k_rot, int64_t k_tokens, int k_chunk0,
                     int chunk_begin, int chunk_end, float* chunk_sum, float* group_sum,
                     int table_chunks, hipStream_t stream) {
+    using Gm = SumGeom<T, D>;
     const hga_params& p = plan.p;
-    constexpr int V = elem<T>::kVec;
-    constexpr int NPB = (D / 2) / V;
     const int gpc = p.chunk / p.group;
-    const int tpc = NPB * gpc;
-    const int cpb = kThreads / tpc;
     const int n_chunks = chunk_end - chunk_begin;
-    dim3 grid((n_chunks + cpb - 1) / cpb, p.batch * p.n_kv_heads);
-    const size_t lds = sizeof(float) * (2 * p.chunk * (D / 2) + 2 * p.group * (D / 2) +
-                                        cpb * gpc * D);
-    hipLaunchKernelGGL((build_summaries_kernel<T, D>), grid, dim3(kThreads), lds, stream,
-                       static_cast<const T*>(k_rot), k_tokens, k_chunk0, chunk_begin, n_chunks,
-                       chunk_sum, group_sum, table_chunks, p.n_kv_heads, plan.phase_chunk,
-                       plan.phase_group, p.chunk, p.group);
+    const int n_bh = p.batch * p.n_kv_heads;
+    const int64_t items = static_cast<int64_t>(n_bh) * n_chunks;
+    int64_t blocks = (items + kWaves - 1) / kWaves;
+    if (blocks > 4096) blocks = 4096;
+    const size_t lds = sizeof(float) * (2 * p.group * (Gm::HALF + 4) + 2 * gpc * (Gm::HALF + 4) +
+                                        kWaves * 2 * Gm::SLICES * (D + 4));
+    hipLaunchKernelGGL((build_summaries_kernel<T, D>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kThreads), lds, stream, static_cast<const T*>(k_rot), k_tokens,
+                       k_chunk0, chunk_begin, n_chunks, chunk_sum, group_sum, table_chunks, n_bh,
+                       plan.phase_group, plan.phase_psi, p.group, p.hf_pairs_chunk);
     return hipGetLastError();
 }
 

@@ -62,6 +62,7 @@ def _params(**kw):
     (dict(rope_base=1.0), -1),
     (dict(rope_base=float("inf")), -1),
     (dict(batch=0), -1),
+    (dict(hf_pairs_chunk=2, hf_pairs_group=5), -2),
 ])
 def test_plan_rejects_bad_params_before_touching_a_device(bad, status):
     lib = hga.library()
