@@ -77,6 +77,59 @@ def attention_flops(w, group_idx: np.ndarray) -> float:
     return 4.0 * d * pairs
 
 
+ATTEND_SOURCES = ("attend_mfma.hip", "attend_common.hpp", "hga_device.hpp", "hga_internal.hpp")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_smalllm_traffic.txt")
+COPY_BYTES = 256 << 20
+
+
+def attend_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in ATTEND_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_30709_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload_key: str):
+    """HBM bytes per attention launch from the committed counter summary, or
+    None when the kernel source changed since the counters were taken."""
+    try:
+        vals = {}
+        with open(TRAFFIC_FILE) as f:
+            for line in f:
+                if "=" in line and not line.lstrip().startswith("#"):
+                    k, v = (x.strip() for x in line.split("=", 1))
+                    vals[k] = v
+        if vals.get("kernel_source_sha256") != attend_source_hash():
+            return None
+        if vals.get("workload") != workload_key:
+            return None
+        return int(float(vals["traffic_bytes_per_launch"]))
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def probe_traffic(w, inp):
+    """For counter collection: the pipeline once, attention 5 times, then 5
+    plain device copies of COPY_BYTES (the calibration for FETCH_SIZE and
+    WRITE_SIZE)."""
+    import torch
+
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    pipe = PrefillPipeline(w, inp)
+    pipe.step()
+    for _ in range(5):
+        pipe.attend()
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"probe": "traffic", "workload": w.key, "copy_bytes": COPY_BYTES,
+                      "kernel_source_sha256": attend_source_hash()}), flush=True)
+
+
 def cpu_baseline(w, inp, max_seconds: float) -> dict:
     """The float64 oracle, as it stands, over the (batch, KV head) units of the
     same workload in order (wrapping around) until max_seconds of CPU work."""
@@ -122,6 +175,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--probe-traffic", action="store_true",
+                    help="run attention and a known-size copy for rocprofv3 --pmc, then exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for "
@@ -141,6 +196,9 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     inp = W.generate(w)
+    if args.probe_traffic:
+        probe_traffic(w, inp)
+        return
     pipe = PrefillPipeline(w, inp)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
@@ -224,7 +282,8 @@ def main():
     achieved = abytes[dominant] / dsec / 1e9
     roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": None, "alg_bytes_per_launch": abytes[dominant],
+                "traffic": measured_traffic(w.key) if dominant == "attend" else None,
+                "alg_bytes_per_launch": abytes[dominant],
                 "mean_launch_us": round(stage_ms[dominant] * 1e3, 2)}
 
     res = {
