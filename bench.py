@@ -3,7 +3,10 @@
 
 One step = the whole hot path over one batch of synthetic input: chunk and
 group summaries, chunk routing, group refinement, gather of the routed K/V,
-and exact attention (five C-ABI calls, inputs already resident in HBM).  The
+and exact attention (inputs already resident in HBM).  The two routing stages
+run as the single call hga_route (four C-ABI calls per step);
+--separate-route issues hga_route_chunks and hga_route_groups instead (five
+calls, bit-identical indices).  The
 default workload is the SmallLM-shaped prefill (B4, 8/8 heads, d64, 8192
 tokens, bf16, C64 G16, first chunk hot, K_c 3, K_g 4 -> 3.125% of the
 context fetched by the last chunk).
@@ -12,7 +15,7 @@ Prints one JSON line.  The step rate comes from an event-free timed loop
 (wall clock between synchronizations); HIP events on the launch stream
 bracket the dominant kernel (attention) in every timed step, and its
 algorithmic bytes over its mean duration give the roofline entry.  A second
-pass with events between all five calls gives the per-stage breakdown.
+pass with events between all calls gives the per-stage breakdown.
 The float64 oracle timed on the host cores over a bounded sample of the same
 workload gives the CPU baseline.
 """
@@ -35,7 +38,8 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
 
-STAGES = ("build_summaries", "route_chunks", "route_groups", "gather_kv", "attend")
+STAGES_SEPARATE = ("build_summaries", "route_chunks", "route_groups", "gather_kv", "attend")
+STAGES_FUSED = ("build_summaries", "route", "gather_kv", "attend")
 
 
 def algorithmic_bytes(w, n_valid_rows: int) -> dict:
@@ -55,6 +59,8 @@ def algorithmic_bytes(w, n_valid_rows: int) -> dict:
         "build_summaries": kv_tok + table_c + table_g,
         "route_chunks": q_tok + table_c + table_c + B * Hkv * nc * w.topk_chunks * 4,
         "route_groups": table_c + table_g + B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4,
+        "route": (q_tok + 2 * table_c + table_g +
+                  B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4),
         "gather_kv": 4 * routed + B * Hkv * nc * w.topk_groups * 4,
         "attend": q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4,
     }
@@ -175,6 +181,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--separate-route", action="store_true",
+                    help="route with hga_route_chunks + hga_route_groups instead of hga_route")
     ap.add_argument("--probe-traffic", action="store_true",
                     help="run attention and a known-size copy for rocprofv3 --pmc, then exit")
     args = ap.parse_args()
@@ -204,18 +212,28 @@ def main():
     sh = stream.cuda_stream
     p = pipe.plan
 
-    calls = (
-        lambda: hga.hga_build_summaries(p, pipe.k, 0, w.n_chunks, pipe.chunk_sum, pipe.group_sum,
-                                        stream=sh),
-        lambda: hga.hga_route_chunks(p, pipe.q, 0, pipe.chunk_sum, pipe.qbar, pipe.chunk_idx,
-                                     stream=sh),
-        lambda: hga.hga_route_groups(p, pipe.qbar, pipe.chunk_idx, 0, pipe.group_sum,
-                                     pipe.group_idx, stream=sh),
-        lambda: hga.hga_gather_kv(p, pipe.group_idx, 0, pipe.k, pipe.v, pipe.k_routed,
-                                  pipe.v_routed, stream=sh),
-        lambda: hga.hga_attend(p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
-                               pipe.group_idx, pipe.out, pipe.lse, stream=sh),
-    )
+    summarise = lambda: hga.hga_build_summaries(p, pipe.k, 0, w.n_chunks, pipe.chunk_sum,
+                                                pipe.group_sum, stream=sh)
+    gather = lambda: hga.hga_gather_kv(p, pipe.group_idx, 0, pipe.k, pipe.v, pipe.k_routed,
+                                       pipe.v_routed, stream=sh)
+    attend = lambda: hga.hga_attend(p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
+                                    pipe.group_idx, pipe.out, pipe.lse, stream=sh)
+    if args.separate_route:
+        STAGES = STAGES_SEPARATE
+        calls = (
+            summarise,
+            lambda: hga.hga_route_chunks(p, pipe.q, 0, pipe.chunk_sum, pipe.qbar, pipe.chunk_idx,
+                                         stream=sh),
+            lambda: hga.hga_route_groups(p, pipe.qbar, pipe.chunk_idx, 0, pipe.group_sum,
+                                         pipe.group_idx, stream=sh),
+            gather, attend)
+    else:
+        STAGES = STAGES_FUSED
+        calls = (
+            summarise,
+            lambda: hga.hga_route(p, pipe.q, 0, pipe.chunk_sum, pipe.group_sum, pipe.qbar,
+                                  pipe.chunk_idx, pipe.group_idx, stream=sh),
+            gather, attend)
 
     for _ in range(args.warmup):
         for f in calls:
@@ -310,6 +328,7 @@ def main():
         "stage_timing": ("attend: HIP events around it in every timed step; other stages: "
                          "a second pass of the same steps with events between all calls"),
         "stages": stages,
+        "route_calls": "separate" if args.separate_route else "fused",
         "roofline": roofline,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }

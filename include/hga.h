@@ -10,6 +10,7 @@
  *   hga_build_summaries  mixed-RoPE chunk and group key summaries (Sec. 3.1, 3.2)
  *   hga_route_chunks     query-chunk -> chunk scoring, top-K_c (Sec. 3.3)
  *   hga_route_groups     group refinement inside the chosen chunks, top-K_g (Sec. 3.3)
+ *   hga_route            both routing stages in one launch, same outputs
  *   hga_gather_kv        copy the routed groups' exact token K/V (Sec. 4.3)
  *   hga_attend           exact causal softmax attention, Eq. (1), over the
  *                        current chunk, the always-visible chunks and the
@@ -174,6 +175,16 @@ hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32
                             int32_t q_chunk0, int32_t n_q_chunks, const float* group_sum,
                             int32_t table_chunks, int32_t* group_idx, void* stream);
 
+/* Both routing stages of Sec. 3.3 in one launch: writes exactly what
+ * hga_route_chunks followed by hga_route_groups on the same arguments writes
+ * (qbar, chunk_idx and group_idx bit-identical), without reading qbar or
+ * chunk_idx back from memory.  Arguments, layouts, requirements and errors
+ * are those of the two calls. */
+hga_status hga_route(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                     int32_t n_q_chunks, const float* chunk_sum, const float* group_sum,
+                     int32_t table_chunks, float* qbar, int32_t* chunk_idx, int32_t* group_idx,
+                     void* stream);
+
 /* Gather the exact token K/V of the routed groups (Sec. 4.3, "gathering
  * exact token K/V for the selected chunks or groups").  Slot s of query chunk
  * c = q_chunk0 + i receives tokens [g*group, (g+1)*group) of group
@@ -212,7 +223,9 @@ hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t
  *               [0, res_tokens/chunk) the rows of that query chunk are NaN.
  *   k_routed, v_routed, group_idx  as produced by hga_gather_kv/route_groups
  *   out         [batch, n_q_heads, n_q_chunks*chunk, head_dim] plan dtype
- *   lse         fp32 [batch, n_q_heads, n_q_chunks*chunk] or NULL */
+ *   lse         fp32 [batch, n_q_heads, n_q_chunks*chunk] or NULL
+ * HGA_EUNSUPPORTED when one head's resident K/V (res_tokens rows) or the
+ * query rows of one KV head span 0xfff00000 bytes or more. */
 hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                       int32_t n_q_chunks, const void* k_res, const void* v_res,
                       int64_t res_tokens, const int32_t* res_slot, const void* k_routed,

@@ -17,15 +17,25 @@
 // one exchange with the lane holding the other half of the tile's keys.
 //   O^T[d][query] += V^T . P^T            (A = V^T, B = P in VGPRs)
 // P is rounded to bf16 for the product; statistics and accumulators are fp32.
-// K and V are staged row-major; the V^T operand (eight keys at one head
-// dimension per lane) comes from gfx950's LDS transpose read
+//
+// Data movement: global memory is copied straight into LDS by buffer loads
+// with the LDS-destination form (64 lanes x 16 bytes land at M0 + 16*lane),
+// so no VGPRs stage the tiles.  The key tiles cycle through NS LDS stages:
+// when tile t is consumed, tiles t+1 .. t+NS-2 are already in flight and the
+// copy of tile t+NS-1 is issued into the stage tile t-1 has freed, with one
+// workgroup barrier per tile.  The workgroup's query rows and the unit's
+// group ids arrive the same way before the first tile.  Rows are unpadded;
+// the 16-byte chunks of row r are stored at chunk ^ swz(r), which spreads
+// the rows read together by one LDS instruction over distinct banks.  The
+// copies are written as inline assembly and waited for with explicit
+// vmcnt counts (loads complete in issue order), because the compiler's own
+// tracking of LDS-destination loads would wait for every copy in flight
+// before any LDS read.  V^T operands come from gfx950's LDS transpose read
 // (ds_read_b64_tr_b16): within each 16-lane group, lane i receives element
 // i%4 of the 64-bit reads issued by lanes 4j + i/4, j = 0..3, so 16 lanes
 // pointing at 4 keys x 16 dimensions hand each lane 4 keys of one dimension.
-// The next key tile is fetched into registers while the current one is in
-// use (the template allows a deeper ring).  All global reads go through
-// buffer descriptors: rows past a buffer's end read
-// as zero without a branch, which keeps the wait counts exact.
+// All global reads go through buffer descriptors: offsets past a buffer's
+// end read as zero.
 #include <math.h>
 
 #include "attend_common.hpp"
@@ -38,26 +48,71 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int KT = 64;  // keys per LDS tile (= chunk)
 constexpr int kXcds = 8;
+constexpr uint32_t kAbsent = 0xffff0000u;  // an offset past every buffer: reads zeros
+constexpr int kMaxGroupSlots = 512;
 
+// Descriptor words of a raw buffer [base, base + bytes) for the copies below
+// (base address, no stride, num_records = bytes); the operands are uniform.
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    u32x4 r;
+    r.x = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+    r.y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32) & 0xffffu);
+    r.z = __builtin_amdgcn_readfirstlane(bytes);
+    r.w = 0x00020000u;
+    return r;
+}
+
+// Copy 16 bytes per lane from buffer offset voff to LDS byte lds + 16*lane.
+__device__ __forceinline__ void copy16_to_lds(const u32x4& rs, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(rs), "s"(lds)
+                 : "memory");
+}
+
+// Copy 4 bytes per lane from buffer offset voff to LDS byte lds + 4*lane.
+__device__ __forceinline__ void copy4_to_lds(const u32x4& rs, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dword %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(rs), "s"(lds)
+                 : "memory");
+}
+
+// Wait until at most N vector-memory loads of this wavefront are in flight.
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Chunk swizzles: the 16-byte chunk j of row r is stored at j ^ swz(r).
+// K (and Q) rows are read as 16-byte A/B fragments by 32 lanes on 32
+// consecutive rows; V rows by the transpose read, 8 consecutive keys at a
+// time.
+// For D = 128 (16 chunks per row) one 4-bit map serves both patterns.
 template <int D>
-struct Smem {
-    // K rows 16 B apart modulo 128 B: the 8 rows of one A-operand read phase
-    // fall in distinct banks.  V rows 32 B apart modulo 128 B: the 4 rows of
-    // one transpose-read group fall in distinct banks.
-    static constexpr int KSTR = D + 8;
-    static constexpr int VSTR = D + 16;
-    static constexpr int kTileBytes = KT * (KSTR + VSTR) * 2;
-    static constexpr int NDT = D / 32;
-    // merge area: per query-tile slot and lane, the output accumulators, m and l
-    static constexpr int kMergeBytes = 2 * 64 * (NDT * 16 + 2) * 4;
-    static constexpr int kBytes = kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes;
-};
+__device__ __forceinline__ int swz_k(int r) {
+    if constexpr (D == 64)
+        return ((r ^ (r >> 3)) & 1) | (((r >> 2) & 1) << 1) | (((r >> 1) & 1) << 2);
+    else
+        return ((r ^ (r >> 3)) & 1) | (((r ^ (r >> 2)) & 1) << 1) | (((r >> 1) & 1) << 2) |
+               ((r & 1) << 3);
+}
+template <int D>
+__device__ __forceinline__ int swz_v(int r) {
+    if constexpr (D == 64)
+        return ((r & 1) << 1) | (((r >> 1) & 1) << 2);
+    else
+        return swz_k<D>(r);
+}
 
-__device__ __forceinline__ bf16x8_t as_bf16x8(const vec16& v) {
-    return __builtin_bit_cast(bf16x8_t, v);
+__device__ __forceinline__ bf16x8_t lds_frag(const bf16_t* p) {
+    return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const vec16*>(p));
 }
 
 __device__ __forceinline__ i16x4_t lds_read_tr16(const bf16_t* p) {
@@ -65,10 +120,24 @@ __device__ __forceinline__ i16x4_t lds_read_tr16(const bf16_t* p) {
         (lds_i16x4_t*)(reinterpret_cast<uintptr_t>(p)));
 }
 
+template <bool B>
+struct BoolTag {
+    static constexpr bool value = B;
+};
+
+template <int D, int NS>
+struct Layout {
+    static constexpr uint32_t kRowBytes = D * 2;
+    static constexpr uint32_t kTileBytes = KT * kRowBytes;  // one of K or V
+    static constexpr uint32_t kStageBytes = 2 * kTileBytes;
+    static constexpr uint32_t kGidOffset = NS * kStageBytes;
+    static constexpr uint32_t kBytes = kGidOffset + kMaxGroupSlots * 4;
+};
+
 // D: head dim; KS: wavefronts sharing one query tile (each takes one 32-key
-// half of every key tile); P: key tiles kept in flight in registers; NW:
+// half of every key tile); NS: LDS stages of the key-tile ring; NW:
 // wavefronts per workgroup (NW / KS query tiles per workgroup).
-template <int D, int KS, int P, int NW>
+template <int D, int KS, int NS, int NW>
 __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const bf16_t* __restrict__ q_rot, int q_chunk0, int n_q_chunks,
     const bf16_t* __restrict__ k_res, const bf16_t* __restrict__ v_res, int64_t res_tokens,
@@ -76,20 +145,25 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const bf16_t* __restrict__ v_routed, const int32_t* __restrict__ group_idx,
     bf16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads, int n_kv, int group_shift,
     int keep_first, int window, int topk_groups, int wg_per_unit, int n_blocks) {
-    using S = Smem<D>;
-    constexpr int KSTR = S::KSTR, VSTR = S::VSTR, NDT = S::NDT;
+    using Lay = Layout<D, NS>;
+    constexpr uint32_t kRowBytes = Lay::kRowBytes, kTileBytes = Lay::kTileBytes,
+                       kStageBytes = Lay::kStageBytes;
+    constexpr int NDT = D / 32;                  // 32-wide output blocks
     constexpr int NKS = D / 16;                  // k-steps of Q.K^T
-    constexpr int VPR = D / 8;                   // 16-byte vectors per row
-    constexpr int kThreads = NW * 64;
-    constexpr int NVEC = KT * VPR / kThreads;    // K (and V) vectors per thread per tile
+    constexpr int CPR = D / 8;                   // 16-byte chunks per row
     constexpr int QT = NW / KS;                  // query tiles per workgroup
     constexpr int NST = 2 / KS;                  // 32-key sub-tiles per wave per tile
-    constexpr uint32_t kRowBytes = D * 2;
+    constexpr int KI = kTileBytes / 1024 / NW;   // copies per wave per tile, for K (and V)
+    constexpr int LPT = 2 * KI;                  // loads per wave per tile
+    constexpr int QI = QT * 32 * kRowBytes / 1024 / NW;  // copies per wave for the query rows
+    constexpr int GI = kMaxGroupSlots * 4 / 256 / NW;    // copies per wave for the group ids
+    static_assert(KI >= 1 && QI >= 1 && GI >= 1, "copy split");
+    static_assert(QT * 32 * kRowBytes <= kStageBytes, "query rows fit one stage");
+    static_assert(NS >= 2 && NS <= 4, "stages");
 
-    __shared__ __align__(16) unsigned char smem[S::kBytes];
-    __shared__ int s_gvalid[512];
-    bf16_t* sK = reinterpret_cast<bf16_t*>(smem);
-    bf16_t* sV = sK + KT * KSTR;
+    extern __shared__ __align__(16) unsigned char smem[];
+    const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
+    const int* s_gid = reinterpret_cast<const int*>(smem + Lay::kGidOffset);
 
     // XCD-aware order: consecutive workgroups of one XCD take consecutive
     // (head, chunk) units, so a unit's previous chunk and the head's sink
@@ -102,7 +176,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const int bh = logical / wg_per_unit / n_q_chunks;
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int half = lane >> 5, col = lane & 31;
     const int r = n_q_heads / n_kv;
     const int nqt = 2 * r;
@@ -110,44 +184,58 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const int c = q_chunk0 + i;
     const int group = 1 << group_shift;
     const int gpc = KT >> group_shift;
-    const int qtile = part * QT + wave % QT;
+    const int qt_local = wave % QT;
+    const int qtile = part * QT + qt_local;
     const int ksplit = wave / QT;
     const bool qactive = qtile < nqt;
     const int64_t unit = static_cast<int64_t>(bh) * n_q_chunks + i;
     const int routed_rows = topk_groups * group;
     const int64_t res_chunks = res_tokens / KT;
 
-    // One descriptor per source: this head's resident K/V and this unit's
-    // routed K/V.  Offsets are 32-bit within each.
-    const buf_rsrc rk_res = make_rsrc(k_res + static_cast<int64_t>(bh) * res_tokens * D,
-                                      static_cast<uint32_t>(res_chunks * KT * kRowBytes));
-    const buf_rsrc rv_res = make_rsrc(v_res + static_cast<int64_t>(bh) * res_tokens * D,
-                                      static_cast<uint32_t>(res_chunks * KT * kRowBytes));
-    const buf_rsrc rk_rt = make_rsrc(k_routed + unit * routed_rows * D, routed_rows * kRowBytes);
-    const buf_rsrc rv_rt = make_rsrc(v_routed + unit * routed_rows * D, routed_rows * kRowBytes);
+    const u32x4 rk_res = rsrc_words(k_res + static_cast<int64_t>(bh) * res_tokens * D,
+                                    static_cast<uint32_t>(res_chunks * kTileBytes));
+    const u32x4 rv_res = rsrc_words(v_res + static_cast<int64_t>(bh) * res_tokens * D,
+                                    static_cast<uint32_t>(res_chunks * kTileBytes));
+    const u32x4 rk_rt = rsrc_words(k_routed + unit * routed_rows * D, routed_rows * kRowBytes);
+    const u32x4 rv_rt = rsrc_words(v_routed + unit * routed_rows * D, routed_rows * kRowBytes);
 
-    // group ids first: their validity is needed only when routed tiles are staged
-    const buf_rsrc g_rsrc = make_rsrc(group_idx + unit * topk_groups, topk_groups * 4);
-    constexpr int NG = 512 / kThreads;           // group-id slots per thread
-    int gval[NG];
+    // 1. The workgroup's query rows into the last stage (swizzled like K),
+    //    and the unit's group ids.
+    {
+        const int64_t qtok = static_cast<int64_t>(n_q_chunks) * KT;
+        const int64_t q_head0 = (static_cast<int64_t>(b) * n_q_heads + j * r) * qtok;
+        const u32x4 rq =
+            rsrc_words(q_rot + q_head0 * D, static_cast<uint32_t>(r * qtok * kRowBytes));
+        const uint32_t qbase = lds0 + (NS - 1) * kStageBytes;
 #pragma unroll
-    for (int u = 0; u < NG; ++u) gval[u] = buf_load_i32(g_rsrc, (tid + kThreads * u) * 4);
+        for (int u = 0; u < QI; ++u) {
+            const int blk = u * NW + wave;
+            const int pch = blk * 64 + lane;
+            const int row = pch / CPR, pc = pch % CPR;
+            const int urow = part * QT * 32 + row;  // query row within the unit
+            uint32_t off = kAbsent;
+            if (urow < r * KT) {
+                const int qh = urow / KT, qt = urow % KT;
+                off = static_cast<uint32_t>((qh * qtok + static_cast<int64_t>(i) * KT + qt) *
+                                            kRowBytes) +
+                      (pc ^ swz_k<D>(row)) * 16;
+            }
+            copy16_to_lds(rq, off, qbase + blk * 1024);
+        }
+        const u32x4 rg = rsrc_words(group_idx + unit * topk_groups, topk_groups * 4);
+#pragma unroll
+        for (int u = 0; u < GI; ++u) {
+            const int blk = u * NW + wave;
+            copy4_to_lds(rg, (blk * 64 + lane) * 4, lds0 + Lay::kGidOffset + blk * 256);
+        }
+    }
 
-    // this lane's query row and its Q fragments (B operand of S^T = K.Q^T)
+    // this lane's query row (token t of head hh)
     const int qrow_in_unit = qtile * 32 + col;
     const int hh = qrow_in_unit / KT, t = qrow_in_unit % KT;
-    const int64_t qtok = static_cast<int64_t>(n_q_chunks) * KT;
-    const int64_t qrow = (static_cast<int64_t>(b) * n_q_heads + j * r + (qactive ? hh : 0)) * qtok +
+    const int64_t qrow = (static_cast<int64_t>(b) * n_q_heads + j * r + (qactive ? hh : 0)) *
+                             (static_cast<int64_t>(n_q_chunks) * KT) +
                          static_cast<int64_t>(i) * KT + t;
-    // uniform descriptor over the r heads of this KV head; inactive lanes read zeros
-    const int64_t q_head0 = (static_cast<int64_t>(b) * n_q_heads + j * r) * qtok;
-    const buf_rsrc q_rsrc = make_rsrc(q_rot + q_head0 * D, static_cast<uint32_t>(r * qtok * kRowBytes));
-    const uint32_t q_off = qactive ? static_cast<uint32_t>((qrow - q_head0) * kRowBytes)
-                                   : 0xffffffffu - 0xffffu;
-    bf16x8_t qf[NKS];
-#pragma unroll
-    for (int kk = 0; kk < NKS; ++kk)
-        qf[kk] = as_bf16x8(buf_load16(q_rsrc, q_off + (kk * 16 + half * 8) * 2));
 
     // tile order: the current chunk, the visible closed chunks, the routed rows
     const VisibleChunks vis(c, keep_first, window);
@@ -156,48 +244,44 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const int n_tiles = 1 + n_vis + n_rt;
     bool bad = false;
 
-    // per-thread byte offset of its vectors inside a 64-row tile
-    uint32_t voff[NVEC];
+    // per-lane source offsets of this wave's copies inside a tile
+    uint32_t koff[KI], voff[KI];
 #pragma unroll
-    for (int u = 0; u < NVEC; ++u) {
-        const int v = tid + kThreads * u;
-        voff[u] = (v / VPR) * kRowBytes + (v % VPR) * 16;
+    for (int u = 0; u < KI; ++u) {
+        const int pch = (u * NW + wave) * 64 + lane;
+        const int row = pch / CPR, pc = pch % CPR;
+        koff[u] = row * kRowBytes + (pc ^ swz_k<D>(row)) * 16;
+        voff[u] = row * kRowBytes + (pc ^ swz_v<D>(row)) * 16;
     }
-
-    vec16 kreg[P][NVEC], vreg[P][NVEC];
-    // Stage tile `tile` in registers; a tile past the end reads as zeros.
-    auto fetch = [&](int tile, vec16 (&kr)[NVEC], vec16 (&vr)[NVEC]) {
-        bool routed = false;
-        uint32_t base = 0xffffffffu - 0xffffu;  // past every buffer: zeros
-        if (tile < n_tiles) {
-            if (tile <= n_vis) {
-                const int cc = tile == 0 ? c : vis.chunk(tile - 1);
-                int64_t slot = res_slot ? res_slot[cc] : cc;
-                if (slot < 0 || slot >= res_chunks) { bad = true; slot = 0; }
-                base = static_cast<uint32_t>(slot * KT * kRowBytes);
+    // Issue the copies of tile `tile` (< n_tiles) into stage `stage`.
+    auto issue = [&](int tile, int stage) {
+        const bool routed = tile > n_vis;
+        uint32_t base;
+        if (!routed) {
+            const int cc = tile == 0 ? c : vis.chunk(tile - 1);
+            const int64_t slot = res_slot ? res_slot[cc] : cc;
+            if (slot < 0 || slot >= res_chunks) {
+                bad = true;
+                base = kAbsent;
             } else {
-                routed = true;
-                base = static_cast<uint32_t>((tile - 1 - n_vis) * KT * kRowBytes);
+                base = static_cast<uint32_t>(slot * kTileBytes);
             }
+        } else {
+            base = static_cast<uint32_t>((tile - 1 - n_vis) * kTileBytes);
         }
-        const buf_rsrc rk = routed ? rk_rt : rk_res;
-        const buf_rsrc rv = routed ? rv_rt : rv_res;
+        const u32x4 rk = routed ? rk_rt : rk_res;
+        const u32x4 rv = routed ? rv_rt : rv_res;
+        const uint32_t sk = lds0 + stage * kStageBytes;
 #pragma unroll
-        for (int u = 0; u < NVEC; ++u) {
-            kr[u] = buf_load16(rk, base + voff[u]);
-            vr[u] = buf_load16(rv, base + voff[u]);
-        }
+        for (int u = 0; u < KI; ++u)
+            copy16_to_lds(rk, base + koff[u], sk + (u * NW + wave) * 1024);
+#pragma unroll
+        for (int u = 0; u < KI; ++u)
+            copy16_to_lds(rv, base + voff[u], sk + kTileBytes + (u * NW + wave) * 1024);
     };
-
 #pragma unroll
-    for (int s = 0; s < P; ++s) fetch(s, kreg[s], vreg[s]);
-
-#pragma unroll
-    for (int u = 0; u < NG; ++u) {
-        const int slot = tid + kThreads * u;
-        if (slot < topk_groups) s_gvalid[slot] = gval[u] >= 0 && gval[u] < c * gpc;
-    }
-
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < n_tiles) issue(s, s);
 
     const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
     f32x16_t oacc[NDT];
@@ -206,112 +290,140 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[dt][e] = 0.f;
     float m_run = -INFINITY, l_run = 0.f;  // m_run in scaled (log2) units
+    bf16x8_t qf[NKS];
 
-    for (int base = 0; base < n_tiles; base += P) {
+    // One key tile: wait for its copies, issue a later tile's, then
+    // S^T = K.Q^T, the online softmax update and O^T += V^T.P^T.  The current
+    // chunk (tile 0, under the causal mask) is a separate instantiation so the
+    // other tiles carry no mask work.
+    auto step = [&](int tile, auto current_tag) {
+        constexpr bool kCurrent = decltype(current_tag)::value;
+        // this wave's copies of `tile` are done once at most `ahead` later
+        // tiles' copies remain in flight
+        const int ahead = min(NS - 2, n_tiles - 1 - tile);
+        if (NS >= 4 && ahead >= 2)
+            wait_loads<(NS >= 4 ? 2 : 0) * LPT>();
+        else if (NS >= 3 && ahead >= 1)
+            wait_loads<(NS >= 3 ? 1 : 0) * LPT>();
+        else
+            wait_loads<0>();
+        __syncthreads();
+        if (kCurrent) {
+            // query fragments (B operand of S^T = K.Q^T): row qt_local*32 + col,
+            // dimensions kk*16 + half*8 .. +8
+            const bf16_t* sq = reinterpret_cast<const bf16_t*>(smem + (NS - 1) * kStageBytes);
+            const int row = qt_local * 32 + col;
 #pragma unroll
-        for (int s = 0; s < P; ++s) {
-            const int tile = base + s;
-            if (tile >= n_tiles) break;
-            const int kind = tile == 0 ? kTileCurrent : (tile <= n_vis ? kTileVisible : kTileRouted);
-            const int rt_row0 = (tile - 1 - n_vis) * KT;
-            __syncthreads();
-#pragma unroll
-            for (int u = 0; u < NVEC; ++u) {
-                const int v = tid + kThreads * u;
-                const int row = v / VPR, cv = v % VPR;
-                *reinterpret_cast<vec16*>(sK + row * KSTR + cv * 8) = kreg[s][u];
-                *reinterpret_cast<vec16*>(sV + row * VSTR + cv * 8) = vreg[s][u];
+            for (int kk = 0; kk < NKS; ++kk)
+                qf[kk] = lds_frag(sq + row * D + ((2 * kk + half) ^ swz_k<D>(row)) * 8);
+            __syncthreads();  // the last stage is overwritten next
+        }
+        if (tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
+
+        const int stage = tile % NS;
+        const bf16_t* sK = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes);
+        const bf16_t* sV = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes + kTileBytes);
+        const int rt_row0 = (tile - 1 - n_vis) * KT;
+
+        // rows that must be masked in a routed tile: past the buffer or of an invalid slot
+        bool partial = false;
+        if (!kCurrent && tile > n_vis) {
+            partial = rt_row0 + KT > routed_rows;
+            for (int g = rt_row0 >> group_shift;
+                 g < (rt_row0 + KT) >> group_shift && g < topk_groups; ++g) {
+                const int id = s_gid[g];
+                partial |= !(id >= 0 && id < c * gpc);
             }
-            __syncthreads();
-            fetch(tile + P, kreg[s], vreg[s]);
+        }
+        if (!qactive) return;
 
-            // rows that must be masked in a routed tile: past the buffer or of an invalid slot
-            bool partial = false;
-            if (kind == kTileRouted) {
-                partial = rt_row0 + KT > routed_rows;
-                for (int g = rt_row0 >> group_shift; g < (rt_row0 + KT) >> group_shift && g < topk_groups; ++g)
-                    partial |= s_gvalid[g] == 0;
-            }
-
-            if (qactive) {
-                f32x16_t sacc[NST];
-                float tmax = -INFINITY;
+        f32x16_t sacc[NST];
+        float tmax = -INFINITY;
 #pragma unroll
-                for (int n = 0; n < NST; ++n) {
-                    const int st = KS == 2 ? ksplit : n;
+        for (int n = 0; n < NST; ++n) {
+            const int st = KS == 2 ? ksplit : n;
+            const int krow = st * 32 + col;
+            bf16x8_t kf[NKS];
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) sacc[n][e] = 0.f;
+            for (int kk = 0; kk < NKS; ++kk)
+                kf[kk] = lds_frag(sK + krow * D + ((2 * kk + half) ^ swz_k<D>(col)) * 8);
 #pragma unroll
-                    for (int kk = 0; kk < NKS; ++kk) {
-                        const bf16x8_t a = as_bf16x8(*reinterpret_cast<const vec16*>(
-                            sK + (st * 32 + col) * KSTR + kk * 16 + half * 8));
-                        sacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], sacc[n], 0, 0, 0);
-                    }
-                    if (kind == kTileCurrent) {
+            for (int e = 0; e < 16; ++e) sacc[n][e] = 0.f;
 #pragma unroll
-                        for (int e = 0; e < 16; ++e) {
-                            const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                            sacc[n][e] = key > t ? -INFINITY : sacc[n][e];
-                        }
-                    } else if (partial) {
+            for (int kk = 0; kk < NKS; ++kk)
+                sacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sacc[n], 0, 0, 0);
+            if (kCurrent) {
 #pragma unroll
-                        for (int e = 0; e < 16; ++e) {
-                            const int row = rt_row0 + st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                            const int slot = min(row >> group_shift, topk_groups - 1);
-                            const bool ok = row < routed_rows && s_gvalid[slot] != 0;
-                            sacc[n][e] = ok ? sacc[n][e] : -INFINITY;
-                        }
-                    }
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[n][e]);
+                for (int e = 0; e < 16; ++e) {
+                    const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                    sacc[n][e] = key > t ? -INFINITY : sacc[n][e];
                 }
-                tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * scale;
-                const float m_new = fmaxf(m_run, tmax);
-                const float m_use = m_new == -INFINITY ? 0.f : m_new;
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-                l_run *= alpha;
+            } else if (partial) {
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
+                for (int e = 0; e < 16; ++e) {
+                    const int row = rt_row0 + st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                    const int slot = min(row >> group_shift, topk_groups - 1);
+                    const int id = s_gid[slot];
+                    const bool ok = row < routed_rows && id >= 0 && id < c * gpc;
+                    sacc[n][e] = ok ? sacc[n][e] : -INFINITY;
+                }
+            }
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
-                m_run = m_new;
+            for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[n][e]);
+        }
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * scale;
+        const float m_new = fmaxf(m_run, tmax);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+        l_run *= alpha;
+        // the output needs rescaling only where the running maximum moved
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
 #pragma unroll
-                for (int n = 0; n < NST; ++n) {
-                    const int st = KS == 2 ? ksplit : n;
+            for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-                    for (int kap = 0; kap < 2; ++kap) {
-                        bf16x8_t pf;
+                for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+        }
+        m_run = m_new;
 #pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const float pv =
-                                __builtin_amdgcn_exp2f(fmaf(sacc[n][kap * 8 + e], scale, -m_use));
-                            l_run += pv;
-                            pf[e] = static_cast<__bf16>(pv);
-                        }
-                        // V^T operand: keys st*32 + kap*16 + {half*4 + 0..3, 8 + half*4 + 0..3}
-                        // at dimension dt*32 + col; each 16-lane group points at
-                        // 4 keys x 16 dimensions.
-                        const int key0 = st * 32 + kap * 16 + half * 4 + ((lane & 15) >> 2);
-                        const int dcol = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+        for (int n = 0; n < NST; ++n) {
+            const int st = KS == 2 ? ksplit : n;
 #pragma unroll
-                        for (int dt = 0; dt < NDT; ++dt) {
-                            const bf16_t* vp = sV + key0 * VSTR + dt * 32 + dcol;
-                            const i16x4_t lo = lds_read_tr16(vp);
-                            const i16x4_t hi = lds_read_tr16(vp + 8 * VSTR);
-                            const bf16x8_t a = __builtin_bit_cast(
-                                bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-                            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, oacc[dt], 0, 0, 0);
-                        }
-                    }
+            for (int kap = 0; kap < 2; ++kap) {
+                bf16x8_t pf;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float pv =
+                        __builtin_amdgcn_exp2f(fmaf(sacc[n][kap * 8 + e], scale, -m_use));
+                    l_run += pv;
+                    pf[e] = static_cast<__bf16>(pv);
+                }
+                // V^T operand: keys st*32 + kap*16 + {half*4 + 0..3, 8 + half*4 + 0..3}
+                // at dimension dt*32 + col; each 16-lane group points at
+                // 4 keys x 16 dimensions.
+                const int key0 = st * 32 + kap * 16 + half * 4 + ((lane & 15) >> 2);
+                const int dcol = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+                const int vs0 = swz_v<D>(key0), vs1 = swz_v<D>(key0 + 8);
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    const int e0 = dt * 32 + dcol;
+                    const bf16_t* vp0 = sV + key0 * D + (((e0 >> 3) ^ vs0) << 3) + (e0 & 7);
+                    const bf16_t* vp1 = sV + (key0 + 8) * D + (((e0 >> 3) ^ vs1) << 3) + (e0 & 7);
+                    const i16x4_t lo = lds_read_tr16(vp0);
+                    const i16x4_t hi = lds_read_tr16(vp1);
+                    const bf16x8_t a = __builtin_bit_cast(
+                        bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                    oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, oacc[dt], 0, 0, 0);
                 }
             }
         }
-    }
+    };
+    step(0, BoolTag<true>{});
+    for (int tile = 1; tile < n_tiles; ++tile) step(tile, BoolTag<false>{});
 
     float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-    __syncthreads();  // LDS tiles are dead from here on
+    __syncthreads();  // LDS stages are dead from here on (every copy was waited for)
     if (KS == 2) {
-        float* mine = reinterpret_cast<float*>(smem) + ((wave % QT) * 64 + lane) * (NDT * 16 + 2);
+        float* mine = reinterpret_cast<float*>(smem) + (qt_local * 64 + lane) * (NDT * 16 + 2);
         if (ksplit == 1) {
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt)
@@ -352,6 +464,29 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     if (lse && half == 0) lse[qrow] = bad ? NAN : (m_run + log2f(l_tot)) * 0.6931471805599453f;
 }
 
+template <int D, int KS, int NS, int NW>
+hipError_t launch_mfma_t(int grid, hipStream_t stream, const bf16_t* q_rot, int q_chunk0,
+                         int n_q_chunks, const bf16_t* k_res, const bf16_t* v_res,
+                         int64_t res_tokens, const int32_t* res_slot, const bf16_t* k_routed,
+                         const bf16_t* v_routed, const int32_t* group_idx, bf16_t* out, float* lse,
+                         int n_q_heads, int n_kv, int group_shift, int keep_first, int window,
+                         int topk_groups, int wg_per_unit, int n_blocks) {
+    constexpr uint32_t kLds = Layout<D, NS>::kBytes;
+    static bool configured = false;  // per instantiation (the limit is a function attribute)
+    if (!configured) {
+        const hipError_t e = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&attend_mfma_kernel<D, KS, NS, NW>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
+        if (e != hipSuccess) return e;
+        configured = true;
+    }
+    hipLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW>), dim3(grid), dim3(NW * 64), kLds,
+                       stream, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                       k_routed, v_routed, group_idx, out, lse, n_q_heads, n_kv, group_shift,
+                       keep_first, window, topk_groups, wg_per_unit, n_blocks);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chunk0,
@@ -362,8 +497,8 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int nqt = 2 * r;
-    // One head per KV head (two query tiles): a workgroup of two wavefronts,
-    // each with every key of its tile; otherwise four query tiles per group.
+    // One head per KV head (two query tiles): two wavefronts per query tile,
+    // each with half of every key tile; otherwise four query tiles per group.
     const bool one_head = nqt <= 2;
     const int wg_per_unit = one_head ? 1 : (nqt + 3) / 4;
     const int64_t n_blocks64 =
@@ -372,23 +507,20 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     const int n_blocks = static_cast<int>(n_blocks64);
     const int grid = (n_blocks + kXcds - 1) / kXcds * kXcds;
     const int group_shift = p.group == 8 ? 3 : (p.group == 16 ? 4 : 5);
-#define HGA_MFMA(DD, KSV, PV, NWV)                                                               \
-    hipLaunchKernelGGL((attend_mfma_kernel<DD, KSV, PV, NWV>), dim3(grid), dim3(NWV * 64), 0,    \
-                       stream, static_cast<const bf16_t*>(q_rot), q_chunk0, n_q_chunks,          \
-                       static_cast<const bf16_t*>(k_res), static_cast<const bf16_t*>(v_res),     \
-                       res_tokens, res_slot, static_cast<const bf16_t*>(k_routed),               \
-                       static_cast<const bf16_t*>(v_routed), group_idx,                          \
-                       static_cast<bf16_t*>(out), lse, p.n_q_heads, p.n_kv_heads, group_shift,   \
-                       p.keep_first, recent_window(p), p.topk_groups, wg_per_unit, n_blocks)
-    // One tile in flight per workgroup: measured faster than deeper register
-    // rings, whose extra VGPRs cost more occupancy than they hide latency.
+#define HGA_MFMA(DD, KSV, NSV, NWV)                                                            \
+    return launch_mfma_t<DD, KSV, NSV, NWV>(                                                   \
+        grid, stream, static_cast<const bf16_t*>(q_rot), q_chunk0, n_q_chunks,                 \
+        static_cast<const bf16_t*>(k_res), static_cast<const bf16_t*>(v_res), res_tokens,      \
+        res_slot, static_cast<const bf16_t*>(k_routed), static_cast<const bf16_t*>(v_routed),  \
+        group_idx, static_cast<bf16_t*>(out), lse, p.n_q_heads, p.n_kv_heads, group_shift,     \
+        p.keep_first, recent_window(p), p.topk_groups, wg_per_unit, n_blocks)
     if (p.head_dim == 64) {
-        if (one_head) HGA_MFMA(64, 2, 1, 4); else HGA_MFMA(64, 1, 1, 4);
-    } else {
-        if (one_head) HGA_MFMA(128, 2, 1, 4); else HGA_MFMA(128, 1, 1, 4);
+        if (one_head) HGA_MFMA(64, 2, 2, 4);
+        HGA_MFMA(64, 1, 2, 4);
     }
+    if (one_head) HGA_MFMA(128, 2, 2, 4);
+    HGA_MFMA(128, 1, 2, 4);
 #undef HGA_MFMA
-    return hipGetLastError();
 }
 
 hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,

@@ -14,6 +14,11 @@
 
 namespace {
 
+// Largest byte extent of one head's slab the kernels address (32-bit
+// offsets, with room above for the "absent" marker offset).
+constexpr int64_t kMaxSlabBytes = 0xfff00000ll;
+
+
 thread_local std::string g_last_error;
 
 hga_status fail(hga_status st, const char* fmt, ...) {
@@ -184,11 +189,15 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
     int max_lds = 0;
     e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    int n_cu = 0;
+    e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
     hga_plan* pl = new (std::nothrow) hga_plan();
     if (!pl) return fail(HGA_EINVAL, "out of host memory");
     pl->p = p;
     pl->device = dev;
     pl->max_lds = max_lds;
+    pl->n_cu = n_cu;
     float* buf = nullptr;
     const size_t bytes = (tc.size() + tg.size()) * sizeof(float);
     e = hipMalloc(&buf, bytes);
@@ -250,9 +259,13 @@ hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t 
                     "hga_build_summaries launch");
 }
 
-hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
-                            int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
-                            float* qbar, int32_t* chunk_idx, void* stream) {
+namespace {
+
+// Checks shared by the chunk-routing calls; *n_max gets the largest number of
+// middle chunks of a query chunk.
+hga_status check_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                              int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
+                              float* qbar, int32_t* chunk_idx, bool groups, int* n_max) {
     HGA_TRY(check_plan(plan));
     const hga_params& p = plan->p;
     if (q_chunk0 < 0 || n_q_chunks < 0 || table_chunks < 0)
@@ -261,22 +274,51 @@ hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_c
     if (static_cast<int64_t>(q_chunk0) + n_q_chunks - 1 > table_chunks)
         return fail(HGA_EINVAL, "query chunk %d needs summaries of earlier chunks but "
                     "table_chunks is %d", q_chunk0 + n_q_chunks - 1, table_chunks);
-    const int n_max = hga::middle_count(p, q_chunk0 + n_q_chunks - 1);
-    if (n_max > hga::kMaxChunkCandidates)
-        return fail(HGA_EUNSUPPORTED, "%d middle chunks exceed the %d-candidate limit", n_max,
+    *n_max = hga::middle_count(p, q_chunk0 + n_q_chunks - 1);
+    if (*n_max > hga::kMaxChunkCandidates)
+        return fail(HGA_EUNSUPPORTED, "%d middle chunks exceed the %d-candidate limit", *n_max,
                     hga::kMaxChunkCandidates);
-    if (hga::route_chunks_lds_bytes(*plan, n_max) > static_cast<size_t>(plan->max_lds))
+    if (hga::route_lds_bytes(*plan, *n_max, groups) > static_cast<size_t>(plan->max_lds))
         return fail(HGA_EUNSUPPORTED, "%d middle chunks do not fit the device's %d-byte LDS",
-                    n_max, plan->max_lds);
+                    *n_max, plan->max_lds);
     HGA_TRY(check_tensor(q_rot, "q_rot"));
     HGA_TRY(check_tensor(qbar, "qbar"));
     HGA_TRY(check_index(chunk_idx, "chunk_idx"));
-    if (n_max > 0) HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
+    if (*n_max > 0) HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
+    return HGA_OK;
+}
+
+}  // namespace
+
+hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
+                            float* qbar, int32_t* chunk_idx, void* stream) {
+    int n_max = 0;
+    HGA_TRY(check_route_chunks(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, table_chunks, qbar,
+                               chunk_idx, false, &n_max));
+    if (n_q_chunks == 0) return HGA_OK;
     clear_stale_error();
     return launched(hga::launch_route_chunks(*plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
                                              table_chunks, qbar, chunk_idx,
                                              static_cast<hipStream_t>(stream)),
                     "hga_route_chunks launch");
+}
+
+hga_status hga_route(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                     int32_t n_q_chunks, const float* chunk_sum, const float* group_sum,
+                     int32_t table_chunks, float* qbar, int32_t* chunk_idx, int32_t* group_idx,
+                     void* stream) {
+    int n_max = 0;
+    HGA_TRY(check_route_chunks(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, table_chunks, qbar,
+                               chunk_idx, true, &n_max));
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_tensor(group_sum, "group_sum"));
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    clear_stale_error();
+    return launched(hga::launch_route(*plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, group_sum,
+                                      table_chunks, qbar, chunk_idx, group_idx,
+                                      static_cast<hipStream_t>(stream)),
+                    "hga_route launch");
 }
 
 hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32_t* chunk_idx,
@@ -357,6 +399,17 @@ hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                     static_cast<long long>(res_tokens));
     if (res_slot && res_tokens < p.chunk)
         return fail(HGA_EINVAL, "resident buffer holds no full chunk");
+    {
+        // the kernels address one head's slab with 32-bit offsets
+        const int64_t row_bytes = static_cast<int64_t>(p.head_dim) * (p.dtype == HGA_BF16 ? 2 : 4);
+        const int64_t r = p.n_q_heads / p.n_kv_heads;
+        const int64_t q_slab = r * (static_cast<int64_t>(n_q_chunks) * p.chunk) * row_bytes;
+        if (res_tokens * row_bytes >= kMaxSlabBytes || q_slab >= kMaxSlabBytes)
+            return fail(HGA_EUNSUPPORTED, "one head's K/V (%lld bytes) or the query rows of one "
+                        "KV head (%lld bytes) exceed the %lld-byte addressing limit",
+                        static_cast<long long>(res_tokens * row_bytes),
+                        static_cast<long long>(q_slab), static_cast<long long>(kMaxSlabBytes));
+    }
     if (res_slot) HGA_TRY(check_index(res_slot, "res_slot"));
     HGA_TRY(check_tensor(q_rot, "q_rot"));
     HGA_TRY(check_tensor(k_res, "k_res"));

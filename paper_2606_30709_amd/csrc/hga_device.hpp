@@ -94,25 +94,45 @@ __device__ __forceinline__ int key_index(uint64_t key) {
     return static_cast<int>(0xffffffffu - static_cast<uint32_t>(key & 0xffffffffu));
 }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int mask) {
-    uint32_t lo = __shfl_xor(static_cast<uint32_t>(x), mask, 64);
-    uint32_t hi = __shfl_xor(static_cast<uint32_t>(x >> 32), mask, 64);
-    return (static_cast<uint64_t>(hi) << 32) | lo;
+// x combined (max) with the value DPP control kCtrl moves into this lane;
+// lanes that receive nothing (outside the row, or rows outside kRowMask) see 0,
+// the smallest unsigned value.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t max_dpp(uint32_t x) {
+    const uint32_t o = static_cast<uint32_t>(
+        __builtin_amdgcn_update_dpp(0, static_cast<int>(x), kCtrl, kRowMask, 0xf, true));
+    return o > x ? o : x;
 }
 
+// Wave-wide maximum of an unsigned value, uniform result.  Within each
+// 16-lane row, shifts by 1, 2, 4, 8 leave the row maximum in the row's lane
+// 15; row broadcasts 15 and 31 carry it into rows 1..3, and lane 63 ends with
+// the maximum of the wave.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+    x = max_dpp<0x111, 0xf>(x);  // row_shr:1
+    x = max_dpp<0x112, 0xf>(x);  // row_shr:2
+    x = max_dpp<0x114, 0xf>(x);  // row_shr:4
+    x = max_dpp<0x118, 0xf>(x);  // row_shr:8
+    x = max_dpp<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+    x = max_dpp<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), 63));
+}
+
+// Wave-wide maximum of a 64-bit key: the high words first, then the low
+// words of the lanes holding that high word.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        uint64_t o = shfl_xor_u64(x, m);
-        x = o > x ? o : x;
-    }
-    return x;
+    const uint32_t hi = static_cast<uint32_t>(x >> 32);
+    const uint32_t top_hi = wave_max_u32(hi);
+    const uint32_t top_lo = wave_max_u32(hi == top_hi ? static_cast<uint32_t>(x) : 0u);
+    return (static_cast<uint64_t>(top_hi) << 32) | top_lo;
 }
 
 // Top-k selection by one wavefront over `n` packed keys in LDS (keys are
 // never zero; zero marks a taken key).  Writes the k selected indices, in
 // ascending order, to sel[0..k) (LDS).  All 64 lanes of the wave must call.
-__device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, int* scratch) {
+// Each round takes the wave-wide maximum of the lanes' best keys; the winning
+// lane drops it and rescans its share.
+__device__ inline void wave_select_topk_lds(uint64_t* keys, int n, int k, int* sel, int* scratch) {
     const int lane = threadIdx.x & 63;
     uint64_t best = 0;
     int best_pos = -1;
@@ -143,6 +163,38 @@ __device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, 
         for (int j = 0; j < k; ++j) rank += scratch[j] < v;
         sel[rank] = v;
     }
+}
+
+// The same selection for n <= 64 * R keys and k <= 64, with each lane's
+// share of the keys held in registers: a round is one wave maximum and a
+// register rescan, and winner `round` is kept by lane `round`.
+template <int R>
+__device__ inline void wave_select_topk_regs(const uint64_t* keys, int n, int k, int* sel) {
+    const int lane = threadIdx.x & 63;
+    uint64_t v[R];
+#pragma unroll
+    for (int t = 0; t < R; ++t) v[t] = lane + 64 * t < n ? keys[lane + 64 * t] : 0;
+    int mine = 0x7fffffff;
+    for (int round = 0; round < k; ++round) {
+        uint64_t best = v[0];
+#pragma unroll
+        for (int t = 1; t < R; ++t) best = v[t] > best ? v[t] : best;
+        const uint64_t top = wave_max_u64(best);
+#pragma unroll
+        for (int t = 0; t < R; ++t) v[t] = v[t] == top ? 0 : v[t];
+        if (lane == round) mine = key_index(top);
+    }
+    int rank = 0;
+    for (int j = 0; j < k; ++j) rank += __builtin_amdgcn_readlane(mine, j) < mine;
+    if (lane < k) sel[rank] = mine;
+}
+
+// Dispatch on size; both forms select the same keys.
+__device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, int* scratch) {
+    if (n <= 64 * 4 && k <= 64)
+        wave_select_topk_regs<4>(keys, n, k, sel);
+    else
+        wave_select_topk_lds(keys, n, k, sel, scratch);
 }
 
 }  // namespace hga

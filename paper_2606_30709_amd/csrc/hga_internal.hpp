@@ -10,6 +10,7 @@ struct hga_plan {
     hga_params p;         // resolved: hf_pairs_* filled in
     int device;
     int max_lds;          // device limit on LDS bytes per workgroup
+    int n_cu;             // compute units of the device
     float* phase_group;   // device [2][group][head_dim/2]: cos then sin of phi_p(o), span = group
     float* phase_psi;     // device [2][chunk/group][head_dim/2]: cos, sin of psi_g theta_p
 };
@@ -31,8 +32,9 @@ inline int middle_count(const hga_params& p, int c) {
     return n > 0 ? n : 0;
 }
 
-// LDS one routing wavefront needs for `n_max` middle-chunk candidates.
-size_t route_chunks_lds_bytes(const hga_plan& plan, int n_max);
+// LDS a routing workgroup of one wavefront needs for `n_max` middle-chunk
+// candidates, with or without the fused group refinement.
+size_t route_lds_bytes(const hga_plan& plan, int n_max, bool groups);
 
 // Kernel launchers; each returns hipSuccess or the launch error.
 hipError_t launch_build_summaries(const hga_plan& plan, const void* k_rot, int64_t k_tokens,
@@ -42,6 +44,10 @@ hipError_t launch_build_summaries(const hga_plan& plan, const void* k_rot, int64
 hipError_t launch_route_chunks(const hga_plan& plan, const void* q_rot, int q_chunk0,
                                int n_q_chunks, const float* chunk_sum, int table_chunks,
                                float* qbar, int32_t* chunk_idx, hipStream_t stream);
+
+hipError_t launch_route(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
+                        const float* chunk_sum, const float* group_sum, int table_chunks,
+                        float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream);
 
 hipError_t launch_route_groups(const hga_plan& plan, const float* qbar, const int32_t* chunk_idx,
                                int q_chunk0, int n_q_chunks, const float* group_sum,

@@ -2,8 +2,8 @@
 // selection, then group refinement with top-K_g selection.
 //
 // One wavefront per (batch, KV head, query chunk) unit and up to four units
-// per workgroup, each wave with its own LDS region and no workgroup barrier.
-// Scores are fp32 dot products (coalesced row reads, a fixed DPP row sum),
+// per workgroup, each wave with its own LDS region.
+// Scores are fp32 dot products in a fixed summation order,
 // packed with their candidate id into 64-bit keys
 // (larger score first, then lower id) held in LDS, and the wave extracts the top k by repeated wave-wide maxima: each lane
 // keeps the best key of its own strided share, so a round costs one wave
@@ -19,59 +19,71 @@ __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 }
 
-// x + x from the lane n below within each 16-lane row (lanes below n add 0).
-template <int kCtrl>
-__device__ __forceinline__ float add_row_shr(float x) {
-    return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kCtrl, 0xf, 0xf, true));
+// x plus the value of the lane that DPP quad permutation kPerm names.
+template <int kPerm>
+__device__ __forceinline__ float add_quad(float x) {
+    return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), kPerm, 0xf, 0xf, false));
 }
 
-// Scores of 64 candidates by one wavefront, coalesced: the 16 lanes of row
-// g = lane/16 read the rows of candidates 16g .. 16g+15, one table row per
-// instruction (lane p takes float4 p, and p+16 for D = 128), form partial
-// dot products with q_bar (broadcast from LDS), and a DPP prefix sum over the
-// row (shifts 1, 2, 4, 8) leaves each candidate's complete score in lane 15
-// of the row.  The summation order is fixed, so scores are bit-reproducible.
-// Lane 15 of each row writes the keys of its 16 candidates; row_of(k) gives
-// the table row (and candidate id) of the batch's k-th candidate, valid(k)
-// whether it exists.
-template <int D, typename RowOf>
+// Scores of 16 * NB candidates by one wavefront.  In each batch of 16, lane l
+// works on candidate l/4, on float4 columns 4u + l%4 (u < D/16) of its table
+// row, so one load instruction reads 64 contiguous bytes of each of 16 rows;
+// all NB * D/16 loads are issued before any is used.  The four partial dot
+// products of a row are added pairwise in a fixed order by quad exchanges
+// ((p0 + p1) + (p2 + p3), the same value in all four lanes), so scores are
+// bit-reproducible.  row_of(k) gives the table row, which is also the
+// candidate id, of the batch's k-th candidate (callers clamp k to the last
+// valid one); keys[k] is written for k < n_valid.
+template <int D, int NB, typename RowOf>
 __device__ __forceinline__ void batch_keys(const float* s_q, const float* table, RowOf row_of,
                                            int n_valid, uint64_t* keys) {
-    constexpr int F4 = D / 64;  // float4 per lane per row
+    constexpr int U = D / 16;
     const int lane = threadIdx.x & 63;
-    const int grp = lane >> 4, p = lane & 15;
-    float4 qv[F4];
+    const int cand = lane >> 2, qd = lane & 3;
+    float4 x[NB][U];
 #pragma unroll
-    for (int f = 0; f < F4; ++f) qv[f] = *reinterpret_cast<const float4*>(s_q + (p + 16 * f) * 4);
-    float part[16];
+    for (int bb = 0; bb < NB; ++bb) {
+        const float* row = table + static_cast<int64_t>(row_of(bb * 16 + cand)) * D;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-        const float* row = table + static_cast<int64_t>(row_of(grp * 16 + k)) * D;
+        for (int u = 0; u < U; ++u) x[bb][u] = *reinterpret_cast<const float4*>(row + (4 * u + qd) * 4);
+    }
+    float4 qv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) qv[u] = *reinterpret_cast<const float4*>(s_q + (4 * u + qd) * 4);
+#pragma unroll
+    for (int bb = 0; bb < NB; ++bb) {
         float a = 0.f;
 #pragma unroll
-        for (int f = 0; f < F4; ++f) {
-            const float4 x = *reinterpret_cast<const float4*>(row + (p + 16 * f) * 4);
-            a = fmaf(qv[f].x, x.x, a);
-            a = fmaf(qv[f].y, x.y, a);
-            a = fmaf(qv[f].z, x.z, a);
-            a = fmaf(qv[f].w, x.w, a);
+        for (int u = 0; u < U; ++u) {
+            a = fmaf(qv[u].x, x[bb][u].x, a);
+            a = fmaf(qv[u].y, x[bb][u].y, a);
+            a = fmaf(qv[u].z, x[bb][u].z, a);
+            a = fmaf(qv[u].w, x[bb][u].w, a);
         }
-        part[k] = a;
+        a = add_quad<0xb1>(a);  // quad_perm [1,0,3,2]
+        a = add_quad<0x4e>(a);  // quad_perm [2,3,0,1]
+        const int m = bb * 16 + cand;
+        if (qd == 0 && m < n_valid) keys[m] = select_key(a, row_of(m));
     }
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-        float x = part[k];
-        x = add_row_shr<0x111>(x);  // row_shr:1
-        x = add_row_shr<0x112>(x);  // row_shr:2
-        x = add_row_shr<0x114>(x);  // row_shr:4
-        x = add_row_shr<0x118>(x);  // row_shr:8
-        part[k] = x;
-    }
-    if (p == 15) {
-#pragma unroll
-        for (int k = 0; k < 16; ++k) {
-            const int m = grp * 16 + k;
-            if (m < n_valid) keys[m] = select_key(part[k], row_of(m));
+}
+
+// Keys of candidates 0 .. n-1 (candidate m at table row row_of(m)), in
+// batches of 64, 32 or 16 by what remains.
+template <int D, typename RowOf>
+__device__ __forceinline__ void score_candidates(const float* s_q, const float* table,
+                                                 RowOf row_of, int n, uint64_t* keys) {
+    for (int m0 = 0; m0 < n;) {
+        const int rem = n - m0;
+        auto ro = [&](int k) { return row_of(m0 + (k < rem ? k : rem - 1)); };
+        if (D == 64 && rem > 32) {
+            batch_keys<D, 4>(s_q, table, ro, rem, keys + m0);
+            m0 += 64;
+        } else if (rem > 16) {
+            batch_keys<D, 2>(s_q, table, ro, rem, keys + m0);
+            m0 += 32;
+        } else {
+            batch_keys<D, 1>(s_q, table, ro, rem, keys + m0);
+            m0 += 16;
         }
     }
 }
@@ -107,85 +119,168 @@ __device__ inline WaveLds carve(unsigned char* base, int d, int n_list, int topk
     return w;
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void route_chunks_kernel(
+// Query-chunk routing for up to four consecutive query chunks of one
+// (batch, KV head), in a workgroup of four wavefronts.  Wavefront w < units
+// owns query chunk w of the group and computes its q_bar; all four stage the
+// chunk-summary table in LDS, 64 rows at a time (the next block's rows are
+// loaded into registers while the current block is scored, and the first
+// block's while q_bar is formed), and each owning wavefront scores its own
+// middle chunks (one table row per lane; four partial dot products over the
+// dimensions d = 0, 1, 2, 3 mod 4, each in order, added pairwise) and selects
+// its top K_c.  With kGroups, the same wavefront goes on
+// to group refinement of its chosen chunks (the work of route_groups_kernel,
+// without a second launch or the q_bar/chunk_idx round trip through memory).
+template <typename T, int D, bool kGroups>
+__global__ __launch_bounds__(256) void route_kernel(
     const T* __restrict__ q_rot, int q_chunk0, int n_q_chunks, const float* __restrict__ chunk_sum,
-    int table_chunks, float* __restrict__ qbar, int32_t* __restrict__ chunk_idx, int n_q_heads,
-    int n_kv, int n_units, int keep_first, int window, int topk, size_t wave_bytes) {
+    const float* __restrict__ group_sum, int table_chunks, float* __restrict__ qbar,
+    int32_t* __restrict__ chunk_idx, int32_t* __restrict__ group_idx, int n_q_heads, int n_kv,
+    int keep_first, int window, int topk, int topk_groups, int gpc_shift, int units_per_block,
+    size_t wave_bytes) {
+    constexpr int kThreads = 256;
     constexpr int chunk = 64;
     constexpr int V = elem<T>::kVec;
     constexpr int VPR = D / V;              // 16-byte vectors per row
     constexpr int NRS = 64 / VPR;           // row slots per wave
-    constexpr int UNROLL = 8;
+    constexpr int UNROLL = 8;               // NRS * UNROLL divides the 64 rows of a head
+    constexpr int TB = 64;                  // table rows per LDS block
+    constexpr int TS = D + 4;               // padded LDS row stride (floats)
+    constexpr int F4 = D / 4;               // float4 per table row
+    constexpr int PF = TB * F4 / kThreads;  // float4 per thread per table block
+    static_assert((NRS * UNROLL) <= 64 && 64 % (NRS * UNROLL) == 0, "q_bar row tiling");
     extern __shared__ __align__(16) unsigned char smem_raw[];
+    float* s_tab = reinterpret_cast<float*>(smem_raw);
+    unsigned char* wave_base = smem_raw + align16(sizeof(float) * TB * TS);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int unit = blockIdx.x * (blockDim.x >> 6) + wave;
-    if (unit >= n_units) return;
-    WaveLds L = carve(smem_raw + wave * wave_bytes, D, 0, topk);
-    const int i = unit % n_q_chunks;
-    const int bh = unit / n_q_chunks;
+    const int blocks_per_head = (n_q_chunks + units_per_block - 1) / units_per_block;
+    const int bh = blockIdx.x / blocks_per_head;
+    const int first_i = (blockIdx.x % blocks_per_head) * units_per_block;
+    const int i = first_i + wave;
+    const bool active = wave < units_per_block && i < n_q_chunks;
+    const int gpc = 1 << gpc_shift;
     const int b = bh / n_kv, j = bh % n_kv;
     const int r = n_q_heads / n_kv;
-    const int c = q_chunk0 + i;
+    const int c = q_chunk0 + (active ? i : 0);
+    const int64_t unit = static_cast<int64_t>(bh) * n_q_chunks + i;
+
+    // Table rows [keep_first, hi) are needed by some wavefront of the group;
+    // the descriptor covers exactly those, so loads past them return zeros.
+    const int last_i = min(n_q_chunks, first_i + units_per_block) - 1;
+    const int hi = q_chunk0 + last_i - window;
+    const float* table = chunk_sum + static_cast<int64_t>(bh) * table_chunks * D;
+    const buf_rsrc t_rsrc =
+        make_rsrc(table, hi > 0 ? static_cast<uint32_t>(hi) * D * sizeof(float) : 0u);
+    float4 pf[PF];
+    auto fetch_block = [&](int r0) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int x = threadIdx.x + u * kThreads;
+            const uint32_t off =
+                (static_cast<uint32_t>(r0 + x / F4) * D + (x % F4) * 4) * sizeof(float);
+            pf[u] = __builtin_bit_cast(float4, buf_load16(t_rsrc, off));
+        }
+    };
+    if (keep_first < hi) fetch_block(keep_first);
 
     // 1. q_bar: mean over the r heads x chunk tokens, fixed summation order.
-    const int cv = lane % VPR, rs = lane / VPR;
-    float acc[V];
+    WaveLds L{};
+    if (active) {
+        L = carve(wave_base + wave * wave_bytes, D, kGroups ? topk : 0,
+                  kGroups && topk_groups > topk ? topk_groups : topk);
+        const int cv = lane % VPR, rs = lane / VPR;
+        float acc[V];
 #pragma unroll
-    for (int e = 0; e < V; ++e) acc[e] = 0.f;
-    const int rows = r * chunk;
-    const int64_t qtok = static_cast<int64_t>(n_q_chunks) * chunk;
-    const T* qbase = q_rot + ((static_cast<int64_t>(b) * n_q_heads + j * r) * qtok +
-                              static_cast<int64_t>(i) * chunk) * D + cv * V;
-    for (int row0 = rs; row0 < rows; row0 += NRS * UNROLL) {
-        vec16 x[UNROLL];
+        for (int e = 0; e < V; ++e) acc[e] = 0.f;
+        const int rows = r * chunk;
+        const int64_t qtok = static_cast<int64_t>(n_q_chunks) * chunk;
+        const T* qbase = q_rot + ((static_cast<int64_t>(b) * n_q_heads + j * r) * qtok +
+                                  static_cast<int64_t>(i) * chunk) * D + cv * V;
+        for (int row0 = rs; row0 < rows; row0 += NRS * UNROLL) {
+            vec16 x[UNROLL];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            const int row = row0 + u * NRS;
-            const int hh = row >> 6, tt = row & 63;
-            x[u] = row < rows ? load16(qbase + (hh * qtok + tt) * D) : vec16{{0u, 0u, 0u, 0u}};
+            for (int u = 0; u < UNROLL; ++u) {
+                const int row = row0 + u * NRS;
+                const int hh = row >> 6, tt = row & 63;
+                x[u] = load16(qbase + (hh * qtok + tt) * D);
+            }
+#pragma unroll
+            for (int u = 0; u < UNROLL; ++u) {
+                float f[V];
+                elem<T>::unpack(x[u], f);
+#pragma unroll
+                for (int e = 0; e < V; ++e) acc[e] += f[e];
+            }
         }
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            float f[V];
-            elem<T>::unpack(x[u], f);
+        for (int m = VPR; m < 64; m <<= 1)
 #pragma unroll
-            for (int e = 0; e < V; ++e) acc[e] += f[e];
+            for (int e = 0; e < V; ++e) acc[e] += __shfl_xor(acc[e], m, 64);
+        const float inv = 1.0f / static_cast<float>(rows);
+        if (rs == 0) {
+#pragma unroll
+            for (int e = 0; e < V; ++e) L.q[cv * V + e] = acc[e] * inv;
         }
-    }
+        wave_sync_lds();
+        if (lane < VPR) {
+            float* out = qbar + unit * D + cv * V;
 #pragma unroll
-    for (int m = VPR; m < 64; m <<= 1)
-#pragma unroll
-        for (int e = 0; e < V; ++e) acc[e] += __shfl_xor(acc[e], m, 64);
-    const float inv = 1.0f / static_cast<float>(rows);
-    if (rs == 0) {
-#pragma unroll
-        for (int e = 0; e < V; ++e) L.q[cv * V + e] = acc[e] * inv;
-    }
-    wave_sync_lds();
-    if (lane < VPR) {
-        float* out = qbar + static_cast<int64_t>(unit) * D + cv * V;
-#pragma unroll
-        for (int e = 0; e < V; ++e) out[e] = L.q[cv * V + e];
+            for (int e = 0; e < V; ++e) out[e] = L.q[cv * V + e];
+        }
     }
 
-    // 2. score the middle chunks [keep_first, c - window).
+    // 2. score the middle chunks [keep_first, c - window) block by block.
     int n = c - window - keep_first;
-    if (n < 0) n = 0;
-    const float* table = chunk_sum + static_cast<int64_t>(bh) * table_chunks * D;
-    for (int m0 = 0; m0 < n; m0 += 64) {
-        const int last = n - 1 - m0;
-        batch_keys<D>(L.q, table, [&](int k) { return keep_first + m0 + min(k, last); }, n - m0,
-                      L.keys + m0);
+    if (!active || n < 0) n = 0;
+    for (int r0 = keep_first; r0 < hi; r0 += TB) {
+        __syncthreads();                                 // the previous block is scored
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int x = threadIdx.x + u * kThreads;
+            *reinterpret_cast<float4*>(s_tab + (x / F4) * TS + (x % F4) * 4) = pf[u];
+        }
+        __syncthreads();
+        if (r0 + TB < hi) fetch_block(r0 + TB);
+        const int m = r0 - keep_first + lane;            // candidate ordinal of this lane
+        if (m < n) {
+            const float* row = s_tab + lane * TS;
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+            for (int f = 0; f < F4; ++f) {
+                const float4 q = *reinterpret_cast<const float4*>(L.q + f * 4);
+                const float4 x = *reinterpret_cast<const float4*>(row + f * 4);
+                a0 = fmaf(q.x, x.x, a0);
+                a1 = fmaf(q.y, x.y, a1);
+                a2 = fmaf(q.z, x.z, a2);
+                a3 = fmaf(q.w, x.w, a3);
+            }
+            L.keys[m] = select_key((a0 + a1) + (a2 + a3), keep_first + m);
+        }
     }
+    if (!active) return;
     wave_sync_lds();
 
-    // 3. top-k, ascending, -1 padded.
+    // 3. top-k chunks, ascending, -1 padded.
     const int k = n < topk ? n : topk;
     wave_select_topk(L.keys, n, k, L.sel, L.scr);
     wave_sync_lds();
-    int32_t* out = chunk_idx + static_cast<int64_t>(unit) * topk;
+    int32_t* out = chunk_idx + unit * topk;
     for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
+    if constexpr (!kGroups) return;
+
+    // 4. group refinement of the chosen chunks.
+    for (int t = lane; t < k; t += 64) L.list[t] = L.sel[t];
+    wave_sync_lds();
+    const int ng = k * gpc;
+    const float* gtab = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
+    score_candidates<D>(
+        L.q, gtab, [&](int m) { return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1)); }, ng,
+        L.keys);
+    wave_sync_lds();
+    const int kg = ng < topk_groups ? ng : topk_groups;
+    wave_select_topk(L.keys, ng, kg, L.sel, L.scr);
+    wave_sync_lds();
+    int32_t* gout = group_idx + unit * topk_groups;
+    for (int t = lane; t < topk_groups; t += 64) gout[t] = t < kg ? L.sel[t] : -1;
 }
 
 template <int D>
@@ -222,14 +317,9 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
 
     const int n = nv * gpc;
     const float* table = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
-    for (int m0 = 0; m0 < n; m0 += 64) {
-        const int last = n - 1 - m0;
-        auto row_of = [&](int k) {
-            const int mm = m0 + min(k, last);
-            return L.list[mm >> gpc_shift] * gpc + (mm & (gpc - 1));
-        };
-        batch_keys<D>(L.q, table, row_of, n - m0, L.keys + m0);
-    }
+    score_candidates<D>(
+        L.q, table, [&](int m) { return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1)); }, n,
+        L.keys);
     wave_sync_lds();
     const int k = n < topk_groups ? n : topk_groups;
     wave_select_topk(L.keys, n, k, L.sel, L.scr);
@@ -244,21 +334,72 @@ int waves_per_block(size_t wave_bytes, int max_lds) {
     return w < 1 ? 1 : (w > 4 ? 4 : w);
 }
 
-template <typename T, int D>
-hipError_t launch_chunks_t(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
-                           const float* chunk_sum, int table_chunks, float* qbar,
-                           int32_t* chunk_idx, hipStream_t stream) {
+// LDS of the fused routing block: the staged table block plus one region per
+// wavefront (q_bar, chunk list, selection, keys for the larger of the two
+// candidate lists).
+struct RouteGeom {
+    size_t wave_bytes;
+    size_t total;
+    int units_per_block;
+};
+
+inline RouteGeom route_geom(const hga_plan& plan, int n_max, bool groups) {
+    const hga_params& p = plan.p;
+    const int gpc = p.chunk / p.group;
+    const int nk = groups && p.topk_chunks * gpc > n_max ? p.topk_chunks * gpc : n_max;
+    const int ntop = groups && p.topk_groups > p.topk_chunks ? p.topk_groups : p.topk_chunks;
+    RouteGeom g;
+    g.wave_bytes = wave_lds_bytes(p.head_dim, groups ? p.topk_chunks : 0, ntop, nk);
+    const size_t tab = align16(sizeof(float) * 64 * (p.head_dim + 4));
+    g.units_per_block = 4;
+    while (g.units_per_block > 1 &&
+           tab + g.units_per_block * g.wave_bytes > static_cast<size_t>(plan.max_lds))
+        g.units_per_block >>= 1;
+    g.total = tab + g.units_per_block * g.wave_bytes;
+    return g;
+}
+
+template <typename T, int D, bool kGroups>
+hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
+                          const float* chunk_sum, const float* group_sum, int table_chunks,
+                          float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream) {
     const hga_params& p = plan.p;
     const int n_max = middle_count(p, q_chunk0 + n_q_chunks - 1);
-    const size_t wb = wave_lds_bytes(D, 0, p.topk_chunks, n_max);
-    const int wpb = waves_per_block(wb, plan.max_lds);
-    const int n_units = p.batch * p.n_kv_heads * n_q_chunks;
-    const int blocks = (n_units + wpb - 1) / wpb;
-    hipLaunchKernelGGL((route_chunks_kernel<T, D>), dim3(blocks), dim3(64 * wpb), wb * wpb, stream,
-                       static_cast<const T*>(q_rot), q_chunk0, n_q_chunks, chunk_sum,
-                       table_chunks, qbar, chunk_idx, p.n_q_heads, p.n_kv_heads, n_units,
-                       p.keep_first, recent_window(p), p.topk_chunks, wb);
+    const RouteGeom g = route_geom(plan, n_max, kGroups);
+    const int upb = g.units_per_block < n_q_chunks ? g.units_per_block : n_q_chunks;
+    const int blocks = p.batch * p.n_kv_heads * ((n_q_chunks + upb - 1) / upb);
+    const int gpc = p.chunk / p.group;
+    const int gpc_shift = gpc == 8 ? 3 : (gpc == 4 ? 2 : 1);
+    hipLaunchKernelGGL((route_kernel<T, D, kGroups>), dim3(blocks), dim3(256), g.total, stream,
+                       static_cast<const T*>(q_rot), q_chunk0, n_q_chunks, chunk_sum, group_sum,
+                       table_chunks, qbar, chunk_idx, group_idx, p.n_q_heads, p.n_kv_heads,
+                       p.keep_first, recent_window(p), p.topk_chunks, p.topk_groups, gpc_shift, upb,
+                       g.wave_bytes);
     return hipGetLastError();
+}
+
+template <bool kGroups>
+hipError_t launch_route_any(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
+                            const float* chunk_sum, const float* group_sum, int table_chunks,
+                            float* qbar, int32_t* chunk_idx, int32_t* group_idx,
+                            hipStream_t stream) {
+    const hga_params& p = plan.p;
+    if (p.dtype == HGA_F32) {
+        if (p.head_dim == 64)
+            return launch_route_t<float, 64, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+                                                      group_sum, table_chunks, qbar, chunk_idx,
+                                                      group_idx, stream);
+        return launch_route_t<float, 128, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+                                                   group_sum, table_chunks, qbar, chunk_idx,
+                                                   group_idx, stream);
+    }
+    if (p.head_dim == 64)
+        return launch_route_t<bf16_t, 64, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+                                                   group_sum, table_chunks, qbar, chunk_idx,
+                                                   group_idx, stream);
+    return launch_route_t<bf16_t, 128, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+                                                group_sum, table_chunks, qbar, chunk_idx,
+                                                group_idx, stream);
 }
 
 template <int D>
@@ -279,26 +420,28 @@ hipError_t launch_groups_t(const hga_plan& plan, const float* qbar, const int32_
 
 }  // namespace
 
-size_t route_chunks_lds_bytes(const hga_plan& plan, int n_max) {
-    return wave_lds_bytes(plan.p.head_dim, 0, plan.p.topk_chunks, n_max);
+size_t route_lds_bytes(const hga_plan& plan, int n_max, bool groups) {
+    // smallest configuration (one wavefront per block) must fit
+    const hga_params& p = plan.p;
+    const int gpc = p.chunk / p.group;
+    const int nk = groups && p.topk_chunks * gpc > n_max ? p.topk_chunks * gpc : n_max;
+    const int ntop = groups && p.topk_groups > p.topk_chunks ? p.topk_groups : p.topk_chunks;
+    return align16(sizeof(float) * 64 * (p.head_dim + 4)) +
+           wave_lds_bytes(p.head_dim, groups ? p.topk_chunks : 0, ntop, nk);
 }
 
 hipError_t launch_route_chunks(const hga_plan& plan, const void* q_rot, int q_chunk0,
                                int n_q_chunks, const float* chunk_sum, int table_chunks,
                                float* qbar, int32_t* chunk_idx, hipStream_t stream) {
-    const hga_params& p = plan.p;
-    if (p.dtype == HGA_F32) {
-        if (p.head_dim == 64)
-            return launch_chunks_t<float, 64>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
-                                              table_chunks, qbar, chunk_idx, stream);
-        return launch_chunks_t<float, 128>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
-                                           table_chunks, qbar, chunk_idx, stream);
-    }
-    if (p.head_dim == 64)
-        return launch_chunks_t<bf16_t, 64>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
-                                           table_chunks, qbar, chunk_idx, stream);
-    return launch_chunks_t<bf16_t, 128>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
-                                        table_chunks, qbar, chunk_idx, stream);
+    return launch_route_any<false>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, nullptr,
+                                   table_chunks, qbar, chunk_idx, nullptr, stream);
+}
+
+hipError_t launch_route(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
+                        const float* chunk_sum, const float* group_sum, int table_chunks,
+                        float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream) {
+    return launch_route_any<true>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, group_sum,
+                                  table_chunks, qbar, chunk_idx, group_idx, stream);
 }
 
 hipError_t launch_route_groups(const hga_plan& plan, const float* qbar, const int32_t* chunk_idx,

@@ -16,8 +16,8 @@ import torch
 
 __all__ = [
     "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
-    "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_gather_kv",
-    "hga_attend", "hga_status_string", "hga_last_error", "hga_version",
+    "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
+    "hga_gather_kv", "hga_attend", "hga_status_string", "hga_last_error", "hga_version",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -26,7 +26,7 @@ _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 
 EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
-    "hga_route_chunks", "hga_route_groups", "hga_gather_kv", "hga_attend",
+    "hga_route_chunks", "hga_route_groups", "hga_route", "hga_gather_kv", "hga_attend",
     "hga_status_string", "hga_last_error", "hga_version",
 )
 
@@ -73,6 +73,7 @@ def library() -> ctypes.CDLL:
             "hga_build_summaries": [vp, vp, i64, i32, i32, i32, vp, vp, i32, vp],
             "hga_route_chunks": [vp, vp, i32, i32, vp, i32, vp, vp, vp],
             "hga_route_groups": [vp, vp, vp, i32, i32, vp, i32, vp, vp],
+            "hga_route": [vp, vp, i32, i32, vp, vp, i32, vp, vp, vp, vp],
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
         }
@@ -200,6 +201,16 @@ def hga_route_groups(plan: Plan, qbar, chunk_idx, q_chunk0: int, group_sum, grou
     _check(library().hga_route_groups(
         plan.handle, _ptr(qbar), _ptr(chunk_idx), q_chunk0, qbar.shape[2], _ptr(group_sum),
         group_sum.shape[2] // gpc, _ptr(group_idx), _stream(stream)))
+
+
+def hga_route(plan: Plan, q_rot, q_chunk0: int, chunk_sum, group_sum, qbar, chunk_idx,
+              group_idx, stream=None):
+    """Both routing stages in one launch; same arguments and outputs as
+    hga_route_chunks followed by hga_route_groups."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_route(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(chunk_sum), _ptr(group_sum),
+        chunk_sum.shape[2], _ptr(qbar), _ptr(chunk_idx), _ptr(group_idx), _stream(stream)))
 
 
 def hga_gather_kv(plan: Plan, group_idx, q_chunk0: int, k_src, v_src, k_routed, v_routed,

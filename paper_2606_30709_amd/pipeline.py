@@ -10,8 +10,10 @@ always-visible first and recent chunks and the current 64-token block.  One
 step routes the block, gathers only its routed groups over the host link,
 attends, and appends the block's summaries (the store's "append").
 
-Both only allocate with torch and call the binding; all arithmetic runs in
-the HIP library.
+Routing runs as the single fused call ``hga_route`` by default
+(``fused_route=False`` issues ``hga_route_chunks`` then ``hga_route_groups``;
+both write bit-identical indices).  Both pipelines only allocate with torch and
+call the binding; all arithmetic runs in the HIP library.
 """
 
 from __future__ import annotations
@@ -35,9 +37,11 @@ def to_device(arr: np.ndarray, dtype: str, device="cuda", pin=False) -> torch.Te
 
 
 class PrefillPipeline:
-    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None):
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
+                 fused_route: bool = True):
         assert not w.decode_block
         self.w = w
+        self.fused_route = fused_route
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
         nc = w.n_chunks
@@ -61,6 +65,10 @@ class PrefillPipeline:
                                 self.group_sum, stream=stream)
 
     def route(self, stream=None):
+        if self.fused_route:
+            hga.hga_route(self.plan, self.q, 0, self.chunk_sum, self.group_sum, self.qbar,
+                          self.chunk_idx, self.group_idx, stream=stream)
+            return
         hga.hga_route_chunks(self.plan, self.q, 0, self.chunk_sum, self.qbar, self.chunk_idx,
                              stream=stream)
         hga.hga_route_groups(self.plan, self.qbar, self.chunk_idx, 0, self.group_sum,
@@ -84,9 +92,11 @@ class PrefillPipeline:
 class DecodePipeline:
     """One query block (the last chunk of the workload) after a host-resident history."""
 
-    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None):
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
+                 fused_route: bool = True):
         assert w.decode_block
         self.w = w
+        self.fused_route = fused_route
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
         f32, i32 = torch.float32, torch.int32
@@ -135,6 +145,10 @@ class DecodePipeline:
         return 2 * n * self.w.group * self.w.head_dim * self.w.elem_bytes
 
     def route(self, stream=None):
+        if self.fused_route:
+            hga.hga_route(self.plan, self.q, self.c, self.chunk_sum, self.group_sum, self.qbar,
+                          self.chunk_idx, self.group_idx, stream=stream)
+            return
         hga.hga_route_chunks(self.plan, self.q, self.c, self.chunk_sum, self.qbar,
                              self.chunk_idx, stream=stream)
         hga.hga_route_groups(self.plan, self.qbar, self.chunk_idx, self.c, self.group_sum,

@@ -20,8 +20,8 @@ def _declared_functions():
 
 def test_header_declares_the_five_calls():
     names = _declared_functions()
-    for n in ("hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_gather_kv",
-              "hga_attend"):
+    for n in ("hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
+              "hga_gather_kv", "hga_attend"):
         assert n in names
     assert set(names) == set(hga.EXPORTED_SYMBOLS)
 
@@ -78,6 +78,7 @@ def test_calls_reject_null_plan():
     assert lib.hga_build_summaries(None, None, 0, 0, 0, 0, None, None, 0, None) == -1
     assert lib.hga_route_chunks(None, None, 0, 0, None, 0, None, None, None) == -1
     assert lib.hga_route_groups(None, None, None, 0, 0, None, 0, None, None) == -1
+    assert lib.hga_route(None, None, 0, 0, None, None, 0, None, None, None, None) == -1
     assert lib.hga_gather_kv(None, None, 0, 0, None, None, 0, 0, None, None, None) == -1
     assert lib.hga_attend(None, None, 0, 0, None, None, 0, None, None, None, None, None, None,
                           None) == -1

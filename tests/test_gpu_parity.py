@@ -216,6 +216,71 @@ def test_determinism_bitwise(hga):
                            b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
 
 
+# ---------------------------------------------------------- fused routing ---
+
+def _route_both_ways(hga, plan, q, q_chunk0, cs, gs, nq, w):
+    """Run hga_route_chunks + hga_route_groups and hga_route on the same inputs."""
+    B, Hkv, d = w.batch, w.n_kv_heads, w.head_dim
+    outs = []
+    for fused in (False, True):
+        qbar = torch.full((B, Hkv, nq, d), float("nan"), device="cuda")
+        ci = torch.full((B, Hkv, nq, w.topk_chunks), -7, dtype=torch.int32, device="cuda")
+        gi = torch.full((B, Hkv, nq, w.topk_groups), -7, dtype=torch.int32, device="cuda")
+        if fused:
+            hga.hga_route(plan, q, q_chunk0, cs, gs, qbar, ci, gi)
+        else:
+            hga.hga_route_chunks(plan, q, q_chunk0, cs, qbar, ci)
+            hga.hga_route_groups(plan, qbar, ci, q_chunk0, gs, gi)
+        outs.append((qbar, ci, gi))
+    torch.cuda.synchronize()
+    (qa, ca, ga), (qf, cf, gf) = outs
+    assert torch.equal(qa.view(torch.int32), qf.view(torch.int32))
+    assert torch.equal(ca, cf)
+    assert torch.equal(ga, gf)
+    assert (ca != -7).all() and (ga != -7).all()
+    return ca, ga
+
+
+FUSED_CASES = dict(SMALL, odd_37=W_("smalllm", batch=1, seq_len=37 * 64, topk_chunks=5,
+                                    topk_groups=11))
+
+
+@pytest.mark.parametrize("key", list(FUSED_CASES))
+def test_fused_route_equals_separate_calls(hga, key):
+    """hga_route writes exactly what hga_route_chunks + hga_route_groups write,
+    for the whole sequence and for a query block starting mid-sequence."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = FUSED_CASES[key]
+    _say(f"[fused-route] {key}")
+    pipe = PrefillPipeline(w, W.generate(w))
+    pipe.summaries()
+    ca_all, ga_all = _route_both_ways(hga, pipe.plan, pipe.q, 0, pipe.chunk_sum,
+                                      pipe.group_sum, w.n_chunks, w)
+    # a ragged query block [c0, c0 + 5) of the same sequence routes as it did
+    # inside the whole sequence
+    c0 = w.n_chunks // 2 + 1
+    n = min(5, w.n_chunks - c0)
+    qb = pipe.q[:, :, c0 * w.chunk:(c0 + n) * w.chunk].contiguous()
+    ca, ga = _route_both_ways(hga, pipe.plan, qb, c0, pipe.chunk_sum, pipe.group_sum, n, w)
+    assert torch.equal(ca, ca_all[:, :, c0:c0 + n])
+    assert torch.equal(ga, ga_all[:, :, c0:c0 + n])
+
+
+def test_fused_route_decode_and_full_size(hga):
+    from paper_2606_30709_amd.pipeline import DecodePipeline, PrefillPipeline
+    w = W.preset("decode64k")
+    _say("[fused-route] decode64k")
+    pipe = DecodePipeline(w, W.generate(w))
+    _route_both_ways(hga, pipe.plan, pipe.q, pipe.c, pipe.chunk_sum, pipe.group_sum, 1, w)
+    for key in ("smalllm", "qwen32k"):
+        w = W.preset(key)
+        _say(f"[fused-route] {key}")
+        pipe = PrefillPipeline(w, W.generate(w))
+        pipe.summaries()
+        _route_both_ways(hga, pipe.plan, pipe.q, 0, pipe.chunk_sum, pipe.group_sum,
+                         w.n_chunks, w)
+
+
 # ----------------------------------------------------------------- decode ---
 
 def _decode_check(hga, w):
