@@ -111,6 +111,20 @@ __device__ __forceinline__ int swz_v(int r) {
         return swz_k<D>(r);
 }
 
+// x and the value of lane l ^ 32 combined, without an LDS round trip:
+// v_permlane32_swap hands each lane of one half the other half's value (the
+// two results hold (partner, own) in lanes 0..31 and (own, partner) above).
+__device__ __forceinline__ float max_xor32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float add_xor32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ bf16x8_t lds_frag(const bf16_t* p) {
     return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const vec16*>(p));
 }
@@ -371,7 +385,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
 #pragma unroll
             for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[n][e]);
         }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * scale;
+        tmax = max_xor32(tmax) * scale;
         const float m_new = fmaxf(m_run, tmax);
         const float m_use = m_new == -INFINITY ? 0.f : m_new;
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
@@ -420,7 +434,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     step(0, BoolTag<true>{});
     for (int tile = 1; tile < n_tiles; ++tile) step(tile, BoolTag<false>{});
 
-    float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    float l_tot = add_xor32(l_run);
     __syncthreads();  // LDS stages are dead from here on (every copy was waited for)
     if (KS == 2) {
         float* mine = reinterpret_cast<float*>(smem) + (qt_local * 64 + lane) * (NDT * 16 + 2);

@@ -189,10 +189,14 @@ __device__ inline void wave_select_topk_regs(const uint64_t* keys, int n, int k,
     if (lane < k) sel[rank] = mine;
 }
 
-// Dispatch on size; both forms select the same keys.
+// Dispatch on size; every form selects the same keys.
 __device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, int* scratch) {
-    if (n <= 64 * 4 && k <= 64)
+    if (k <= 64 && n <= 64 * 4)
         wave_select_topk_regs<4>(keys, n, k, sel);
+    else if (k <= 64 && n <= 64 * 8)
+        wave_select_topk_regs<8>(keys, n, k, sel);
+    else if (k <= 64 && n <= 64 * 16)
+        wave_select_topk_regs<16>(keys, n, k, sel);
     else
         wave_select_topk_lds(keys, n, k, sel, scratch);
 }

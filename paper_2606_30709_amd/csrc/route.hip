@@ -142,7 +142,7 @@ __global__ __launch_bounds__(256) void route_kernel(
     constexpr int V = elem<T>::kVec;
     constexpr int VPR = D / V;              // 16-byte vectors per row
     constexpr int NRS = 64 / VPR;           // row slots per wave
-    constexpr int UNROLL = 8;               // NRS * UNROLL divides the 64 rows of a head
+    constexpr int UNROLL = 64 / NRS < 16 ? 64 / NRS : 16;  // NRS * UNROLL divides 64 rows
     constexpr int TB = 64;                  // table rows per LDS block
     constexpr int TS = D + 4;               // padded LDS row stride (floats)
     constexpr int F4 = D / 4;               // float4 per table row
