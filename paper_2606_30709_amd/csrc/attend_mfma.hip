@@ -148,9 +148,174 @@ struct Layout {
     static constexpr uint32_t kBytes = kGidOffset + kMaxGroupSlots * 4;
 };
 
-// D: head dim; KS: wavefronts sharing one query tile (each takes one 32-key
-// half of every key tile); NS: LDS stages of the key-tile ring; NW:
-// wavefronts per workgroup (NW / KS query tiles per workgroup).
+// Per-key-tile arithmetic shared by both kernels, for one wavefront:
+//   S^T = K.Q^T over its 32-key sub-tile(s), the causal mask (current chunk)
+//   or the routed-row mask (partial routed tile), the online-softmax update
+//   of (m_run, l_run, oacc), and O^T += V^T.P^T.
+// sK/sV: the staged tile; ksplit: this wave's key half when KS == 2;
+// t: this lane's query token; rt_row0: first routed row of the tile.
+template <int D, int KS, bool kCurrent>
+__device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
+                                          const bf16x8_t (&qf)[D / 16], f32x16_t (&oacc)[D / 32],
+                                          float& m_run, float& l_run, int ksplit, int t,
+                                          bool partial, int rt_row0, const int* s_gid,
+                                          int routed_rows, int topk_groups, int group_shift,
+                                          int id_limit) {
+    constexpr int NDT = D / 32, NKS = D / 16, NST = 2 / KS;
+    const int lane = threadIdx.x & 63;
+    const int half = lane >> 5, col = lane & 31;
+    const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
+    f32x16_t sacc[NST];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int n = 0; n < NST; ++n) {
+        const int st = KS == 2 ? ksplit : n;
+        const int krow = st * 32 + col;
+        bf16x8_t kf[NKS];
+#pragma unroll
+        for (int kk = 0; kk < NKS; ++kk)
+            kf[kk] = lds_frag(sK + krow * D + ((2 * kk + half) ^ swz_k<D>(col)) * 8);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[n][e] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < NKS; ++kk)
+            sacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sacc[n], 0, 0, 0);
+        if (kCurrent) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                sacc[n][e] = key > t ? -INFINITY : sacc[n][e];
+            }
+        } else if (partial) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int row = rt_row0 + st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                const int slot = min(row >> group_shift, topk_groups - 1);
+                const int id = s_gid[slot];
+                const bool ok = row < routed_rows && id >= 0 && id < id_limit;
+                sacc[n][e] = ok ? sacc[n][e] : -INFINITY;
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[n][e]);
+    }
+    tmax = max_xor32(tmax) * scale;
+    const float m_new = fmaxf(m_run, tmax);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    l_run *= alpha;
+    // the output needs rescaling only where the running maximum moved
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+    }
+    m_run = m_new;
+#pragma unroll
+    for (int n = 0; n < NST; ++n) {
+        const int st = KS == 2 ? ksplit : n;
+#pragma unroll
+        for (int kap = 0; kap < 2; ++kap) {
+            bf16x8_t pf;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[n][kap * 8 + e], scale, -m_use));
+                l_run += pv;
+                pf[e] = static_cast<__bf16>(pv);
+            }
+            // V^T operand: keys st*32 + kap*16 + {half*4 + 0..3, 8 + half*4 + 0..3}
+            // at dimension dt*32 + col; each 16-lane group points at
+            // 4 keys x 16 dimensions.
+            const int key0 = st * 32 + kap * 16 + half * 4 + ((lane & 15) >> 2);
+            const int dcol = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
+            const int vs0 = swz_v<D>(key0), vs1 = swz_v<D>(key0 + 8);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) {
+                const int e0 = dt * 32 + dcol;
+                const bf16_t* vp0 = sV + key0 * D + (((e0 >> 3) ^ vs0) << 3) + (e0 & 7);
+                const bf16_t* vp1 = sV + (key0 + 8) * D + (((e0 >> 3) ^ vs1) << 3) + (e0 & 7);
+                const i16x4_t lo = lds_read_tr16(vp0);
+                const i16x4_t hi = lds_read_tr16(vp1);
+                const bf16x8_t a = __builtin_bit_cast(
+                    bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, oacc[dt], 0, 0, 0);
+            }
+        }
+    }
+}
+
+// Whether routed tile rows [rt_row0, rt_row0 + 64) include any row to mask.
+__device__ __forceinline__ bool routed_tile_partial(int rt_row0, const int* s_gid, int routed_rows,
+                                                    int topk_groups, int group_shift,
+                                                    int id_limit) {
+    bool partial = rt_row0 + KT > routed_rows;
+    for (int g = rt_row0 >> group_shift; g < (rt_row0 + KT) >> group_shift && g < topk_groups;
+         ++g) {
+        const int id = s_gid[g];
+        partial |= !(id >= 0 && id < id_limit);
+    }
+    return partial;
+}
+
+// Combine the two key halves of a query tile (KS == 2) through LDS (`area`:
+// QT * 64 * NDT*16 floats, `ml`: QT * 128 floats, both free), then store the
+// normalised output and the log-sum-exp.  Every wave of the workgroup calls.
+template <int D, int KS, int QT>
+__device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_run, float l_run,
+                                            float* area, float* ml_area, int qt_local, int ksplit,
+                                            bool qactive, bool bad, bf16_t* orow, float* lse_at) {
+    constexpr int NDT = D / 32;
+    const int lane = threadIdx.x & 63, half = lane >> 5;
+    float l_tot = add_xor32(l_run);
+    if (KS == 2) {
+        // element k of this lane at [qt_local][k][lane]: lanes contiguous
+        float* mine = area + qt_local * (NDT * 16 * 64) + lane;
+        float* ml = ml_area + qt_local * 128 + lane;
+        if (ksplit == 1) {
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) mine[(dt * 16 + e) * 64] = oacc[dt][e];
+            ml[0] = m_run;
+            ml[64] = l_tot;
+        }
+        __syncthreads();
+        if (ksplit == 0) {
+            const float mb = ml[0], lb = ml[64];
+            const float m = fmaxf(m_run, mb);
+            const float mu = m == -INFINITY ? 0.f : m;
+            const float fa = __builtin_amdgcn_exp2f(m_run - mu), fb = __builtin_amdgcn_exp2f(mb - mu);
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    oacc[dt][e] = oacc[dt][e] * fa + mine[(dt * 16 + e) * 64] * fb;
+            l_tot = l_tot * fa + lb * fb;
+            m_run = m;
+        }
+    }
+    if (!qactive || ksplit != 0) return;
+    const float inv = bad ? NAN : 1.0f / l_tot;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+            const int d0 = dt * 32 + g4 * 8 + half * 4;
+            typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+            bf16x4_t o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(oacc[dt][g4 * 4 + e] * inv);
+            *reinterpret_cast<bf16x4_t*>(orow + d0) = o;
+        }
+    if (lse_at && half == 0) *lse_at = bad ? NAN : (m_run + log2f(l_tot)) * 0.6931471805599453f;
+}
+
+// D: head dim; KS: wavefronts sharing one query tile (each
+// takes one 32-key half of every key tile); NS: LDS stages of the key-tile
+// ring; NW: wavefronts per workgroup (NW / KS query tiles per workgroup).
+// One workgroup per (unit, part); its query rows and group ids are copied
+// with the first tiles, then the key tiles stream through the ring.
 template <int D, int KS, int NS, int NW>
 __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const bf16_t* __restrict__ q_rot, int q_chunk0, int n_q_chunks,
@@ -166,7 +331,6 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     constexpr int NKS = D / 16;                  // k-steps of Q.K^T
     constexpr int CPR = D / 8;                   // 16-byte chunks per row
     constexpr int QT = NW / KS;                  // query tiles per workgroup
-    constexpr int NST = 2 / KS;                  // 32-key sub-tiles per wave per tile
     constexpr int KI = kTileBytes / 1024 / NW;   // copies per wave per tile, for K (and V)
     constexpr int LPT = 2 * KI;                  // loads per wave per tile
     constexpr int QI = QT * 32 * kRowBytes / 1024 / NW;  // copies per wave for the query rows
@@ -174,6 +338,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     static_assert(KI >= 1 && QI >= 1 && GI >= 1, "copy split");
     static_assert(QT * 32 * kRowBytes <= kStageBytes, "query rows fit one stage");
     static_assert(NS >= 2 && NS <= 4, "stages");
+    static_assert(KS == 1 || QT * 64 * NDT * 16 * 4 <= NS * kStageBytes, "merge area");
 
     extern __shared__ __align__(16) unsigned char smem[];
     const uint32_t lds0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(smem));
@@ -297,7 +462,6 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     for (int s = 0; s < NS - 1; ++s)
         if (s < n_tiles) issue(s, s);
 
-    const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
     f32x16_t oacc[NDT];
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -306,10 +470,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     float m_run = -INFINITY, l_run = 0.f;  // m_run in scaled (log2) units
     bf16x8_t qf[NKS];
 
-    // One key tile: wait for its copies, issue a later tile's, then
-    // S^T = K.Q^T, the online softmax update and O^T += V^T.P^T.  The current
-    // chunk (tile 0, under the causal mask) is a separate instantiation so the
-    // other tiles carry no mask work.
+    // One key tile: wait for its copies, issue a later tile's, then the
+    // tile's arithmetic.  The current chunk (tile 0, under the causal mask)
+    // is a separate instantiation so the other tiles carry no mask work.
     auto step = [&](int tile, auto current_tag) {
         constexpr bool kCurrent = decltype(current_tag)::value;
         // this wave's copies of `tile` are done once at most `ahead` later
@@ -338,153 +501,29 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
         const bf16_t* sK = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes);
         const bf16_t* sV = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes + kTileBytes);
         const int rt_row0 = (tile - 1 - n_vis) * KT;
-
-        // rows that must be masked in a routed tile: past the buffer or of an invalid slot
-        bool partial = false;
-        if (!kCurrent && tile > n_vis) {
-            partial = rt_row0 + KT > routed_rows;
-            for (int g = rt_row0 >> group_shift;
-                 g < (rt_row0 + KT) >> group_shift && g < topk_groups; ++g) {
-                const int id = s_gid[g];
-                partial |= !(id >= 0 && id < c * gpc);
-            }
-        }
-        if (!qactive) return;
-
-        f32x16_t sacc[NST];
-        float tmax = -INFINITY;
-#pragma unroll
-        for (int n = 0; n < NST; ++n) {
-            const int st = KS == 2 ? ksplit : n;
-            const int krow = st * 32 + col;
-            bf16x8_t kf[NKS];
-#pragma unroll
-            for (int kk = 0; kk < NKS; ++kk)
-                kf[kk] = lds_frag(sK + krow * D + ((2 * kk + half) ^ swz_k<D>(col)) * 8);
-#pragma unroll
-            for (int e = 0; e < 16; ++e) sacc[n][e] = 0.f;
-#pragma unroll
-            for (int kk = 0; kk < NKS; ++kk)
-                sacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sacc[n], 0, 0, 0);
-            if (kCurrent) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                    sacc[n][e] = key > t ? -INFINITY : sacc[n][e];
-                }
-            } else if (partial) {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    const int row = rt_row0 + st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                    const int slot = min(row >> group_shift, topk_groups - 1);
-                    const int id = s_gid[slot];
-                    const bool ok = row < routed_rows && id >= 0 && id < c * gpc;
-                    sacc[n][e] = ok ? sacc[n][e] : -INFINITY;
-                }
-            }
-#pragma unroll
-            for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[n][e]);
-        }
-        tmax = max_xor32(tmax) * scale;
-        const float m_new = fmaxf(m_run, tmax);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-        l_run *= alpha;
-        // the output needs rescaling only where the running maximum moved
-        if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
-        }
-        m_run = m_new;
-#pragma unroll
-        for (int n = 0; n < NST; ++n) {
-            const int st = KS == 2 ? ksplit : n;
-#pragma unroll
-            for (int kap = 0; kap < 2; ++kap) {
-                bf16x8_t pf;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float pv =
-                        __builtin_amdgcn_exp2f(fmaf(sacc[n][kap * 8 + e], scale, -m_use));
-                    l_run += pv;
-                    pf[e] = static_cast<__bf16>(pv);
-                }
-                // V^T operand: keys st*32 + kap*16 + {half*4 + 0..3, 8 + half*4 + 0..3}
-                // at dimension dt*32 + col; each 16-lane group points at
-                // 4 keys x 16 dimensions.
-                const int key0 = st * 32 + kap * 16 + half * 4 + ((lane & 15) >> 2);
-                const int dcol = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
-                const int vs0 = swz_v<D>(key0), vs1 = swz_v<D>(key0 + 8);
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    const int e0 = dt * 32 + dcol;
-                    const bf16_t* vp0 = sV + key0 * D + (((e0 >> 3) ^ vs0) << 3) + (e0 & 7);
-                    const bf16_t* vp1 = sV + (key0 + 8) * D + (((e0 >> 3) ^ vs1) << 3) + (e0 & 7);
-                    const i16x4_t lo = lds_read_tr16(vp0);
-                    const i16x4_t hi = lds_read_tr16(vp1);
-                    const bf16x8_t a = __builtin_bit_cast(
-                        bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-                    oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, oacc[dt], 0, 0, 0);
-                }
-            }
-        }
+        const bool partial =
+            !kCurrent && tile > n_vis &&
+            routed_tile_partial(rt_row0, s_gid, routed_rows, topk_groups, group_shift, c * gpc);
+        if (qactive)
+            tile_math<D, KS, kCurrent>(sK, sV, qf, oacc, m_run, l_run, ksplit, t, partial, rt_row0,
+                                       s_gid, routed_rows, topk_groups, group_shift, c * gpc);
     };
     step(0, BoolTag<true>{});
     for (int tile = 1; tile < n_tiles; ++tile) step(tile, BoolTag<false>{});
 
-    float l_tot = add_xor32(l_run);
     __syncthreads();  // LDS stages are dead from here on (every copy was waited for)
-    if (KS == 2) {
-        float* mine = reinterpret_cast<float*>(smem) + (qt_local * 64 + lane) * (NDT * 16 + 2);
-        if (ksplit == 1) {
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) mine[dt * 16 + e] = oacc[dt][e];
-            mine[NDT * 16] = m_run;
-            mine[NDT * 16 + 1] = l_tot;
-        }
-        __syncthreads();
-        if (ksplit == 0) {
-            const float mb = mine[NDT * 16], lb = mine[NDT * 16 + 1];
-            const float m = fmaxf(m_run, mb);
-            const float mu = m == -INFINITY ? 0.f : m;
-            const float fa = __builtin_amdgcn_exp2f(m_run - mu), fb = __builtin_amdgcn_exp2f(mb - mu);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) oacc[dt][e] = oacc[dt][e] * fa + mine[dt * 16 + e] * fb;
-            l_tot = l_tot * fa + lb * fb;
-            m_run = m;
-        }
-    }
-    if (!qactive || ksplit != 0) return;
-
-    const float inv = bad ? NAN : 1.0f / l_tot;
-    bf16_t* orow = out + qrow * D;
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-            const int d0 = dt * 32 + g4 * 8 + half * 4;
-            typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-            bf16x4_t o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(oacc[dt][g4 * 4 + e] * inv);
-            *reinterpret_cast<bf16x4_t*>(orow + d0) = o;
-        }
-    if (lse && half == 0) lse[qrow] = bad ? NAN : (m_run + log2f(l_tot)) * 0.6931471805599453f;
+    finish_rows<D, KS, QT>(oacc, m_run, l_run, reinterpret_cast<float*>(smem),
+                           reinterpret_cast<float*>(smem) + QT * 64 * NDT * 16, qt_local, ksplit,
+                           qactive, bad, out + qrow * D, lse ? lse + qrow : nullptr);
 }
 
 template <int D, int KS, int NS, int NW>
-hipError_t launch_mfma_t(int grid, hipStream_t stream, const bf16_t* q_rot, int q_chunk0,
-                         int n_q_chunks, const bf16_t* k_res, const bf16_t* v_res,
+hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, const bf16_t* q_rot,
+                         int q_chunk0, int n_q_chunks, const bf16_t* k_res, const bf16_t* v_res,
                          int64_t res_tokens, const int32_t* res_slot, const bf16_t* k_routed,
                          const bf16_t* v_routed, const int32_t* group_idx, bf16_t* out, float* lse,
-                         int n_q_heads, int n_kv, int group_shift, int keep_first, int window,
-                         int topk_groups, int wg_per_unit, int n_blocks) {
+                         int group_shift, int wg_per_unit, int n_items) {
+    const hga_params& p = plan.p;
     constexpr uint32_t kLds = Layout<D, NS>::kBytes;
     static bool configured = false;  // per instantiation (the limit is a function attribute)
     if (!configured) {
@@ -494,10 +533,12 @@ hipError_t launch_mfma_t(int grid, hipStream_t stream, const bf16_t* q_rot, int 
         if (e != hipSuccess) return e;
         configured = true;
     }
+    const int grid = (n_items + kXcds - 1) / kXcds * kXcds;
     hipLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW>), dim3(grid), dim3(NW * 64), kLds,
                        stream, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
-                       k_routed, v_routed, group_idx, out, lse, n_q_heads, n_kv, group_shift,
-                       keep_first, window, topk_groups, wg_per_unit, n_blocks);
+                       k_routed, v_routed, group_idx, out, lse, p.n_q_heads, p.n_kv_heads,
+                       group_shift, p.keep_first, recent_window(p), p.topk_groups, wg_per_unit,
+                       n_items);
     return hipGetLastError();
 }
 
@@ -515,26 +556,27 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     // each with half of every key tile; otherwise four query tiles per group.
     const bool one_head = nqt <= 2;
     const int wg_per_unit = one_head ? 1 : (nqt + 3) / 4;
-    const int64_t n_blocks64 =
+    const int64_t n_items64 =
         static_cast<int64_t>(p.batch) * p.n_kv_heads * n_q_chunks * wg_per_unit;
-    if (n_blocks64 > (int64_t(1) << 30)) return hipErrorInvalidConfiguration;
-    const int n_blocks = static_cast<int>(n_blocks64);
-    const int grid = (n_blocks + kXcds - 1) / kXcds * kXcds;
+    if (n_items64 > (int64_t(1) << 30)) return hipErrorInvalidConfiguration;
+    const int n_items = static_cast<int>(n_items64);
     const int group_shift = p.group == 8 ? 3 : (p.group == 16 ? 4 : 5);
-#define HGA_MFMA(DD, KSV, NSV, NWV)                                                            \
-    return launch_mfma_t<DD, KSV, NSV, NWV>(                                                   \
-        grid, stream, static_cast<const bf16_t*>(q_rot), q_chunk0, n_q_chunks,                 \
-        static_cast<const bf16_t*>(k_res), static_cast<const bf16_t*>(v_res), res_tokens,      \
-        res_slot, static_cast<const bf16_t*>(k_routed), static_cast<const bf16_t*>(v_routed),  \
-        group_idx, static_cast<bf16_t*>(out), lse, p.n_q_heads, p.n_kv_heads, group_shift,     \
-        p.keep_first, recent_window(p), p.topk_groups, wg_per_unit, n_blocks)
+    const bf16_t* q = static_cast<const bf16_t*>(q_rot);
+    const bf16_t* kr = static_cast<const bf16_t*>(k_res);
+    const bf16_t* vr = static_cast<const bf16_t*>(v_res);
+    const bf16_t* kt = static_cast<const bf16_t*>(k_routed);
+    const bf16_t* vt = static_cast<const bf16_t*>(v_routed);
+    bf16_t* o = static_cast<bf16_t*>(out);
+#define HGA_ARGS                                                                                 \
+    plan, stream, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot, kt, vt, group_idx, o,   \
+        lse, group_shift, wg_per_unit, n_items
     if (p.head_dim == 64) {
-        if (one_head) HGA_MFMA(64, 2, 2, 4);
-        HGA_MFMA(64, 1, 2, 4);
+        if (one_head) return launch_mfma_t<64, 2, 2, 4>(HGA_ARGS);
+        return launch_mfma_t<64, 1, 2, 4>(HGA_ARGS);
     }
-    if (one_head) HGA_MFMA(128, 2, 2, 4);
-    HGA_MFMA(128, 1, 2, 4);
-#undef HGA_MFMA
+    if (one_head) return launch_mfma_t<128, 2, 2, 4>(HGA_ARGS);
+    return launch_mfma_t<128, 1, 2, 4>(HGA_ARGS);
+#undef HGA_ARGS
 }
 
 hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,
