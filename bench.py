@@ -6,16 +6,17 @@ group summaries, chunk routing, group refinement, gather of the routed K/V,
 and exact attention (inputs already resident in HBM).  The two routing stages
 run as the single call hga_route (four C-ABI calls per step);
 --separate-route issues hga_route_chunks and hga_route_groups instead (five
-calls, bit-identical indices).  The
-default workload is the SmallLM-shaped prefill (B4, 8/8 heads, d64, 8192
-tokens, bf16, C64 G16, first chunk hot, K_c 3, K_g 4 -> 3.125% of the
-context fetched by the last chunk).
+calls, bit-identical indices).  The default workload is the SmallLM-shaped
+prefill (B4, 8/8 heads, d64, 8192 tokens, bf16, C64 G16, first chunk hot,
+K_c 3, K_g 4 -> 3.125% of the context fetched by the last chunk).
 
-Prints one JSON line.  The step rate comes from an event-free timed loop
-(wall clock between synchronizations); HIP events on the launch stream
-bracket the dominant kernel (attention) in every timed step, and its
-algorithmic bytes over its mean duration give the roofline entry.  A second
-pass with events between all calls gives the per-stage breakdown.
+Prints one JSON line.  The step rate comes from the wall clock between two
+synchronizations around the timed steps.  In every timed step the dominant
+kernel (attention) is launched through hga_attend_timed, whose dispatch
+records a pair of HIP events at the kernel's own start and end on the
+launch stream; its algorithmic bytes over the mean duration give the
+roofline entry.  A second pass with events between all calls gives the
+per-stage breakdown of the other kernels.
 The float64 oracle timed on the host cores over a bounded sample of the same
 workload gives the CPU baseline.
 """
@@ -218,6 +219,10 @@ def main():
                                        pipe.v_routed, stream=sh)
     attend = lambda: hga.hga_attend(p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
                                     pipe.group_idx, pipe.out, pipe.lse, stream=sh)
+    # the dominant kernel's own dispatch records these (hga_attend_timed)
+    attend_timed = lambda e0, e1: hga.hga_attend_timed(
+        p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed, pipe.group_idx, pipe.out,
+        e0, e1, lse=pipe.lse, stream=sh)
     if args.separate_route:
         STAGES = STAGES_SEPARATE
         calls = (
@@ -240,13 +245,16 @@ def main():
             f()
     torch.cuda.synchronize()
 
-    # Timed region: K steps, with HIP events bracketing only the dominant
-    # kernel (attention) on the launch stream; whole-step rate from the wall
-    # clock between two synchronizations.
+    # Timed region: K steps; the dominant kernel (attention) records a pair of
+    # HIP events at its own dispatch start and end in every step; whole-step
+    # rate from the wall clock between two synchronizations.
     K = args.steps
     att = len(calls) - 1
     ev_a = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             for _ in range(K)]
+    for a, b in ev_a:  # events exist once recorded; the kernel dispatch re-records them
+        a.record(stream)
+        b.record(stream)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -254,9 +262,7 @@ def main():
     for s in range(K):
         for n, f in enumerate(calls):
             if n == att:
-                ev_a[s][0].record(stream)
-                f()
-                ev_a[s][1].record(stream)
+                attend_timed(ev_a[s][0], ev_a[s][1])
             else:
                 f()
     ev1.record(stream)
@@ -325,8 +331,9 @@ def main():
             "seed": inp["seed"],
         },
         "gpu_ms_per_step_events": round(gpu_step_ms, 4),
-        "stage_timing": ("attend: HIP events around it in every timed step; other stages: "
-                         "a second pass of the same steps with events between all calls"),
+        "stage_timing": ("attend: HIP events recorded by its own dispatch in every timed step; "
+                         "other stages: a second pass of the same steps with events between "
+                         "all calls"),
         "stages": stages,
         "route_calls": "separate" if args.separate_route else "fused",
         "roofline": roofline,

@@ -232,6 +232,18 @@ hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                       const void* v_routed, const int32_t* group_idx, void* out, float* lse,
                       void* stream);
 
+/* hga_attend for measurement: the same work and results, and the attention
+ * kernel's own dispatch records start_event when it begins and stop_event
+ * when it ends (both hipEvent_t created by the caller; either may be NULL).
+ * hipEventElapsedTime between them is the kernel's duration, without the
+ * queue time that separate event records on the stream would add.  Same
+ * arguments, requirements and errors as hga_attend otherwise. */
+hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const void* k_res, const void* v_res,
+                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                            void* start_event, void* stop_event, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* hga_status_string(int32_t status);
 

@@ -36,6 +36,7 @@
 // pointing at 4 keys x 16 dimensions hand each lane 4 keys of one dimension.
 // All global reads go through buffer descriptors: offsets past a buffer's
 // end read as zero.
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include "attend_common.hpp"
@@ -518,11 +519,12 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
 }
 
 template <int D, int KS, int NS, int NW>
-hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, const bf16_t* q_rot,
-                         int q_chunk0, int n_q_chunks, const bf16_t* k_res, const bf16_t* v_res,
-                         int64_t res_tokens, const int32_t* res_slot, const bf16_t* k_routed,
-                         const bf16_t* v_routed, const int32_t* group_idx, bf16_t* out, float* lse,
-                         int group_shift, int wg_per_unit, int n_items) {
+hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev_start,
+                         hipEvent_t ev_stop, const bf16_t* q_rot, int q_chunk0, int n_q_chunks,
+                         const bf16_t* k_res, const bf16_t* v_res, int64_t res_tokens,
+                         const int32_t* res_slot, const bf16_t* k_routed, const bf16_t* v_routed,
+                         const int32_t* group_idx, bf16_t* out, float* lse, int group_shift,
+                         int wg_per_unit, int n_items) {
     const hga_params& p = plan.p;
     constexpr uint32_t kLds = Layout<D, NS>::kBytes;
     static bool configured = false;  // per instantiation (the limit is a function attribute)
@@ -534,11 +536,11 @@ hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, const bf16_t*
         configured = true;
     }
     const int grid = (n_items + kXcds - 1) / kXcds * kXcds;
-    hipLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW>), dim3(grid), dim3(NW * 64), kLds,
-                       stream, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
-                       k_routed, v_routed, group_idx, out, lse, p.n_q_heads, p.n_kv_heads,
-                       group_shift, p.keep_first, recent_window(p), p.topk_groups, wg_per_unit,
-                       n_items);
+    hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW>), dim3(grid), dim3(NW * 64), kLds,
+                          stream, ev_start, ev_stop, 0, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+                          res_tokens, res_slot, k_routed, v_routed, group_idx, out, lse,
+                          p.n_q_heads, p.n_kv_heads, group_shift, p.keep_first, recent_window(p),
+                          p.topk_groups, wg_per_unit, n_items);
     return hipGetLastError();
 }
 
@@ -548,7 +550,8 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
                               int n_q_chunks, const void* k_res, const void* v_res,
                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                               const void* v_routed, const int32_t* group_idx, void* out,
-                              float* lse, hipStream_t stream) {
+                              float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
+                              hipStream_t stream) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int nqt = 2 * r;
@@ -568,7 +571,7 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     const bf16_t* vt = static_cast<const bf16_t*>(v_routed);
     bf16_t* o = static_cast<bf16_t*>(out);
 #define HGA_ARGS                                                                                 \
-    plan, stream, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot, kt, vt, group_idx, o,   \
+    plan, stream, ev_start, ev_stop, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot, kt, vt, group_idx, o,   \
         lse, group_shift, wg_per_unit, n_items
     if (p.head_dim == 64) {
         if (one_head) return launch_mfma_t<64, 2, 2, 4>(HGA_ARGS);
@@ -583,17 +586,21 @@ hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chu
                               int n_q_chunks, const void* k_res, const void* v_res,
                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                               const void* v_routed, const int32_t* group_idx, void* out,
-                              float* lse, hipStream_t stream);
+                              float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
+                              hipStream_t stream);
 
 hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                          const void* k_res, const void* v_res, int64_t res_tokens,
                          const int32_t* res_slot, const void* k_routed, const void* v_routed,
-                         const int32_t* group_idx, void* out, float* lse, hipStream_t stream) {
+                         const int32_t* group_idx, void* out, float* lse, hipEvent_t ev_start,
+                         hipEvent_t ev_stop, hipStream_t stream) {
     if (plan.p.dtype == HGA_F32)
         return launch_attend_valu(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
-                                  res_slot, k_routed, v_routed, group_idx, out, lse, stream);
+                                  res_slot, k_routed, v_routed, group_idx, out, lse, ev_start,
+                                  ev_stop, stream);
     return launch_attend_mfma(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
-                              res_slot, k_routed, v_routed, group_idx, out, lse, stream);
+                              res_slot, k_routed, v_routed, group_idx, out, lse, ev_start, ev_stop,
+                              stream);
 }
 
 }  // namespace hga

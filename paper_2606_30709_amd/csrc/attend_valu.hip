@@ -6,6 +6,7 @@
 // accumulator in registers.  Key tiles of 16 rows are staged in LDS as fp32
 // (read as broadcasts), and the softmax is the online (running max / running
 // sum) form, rescaled once per tile.
+#include <hip/hip_ext.h>
 #include <math.h>
 
 #include "attend_common.hpp"
@@ -145,18 +146,19 @@ hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chu
                               int n_q_chunks, const void* k_res, const void* v_res,
                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                               const void* v_routed, const int32_t* group_idx, void* out,
-                              float* lse, hipStream_t stream) {
+                              float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
+                              hipStream_t stream) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     dim3 grid(n_q_chunks * r, p.batch * p.n_kv_heads);
 #define HGA_VALU(DD)                                                                            \
-    hipLaunchKernelGGL((attend_valu_kernel<DD>), grid, dim3(64), 0, stream,                     \
-                       static_cast<const float*>(q_rot), q_chunk0, n_q_chunks,                  \
-                       static_cast<const float*>(k_res), static_cast<const float*>(v_res),      \
-                       res_tokens, res_slot, static_cast<const float*>(k_routed),               \
-                       static_cast<const float*>(v_routed), group_idx,                          \
-                       static_cast<float*>(out), lse, p.n_q_heads, p.n_kv_heads, p.chunk,       \
-                       p.group, p.keep_first, recent_window(p), p.topk_groups)
+    hipExtLaunchKernelGGL((attend_valu_kernel<DD>), grid, dim3(64), 0, stream, ev_start, ev_stop, \
+                          0, static_cast<const float*>(q_rot), q_chunk0, n_q_chunks,            \
+                          static_cast<const float*>(k_res), static_cast<const float*>(v_res),   \
+                          res_tokens, res_slot, static_cast<const float*>(k_routed),            \
+                          static_cast<const float*>(v_routed), group_idx,                       \
+                          static_cast<float*>(out), lse, p.n_q_heads, p.n_kv_heads, p.chunk,    \
+                          p.group, p.keep_first, recent_window(p), p.topk_groups)
     if (p.head_dim == 64) HGA_VALU(64); else HGA_VALU(128);
 #undef HGA_VALU
     return hipGetLastError();

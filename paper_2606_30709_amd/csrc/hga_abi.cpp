@@ -382,11 +382,11 @@ hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t
                     "hga_gather_kv launch");
 }
 
-hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
-                      int32_t n_q_chunks, const void* k_res, const void* v_res,
-                      int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
-                      const void* v_routed, const int32_t* group_idx, void* out, float* lse,
-                      void* stream) {
+hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const void* k_res, const void* v_res,
+                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                            void* start_event, void* stop_event, void* stream) {
     HGA_TRY(check_plan(plan));
     const hga_params& p = plan->p;
     if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
@@ -422,8 +422,19 @@ hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
     clear_stale_error();
     return launched(hga::launch_attend(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
                                        res_tokens, res_slot, k_routed, v_routed, group_idx, out,
-                                       lse, static_cast<hipStream_t>(stream)),
+                                       lse, static_cast<hipEvent_t>(start_event),
+                                       static_cast<hipEvent_t>(stop_event),
+                                       static_cast<hipStream_t>(stream)),
                     "hga_attend launch");
+}
+
+hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                      int32_t n_q_chunks, const void* k_res, const void* v_res,
+                      int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                      const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                      void* stream) {
+    return hga_attend_timed(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                            k_routed, v_routed, group_idx, out, lse, nullptr, nullptr, stream);
 }
 
 }  // extern "C"

@@ -58,9 +58,11 @@ hipError_t launch_gather_kv(const hga_plan& plan, const int32_t* group_idx, int 
                             int64_t src_tokens, void* k_routed, void* v_routed,
                             hipStream_t stream);
 
+// start/stop (may be null) are recorded by the attention kernel's dispatch.
 hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                          const void* k_res, const void* v_res, int64_t res_tokens,
                          const int32_t* res_slot, const void* k_routed, const void* v_routed,
-                         const int32_t* group_idx, void* out, float* lse, hipStream_t stream);
+                         const int32_t* group_idx, void* out, float* lse, hipEvent_t start,
+                         hipEvent_t stop, hipStream_t stream);
 
 }  // namespace hga

@@ -17,7 +17,8 @@ import torch
 __all__ = [
     "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
-    "hga_gather_kv", "hga_attend", "hga_status_string", "hga_last_error", "hga_version",
+    "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_status_string", "hga_last_error",
+    "hga_version",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -27,7 +28,7 @@ _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_gather_kv", "hga_attend",
-    "hga_status_string", "hga_last_error", "hga_version",
+    "hga_attend_timed", "hga_status_string", "hga_last_error", "hga_version",
 )
 
 
@@ -76,6 +77,7 @@ def library() -> ctypes.CDLL:
             "hga_route": [vp, vp, i32, i32, vp, vp, i32, vp, vp, vp, vp],
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
+            "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
@@ -232,3 +234,15 @@ def hga_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v_route
         plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
         _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
         _stream(stream)))
+
+
+def hga_attend_timed(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v_routed,
+                     group_idx, out, start_event, stop_event, lse=None, res_slot=None,
+                     stream=None):
+    """hga_attend whose kernel dispatch records the two events (torch.cuda.Event
+    objects that have been recorded once, so that they exist)."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_attend_timed(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
+        start_event.cuda_event, stop_event.cuda_event, _stream(stream)))

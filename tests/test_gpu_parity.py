@@ -281,6 +281,31 @@ def test_fused_route_decode_and_full_size(hga):
                          w.n_chunks, w)
 
 
+def test_attend_timed_records_kernel_events(hga):
+    """hga_attend_timed writes what hga_attend writes, and its dispatch records
+    the two events (a positive duration between them)."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    for key in ("smalllm_2k", "tiny"):
+        w = SMALL[key]
+        pipe = PrefillPipeline(w, W.generate(w))
+        pipe.step()
+        torch.cuda.synchronize()
+        ref_o, ref_l = pipe.out.clone(), pipe.lse.clone()
+        pipe.out.fill_(float("nan"))
+        pipe.lse.fill_(float("nan"))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        e1.record()
+        hga.hga_attend_timed(pipe.plan, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
+                             pipe.group_idx, pipe.out, e0, e1, lse=pipe.lse)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        _say(f"[timed] {key}: {ms * 1e3:.1f} us")
+        assert ms > 0
+        assert torch.equal(pipe.out.view(torch.uint8), ref_o.view(torch.uint8))
+        assert torch.equal(pipe.lse, ref_l)
+
+
 # ----------------------------------------------------------------- decode ---
 
 def _decode_check(hga, w):
