@@ -149,12 +149,15 @@ struct Layout {
     static constexpr uint32_t kBytes = kGidOffset + kMaxGroupSlots * 4;
 };
 
-// Per-key-tile arithmetic shared by both kernels, for one wavefront:
+// Per-key-tile arithmetic for one wavefront:
 //   S^T = K.Q^T over its 32-key sub-tile(s), the causal mask (current chunk)
 //   or the routed-row mask (partial routed tile), the online-softmax update
 //   of (m_run, l_run, oacc), and O^T += V^T.P^T.
 // sK/sV: the staged tile; ksplit: this wave's key half when KS == 2;
 // t: this lane's query token; rt_row0: first routed row of the tile.
+// With both sub-tiles in one wavefront (KS == 1) the softmax is updated per
+// 32-key sub-tile, so the matrix products of one sub-tile are independent of
+// the exponentials of the other and the two overlap in the wavefront.
 template <int D, int KS, bool kCurrent>
 __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
                                           const bf16x8_t (&qf)[D / 16], f32x16_t (&oacc)[D / 32],
@@ -166,26 +169,24 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
     const int lane = threadIdx.x & 63;
     const int half = lane >> 5, col = lane & 31;
     const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
-    f32x16_t sacc[NST];
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int n = 0; n < NST; ++n) {
-        const int st = KS == 2 ? ksplit : n;
+
+    // S^T of 32-key sub-tile st, masked
+    auto qk = [&](int st, f32x16_t& sacc) {
         const int krow = st * 32 + col;
         bf16x8_t kf[NKS];
 #pragma unroll
         for (int kk = 0; kk < NKS; ++kk)
             kf[kk] = lds_frag(sK + krow * D + ((2 * kk + half) ^ swz_k<D>(col)) * 8);
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[n][e] = 0.f;
+        for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
 #pragma unroll
         for (int kk = 0; kk < NKS; ++kk)
-            sacc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sacc[n], 0, 0, 0);
+            sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sacc, 0, 0, 0);
         if (kCurrent) {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                sacc[n][e] = key > t ? -INFINITY : sacc[n][e];
+                sacc[e] = key > t ? -INFINITY : sacc[e];
             }
         } else if (partial) {
 #pragma unroll
@@ -194,37 +195,50 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
                 const int slot = min(row >> group_shift, topk_groups - 1);
                 const int id = s_gid[slot];
                 const bool ok = row < routed_rows && id >= 0 && id < id_limit;
-                sacc[n][e] = ok ? sacc[n][e] : -INFINITY;
+                sacc[e] = ok ? sacc[e] : -INFINITY;
             }
         }
+    };
+    // online-softmax update with the scores of `n` sub-tiles; P as bf16
+    auto update = [&](const f32x16_t* sacc, int n, bf16x8_t* pf) {
+        float tmax = -INFINITY;
+        for (int k = 0; k < n; ++k)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[n][e]);
-    }
-    tmax = max_xor32(tmax) * scale;
-    const float m_new = fmaxf(m_run, tmax);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    l_run *= alpha;
-    // the output needs rescaling only where the running maximum moved
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+            for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[k][e]);
+        tmax = max_xor32(tmax) * scale;
+        // The reference point m_run of the exponentials moves only when the
+        // tile's maximum exceeds it by more than kSlack (log2 units): the
+        // weights exp2(s - m_run) then stay below 2^kSlack, exact in fp32 and
+        // in bf16's range, and the rescale of the output is rarely needed.
+        // The normalisation and the log-sum-exp use the same m_run, so the
+        // result is the softmax for any reference point.
+        constexpr float kSlack = 8.0f;
+        const bool grow = tmax > m_run + kSlack;  // false while the row is fully masked
+        if (__builtin_amdgcn_ballot_w64(grow)) {
+            const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - tmax) : 1.0f;
+            l_run *= alpha;
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt)
+            for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
-    }
-    m_run = m_new;
+                for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
+            m_run = grow ? tmax : m_run;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
+        for (int k = 0; k < n; ++k)
 #pragma unroll
-    for (int n = 0; n < NST; ++n) {
-        const int st = KS == 2 ? ksplit : n;
+            for (int kap = 0; kap < 2; ++kap)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float pv =
+                        __builtin_amdgcn_exp2f(fmaf(sacc[k][kap * 8 + e], scale, -m_use));
+                    l_run += pv;
+                    pf[2 * k + kap][e] = static_cast<__bf16>(pv);
+                }
+    };
+    // O^T += V^T.P^T for 32-key sub-tile st
+    auto pv = [&](int st, const bf16x8_t* pf) {
 #pragma unroll
         for (int kap = 0; kap < 2; ++kap) {
-            bf16x8_t pf;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[n][kap * 8 + e], scale, -m_use));
-                l_run += pv;
-                pf[e] = static_cast<__bf16>(pv);
-            }
             // V^T operand: keys st*32 + kap*16 + {half*4 + 0..3, 8 + half*4 + 0..3}
             // at dimension dt*32 + col; each 16-lane group points at
             // 4 keys x 16 dimensions.
@@ -240,9 +254,26 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
                 const i16x4_t hi = lds_read_tr16(vp1);
                 const bf16x8_t a = __builtin_bit_cast(
                     bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf, oacc[dt], 0, 0, 0);
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pf[kap], oacc[dt], 0, 0, 0);
             }
         }
+    };
+
+    if constexpr (NST == 1) {
+        f32x16_t sacc[1];
+        bf16x8_t pf[2];
+        qk(ksplit, sacc[0]);
+        update(sacc, 1, pf);
+        pv(ksplit, pf);
+    } else {
+        f32x16_t s0[1], s1[1];
+        bf16x8_t p0[2], p1[2];
+        qk(0, s0[0]);
+        qk(1, s1[0]);
+        update(s0, 1, p0);
+        pv(0, p0);
+        update(s1, 1, p1);
+        pv(1, p1);
     }
 }
 
