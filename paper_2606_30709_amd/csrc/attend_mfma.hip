@@ -24,10 +24,11 @@
 // when tile t is consumed, tiles t+1 .. t+NS-2 are already in flight and the
 // copy of tile t+NS-1 is issued into the stage tile t-1 has freed, with one
 // workgroup barrier per tile.  The workgroup's query rows and the unit's
-// group ids arrive the same way before the first tile.  Rows are unpadded;
-// the 16-byte chunks of row r are stored at chunk ^ swz(r), which spreads
-// the rows read together by one LDS instruction over distinct banks.  The
-// copies are written as inline assembly and waited for with explicit
+// group ids arrive the same way before the first tile.  Each copy lane
+// picks its source 16 bytes so that K lands row-major with an XOR swizzle
+// and V in the order its transpose reads consume it (see swz_k and
+// v_slot_source): LDS reads are free of bank conflicts, and the V reads are
+// addressed by immediate offsets from one base register.  The copies are written as inline assembly and waited for with explicit
 // vmcnt counts (loads complete in issue order), because the compiler's own
 // tracking of LDS-destination loads would wait for every copy in flight
 // before any LDS read.  V^T operands come from gfx950's LDS transpose read
@@ -91,11 +92,19 @@ __device__ __forceinline__ void wait_loads() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-// Chunk swizzles: the 16-byte chunk j of row r is stored at j ^ swz(r).
-// K (and Q) rows are read as 16-byte A/B fragments by 32 lanes on 32
-// consecutive rows; V rows by the transpose read, 8 consecutive keys at a
-// time.
-// For D = 128 (16 chunks per row) one 4-bit map serves both patterns.
+// LDS layout of a staged tile.
+// * K and the query rows are row-major, unpadded, with the 16-byte chunk j of
+//   row r stored at j ^ swz_k(r): the 16-byte A/B fragments read by 32 lanes
+//   on 32 consecutive rows then fall in distinct banks, and each copy reads
+//   whole rows.  (For D = 128, 16 chunks per row, the map uses four bits.)
+// * V is stored in the order its transpose reads consume it: block
+//   (st, kap, hi, dt) -- keys st*32 + kap*16 + 8*hi + 0..7, dimensions
+//   dt*32 .. dt*32+31 -- is 512 B at (((st*2 + kap)*2 + hi)*NDT + dt) * 512,
+//   lane l holding the 8 bytes its ds_read_b64_tr_b16 asks for: key
+//   (l>>5)*4 + ((l&15)>>2), dimensions ((l>>4)&1)*16 + (l&3)*4 .. +4 (two
+//   lanes share each 16-byte slot).  Every V read is one contiguous block
+//   (no bank conflicts) at an immediate offset from one base register, and
+//   a copy still reads 8 rows x 128 contiguous bytes.
 template <int D>
 __device__ __forceinline__ int swz_k(int r) {
     if constexpr (D == 64)
@@ -104,12 +113,14 @@ __device__ __forceinline__ int swz_k(int r) {
         return ((r ^ (r >> 3)) & 1) | (((r ^ (r >> 2)) & 1) << 1) | (((r >> 1) & 1) << 2) |
                ((r & 1) << 3);
 }
+// Source (row, 16-byte chunk) of 16-byte slot P of the V region.
 template <int D>
-__device__ __forceinline__ int swz_v(int r) {
-    if constexpr (D == 64)
-        return ((r & 1) << 1) | (((r >> 1) & 1) << 2);
-    else
-        return swz_k<D>(r);
+__device__ __forceinline__ void v_slot_source(int P, int& row, int& chunk) {
+    constexpr int NDT = D / 32;
+    const int blk = P >> 5, q = P & 31;  // 32 slots per 512-byte block
+    const int dt = blk % NDT, h = blk / NDT;  // h = (st*2 + kap)*2 + hi
+    row = (h >> 2) * 32 + ((h >> 1) & 1) * 16 + (h & 1) * 8 + (q >> 4) * 4 + ((q & 7) >> 1);
+    chunk = dt * 4 + ((q >> 3) & 1) * 2 + (q & 1);
 }
 
 // x and the value of lane l ^ 32 combined, without an LDS round trip:
@@ -240,16 +251,12 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
 #pragma unroll
         for (int kap = 0; kap < 2; ++kap) {
             // V^T operand: keys st*32 + kap*16 + {half*4 + 0..3, 8 + half*4 + 0..3}
-            // at dimension dt*32 + col; each 16-lane group points at
-            // 4 keys x 16 dimensions.
-            const int key0 = st * 32 + kap * 16 + half * 4 + ((lane & 15) >> 2);
-            const int dcol = ((lane >> 4) & 1) * 16 + (lane & 3) * 4;
-            const int vs0 = swz_v<D>(key0), vs1 = swz_v<D>(key0 + 8);
+            // at dimension dt*32 + col, from the two transpose-read blocks
+            // (st, kap, 0, dt) and (st, kap, 1, dt).
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) {
-                const int e0 = dt * 32 + dcol;
-                const bf16_t* vp0 = sV + key0 * D + (((e0 >> 3) ^ vs0) << 3) + (e0 & 7);
-                const bf16_t* vp1 = sV + (key0 + 8) * D + (((e0 >> 3) ^ vs1) << 3) + (e0 & 7);
+                const bf16_t* vp0 = sV + ((((st * 2 + kap) * 2 + 0) * NDT + dt) * 64 + lane) * 4;
+                const bf16_t* vp1 = sV + ((((st * 2 + kap) * 2 + 1) * NDT + dt) * 64 + lane) * 4;
                 const i16x4_t lo = lds_read_tr16(vp0);
                 const i16x4_t hi = lds_read_tr16(vp1);
                 const bf16x8_t a = __builtin_bit_cast(
@@ -361,7 +368,6 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
                        kStageBytes = Lay::kStageBytes;
     constexpr int NDT = D / 32;                  // 32-wide output blocks
     constexpr int NKS = D / 16;                  // k-steps of Q.K^T
-    constexpr int CPR = D / 8;                   // 16-byte chunks per row
     constexpr int QT = NW / KS;                  // query tiles per workgroup
     constexpr int KI = kTileBytes / 1024 / NW;   // copies per wave per tile, for K (and V)
     constexpr int LPT = 2 * KI;                  // loads per wave per tile
@@ -422,7 +428,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
         for (int u = 0; u < QI; ++u) {
             const int blk = u * NW + wave;
             const int pch = blk * 64 + lane;
-            const int row = pch / CPR, pc = pch % CPR;
+            const int row = pch / (D / 8), pc = pch % (D / 8);
             const int urow = part * QT * 32 + row;  // query row within the unit
             uint32_t off = kAbsent;
             if (urow < r * KT) {
@@ -460,9 +466,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
 #pragma unroll
     for (int u = 0; u < KI; ++u) {
         const int pch = (u * NW + wave) * 64 + lane;
-        const int row = pch / CPR, pc = pch % CPR;
+        const int row = pch / (D / 8), pc = pch % (D / 8);
         koff[u] = row * kRowBytes + (pc ^ swz_k<D>(row)) * 16;
-        voff[u] = row * kRowBytes + (pc ^ swz_v<D>(row)) * 16;
+        int vrow, vch;
+        v_slot_source<D>(pch, vrow, vch);
+        voff[u] = vrow * kRowBytes + vch * 16;
     }
     // Issue the copies of tile `tile` (< n_tiles) into stage `stage`.
     auto issue = [&](int tile, int stage) {
