@@ -3,10 +3,11 @@
 
 One step = the whole hot path over one batch of synthetic input: chunk and
 group summaries, chunk routing, group refinement, gather of the routed K/V,
-and exact attention (inputs already resident in HBM).  The two routing stages
-run as the single call hga_route (four C-ABI calls per step);
---separate-route issues hga_route_chunks and hga_route_groups instead (five
-calls, bit-identical indices).  The default workload is the SmallLM-shaped
+and exact attention (inputs already resident in HBM).  By default a step is
+four C-ABI calls: hga_build_summaries_qbar (summaries and the routing query
+means in one launch), hga_route_qbar (chunk and group selection),
+hga_gather_kv and hga_attend; --route fused / separate use hga_route or the
+two routing calls instead (identical results).  The default workload is the SmallLM-shaped
 prefill (B4, 8/8 heads, d64, 8192 tokens, bf16, C64 G16, first chunk hot,
 K_c 3, K_g 4 -> 3.125% of the context fetched by the last chunk).
 
@@ -39,8 +40,11 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
 
-STAGES_SEPARATE = ("build_summaries", "route_chunks", "route_groups", "gather_kv", "attend")
-STAGES_FUSED = ("build_summaries", "route", "gather_kv", "attend")
+STAGES = {
+    "qbar": ("build_summaries_qbar", "route_qbar", "gather_kv", "attend"),
+    "fused": ("build_summaries", "route", "gather_kv", "attend"),
+    "separate": ("build_summaries", "route_chunks", "route_groups", "gather_kv", "attend"),
+}
 
 
 def algorithmic_bytes(w, n_valid_rows: int) -> dict:
@@ -62,6 +66,8 @@ def algorithmic_bytes(w, n_valid_rows: int) -> dict:
         "route_groups": table_c + table_g + B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4,
         "route": (q_tok + 2 * table_c + table_g +
                   B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4),
+        "build_summaries_qbar": kv_tok + table_c + table_g + q_tok + table_c,
+        "route_qbar": 2 * table_c + table_g + B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4,
         "gather_kv": 4 * routed + B * Hkv * nc * w.topk_groups * 4,
         "attend": q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4,
     }
@@ -182,8 +188,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--separate-route", action="store_true",
-                    help="route with hga_route_chunks + hga_route_groups instead of hga_route")
+    ap.add_argument("--route", choices=("qbar", "fused", "separate"), default="qbar",
+                    help="qbar: hga_build_summaries_qbar + hga_route_qbar; fused: "
+                         "hga_build_summaries + hga_route; separate: hga_build_summaries + "
+                         "hga_route_chunks + hga_route_groups (identical results)")
     ap.add_argument("--probe-traffic", action="store_true",
                     help="run attention and a known-size copy for rocprofv3 --pmc, then exit")
     args = ap.parse_args()
@@ -223,8 +231,8 @@ def main():
     attend_timed = lambda e0, e1: hga.hga_attend_timed(
         p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed, pipe.group_idx, pipe.out,
         e0, e1, lse=pipe.lse, stream=sh)
-    if args.separate_route:
-        STAGES = STAGES_SEPARATE
+    stage_names = STAGES[args.route]
+    if args.route == "separate":
         calls = (
             summarise,
             lambda: hga.hga_route_chunks(p, pipe.q, 0, pipe.chunk_sum, pipe.qbar, pipe.chunk_idx,
@@ -232,12 +240,18 @@ def main():
             lambda: hga.hga_route_groups(p, pipe.qbar, pipe.chunk_idx, 0, pipe.group_sum,
                                          pipe.group_idx, stream=sh),
             gather, attend)
-    else:
-        STAGES = STAGES_FUSED
+    elif args.route == "fused":
         calls = (
             summarise,
             lambda: hga.hga_route(p, pipe.q, 0, pipe.chunk_sum, pipe.group_sum, pipe.qbar,
                                   pipe.chunk_idx, pipe.group_idx, stream=sh),
+            gather, attend)
+    else:
+        calls = (
+            lambda: hga.hga_build_summaries_qbar(p, pipe.k, 0, 0, w.n_chunks, pipe.chunk_sum,
+                                                 pipe.group_sum, pipe.q, 0, pipe.qbar, stream=sh),
+            lambda: hga.hga_route_qbar(p, pipe.qbar, 0, pipe.chunk_sum, pipe.group_sum,
+                                       pipe.chunk_idx, pipe.group_idx, stream=sh),
             gather, attend)
 
     for _ in range(args.warmup):
@@ -282,7 +296,7 @@ def main():
             ev[s][n + 1].record(stream)
     torch.cuda.synchronize()
     stage_ms = {name: float(np.mean([ev[s][n].elapsed_time(ev[s][n + 1]) for s in range(KB)]))
-                for n, name in enumerate(STAGES)}
+                for n, name in enumerate(stage_names)}
     stage_ms["attend"] = attend_ms
     wall_ms = (t1 - t0) * 1e3 / K
     tokens = w.batch * w.seq_len
@@ -291,9 +305,9 @@ def main():
     abytes = algorithmic_bytes(w, n_valid_rows)
     flops = attention_flops(w, gi)
 
-    dominant = max(STAGES, key=lambda s: stage_ms[s])
+    dominant = max(stage_names, key=lambda s: stage_ms[s])
     stages = {}
-    for sname in STAGES:
+    for sname in stage_names:
         sec = stage_ms[sname] * 1e-3
         ent = {"us": round(stage_ms[sname] * 1e3, 2),
                "alg_bytes": abytes[sname], "GB_s": round(abytes[sname] / sec / 1e9, 1),
@@ -335,7 +349,7 @@ def main():
                          "other stages: a second pass of the same steps with events between "
                          "all calls"),
         "stages": stages,
-        "route_calls": "separate" if args.separate_route else "fused",
+        "route_calls": args.route,
         "roofline": roofline,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }

@@ -11,6 +11,8 @@
  *   hga_route_chunks     query-chunk -> chunk scoring, top-K_c (Sec. 3.3)
  *   hga_route_groups     group refinement inside the chosen chunks, top-K_g (Sec. 3.3)
  *   hga_route            both routing stages in one launch, same outputs
+ *   hga_build_summaries_qbar  summaries and the routing query means in one launch
+ *   hga_route_qbar       hga_route's selection stages from a given q_bar
  *   hga_gather_kv        copy the routed groups' exact token K/V (Sec. 4.3)
  *   hga_attend           exact causal softmax attention, Eq. (1), over the
  *                        current chunk, the always-visible chunks and the
@@ -184,6 +186,36 @@ hga_status hga_route(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                      int32_t n_q_chunks, const float* chunk_sum, const float* group_sum,
                      int32_t table_chunks, float* qbar, int32_t* chunk_idx, int32_t* group_idx,
                      void* stream);
+
+/* hga_build_summaries and the q_bar reduction of hga_route_chunks (Sec. 3.3:
+ * the mean of q_rot over each query chunk's tokens and the query heads of its
+ * KV head) in one launch: the two read different tensors (K and Q) and do
+ * not depend on each other.  chunk_sum/group_sum receive exactly what
+ * hga_build_summaries writes, and qbar exactly what hga_route_chunks (or
+ * hga_route) writes for the same query rows.
+ *
+ *   k_rot .. table_chunks   as for hga_build_summaries
+ *   q_rot                   [batch, n_q_heads, n_q_chunks * chunk, head_dim]
+ *                           plan dtype (query chunks q_chunk0 ..)
+ *   qbar                    fp32 out [batch, n_kv_heads, n_q_chunks, head_dim]
+ * Requirements and errors: those of hga_build_summaries, plus q_chunk0 >= 0
+ * and n_q_chunks >= 0.  Either part may be empty. */
+hga_status hga_build_summaries_qbar(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
+                                    int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
+                                    float* chunk_sum, float* group_sum, int32_t table_chunks,
+                                    const void* q_rot, int32_t q_chunk0, int32_t n_q_chunks,
+                                    float* qbar, void* stream);
+
+/* The selection stages of hga_route (chunk scores and top-K_c, group
+ * refinement and top-K_g, Sec. 3.3) from a given q_bar, e.g. the one
+ * hga_build_summaries_qbar wrote; chunk_idx and group_idx are exactly what
+ * hga_route writes when it computes the same q_bar itself.  qbar is read
+ * only.  Arguments, layouts, requirements and errors are those of
+ * hga_route. */
+hga_status hga_route_qbar(const hga_plan* plan, const float* qbar, int32_t q_chunk0,
+                          int32_t n_q_chunks, const float* chunk_sum, const float* group_sum,
+                          int32_t table_chunks, int32_t* chunk_idx, int32_t* group_idx,
+                          void* stream);
 
 /* Gather the exact token K/V of the routed groups (Sec. 4.3, "gathering
  * exact token K/V for the selected chunks or groups").  Slot s of query chunk

@@ -233,10 +233,12 @@ hga_status hga_plan_params(const hga_plan* plan, hga_params* out) {
     return HGA_OK;
 }
 
-hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
-                               int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
-                               float* chunk_sum, float* group_sum, int32_t table_chunks,
-                               void* stream) {
+namespace {
+
+// Checks of a summary build; *empty is set when the chunk range is empty.
+hga_status check_summaries(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
+                           int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
+                           float* chunk_sum, float* group_sum, int32_t table_chunks, bool* empty) {
     HGA_TRY(check_plan(plan));
     const hga_params& p = plan->p;
     if (k_tokens < 0 || k_chunk0 < 0 || table_chunks < 0)
@@ -248,15 +250,52 @@ hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t 
         return fail(HGA_EINVAL, "chunks up to %d need %lld tokens of k_rot, have %lld", chunk_end,
                     static_cast<long long>(static_cast<int64_t>(chunk_end - k_chunk0) * p.chunk),
                     static_cast<long long>(k_tokens));
-    if (chunk_end == chunk_begin) return HGA_OK;
+    *empty = chunk_end == chunk_begin;
+    if (*empty) return HGA_OK;
     HGA_TRY(check_tensor(k_rot, "k_rot"));
     HGA_TRY(check_tensor(chunk_sum, "chunk_sum"));
     HGA_TRY(check_tensor(group_sum, "group_sum"));
+    return HGA_OK;
+}
+
+}  // namespace
+
+hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
+                               int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
+                               float* chunk_sum, float* group_sum, int32_t table_chunks,
+                               void* stream) {
+    bool empty = false;
+    HGA_TRY(check_summaries(plan, k_rot, k_tokens, k_chunk0, chunk_begin, chunk_end, chunk_sum,
+                            group_sum, table_chunks, &empty));
+    if (empty) return HGA_OK;
     clear_stale_error();
     return launched(hga::launch_build_summaries(*plan, k_rot, k_tokens, k_chunk0, chunk_begin,
                                                 chunk_end, chunk_sum, group_sum, table_chunks,
                                                 static_cast<hipStream_t>(stream)),
                     "hga_build_summaries launch");
+}
+
+hga_status hga_build_summaries_qbar(const hga_plan* plan, const void* k_rot, int64_t k_tokens,
+                                    int32_t k_chunk0, int32_t chunk_begin, int32_t chunk_end,
+                                    float* chunk_sum, float* group_sum, int32_t table_chunks,
+                                    const void* q_rot, int32_t q_chunk0, int32_t n_q_chunks,
+                                    float* qbar, void* stream) {
+    bool empty = false;
+    HGA_TRY(check_summaries(plan, k_rot, k_tokens, k_chunk0, chunk_begin, chunk_end, chunk_sum,
+                            group_sum, table_chunks, &empty));
+    if (q_chunk0 < 0 || n_q_chunks < 0)
+        return fail(HGA_EINVAL, "q_chunk0 and n_q_chunks must be >= 0");
+    if (n_q_chunks > 0) {
+        HGA_TRY(check_tensor(q_rot, "q_rot"));
+        HGA_TRY(check_tensor(qbar, "qbar"));
+    }
+    if (empty && n_q_chunks == 0) return HGA_OK;
+    clear_stale_error();
+    return launched(hga::launch_summaries_qbar(*plan, k_rot, k_tokens, k_chunk0, chunk_begin,
+                                               chunk_end, chunk_sum, group_sum, table_chunks,
+                                               q_rot, q_chunk0, n_q_chunks, qbar,
+                                               static_cast<hipStream_t>(stream)),
+                    "hga_build_summaries_qbar launch");
 }
 
 namespace {
@@ -265,7 +304,8 @@ namespace {
 // middle chunks of a query chunk.
 hga_status check_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                               int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
-                              float* qbar, int32_t* chunk_idx, bool groups, int* n_max) {
+                              float* qbar, int32_t* chunk_idx, bool groups, int* n_max,
+                              const char* q_name = "q_rot") {
     HGA_TRY(check_plan(plan));
     const hga_params& p = plan->p;
     if (q_chunk0 < 0 || n_q_chunks < 0 || table_chunks < 0)
@@ -319,6 +359,24 @@ hga_status hga_route(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                                       table_chunks, qbar, chunk_idx, group_idx,
                                       static_cast<hipStream_t>(stream)),
                     "hga_route launch");
+}
+
+hga_status hga_route_qbar(const hga_plan* plan, const float* qbar, int32_t q_chunk0,
+                          int32_t n_q_chunks, const float* chunk_sum, const float* group_sum,
+                          int32_t table_chunks, int32_t* chunk_idx, int32_t* group_idx,
+                          void* stream) {
+    int n_max = 0;
+    // the checks of hga_route, with qbar in the place of the query rows
+    HGA_TRY(check_route_chunks(plan, qbar, q_chunk0, n_q_chunks, chunk_sum, table_chunks,
+                               const_cast<float*>(qbar), chunk_idx, true, &n_max, "qbar"));
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_tensor(group_sum, "group_sum"));
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    clear_stale_error();
+    return launched(hga::launch_route_from_qbar(*plan, qbar, q_chunk0, n_q_chunks, chunk_sum,
+                                                group_sum, table_chunks, chunk_idx, group_idx,
+                                                static_cast<hipStream_t>(stream)),
+                    "hga_route_qbar launch");
 }
 
 hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32_t* chunk_idx,

@@ -49,6 +49,19 @@ hipError_t launch_route(const hga_plan& plan, const void* q_rot, int q_chunk0, i
                         const float* chunk_sum, const float* group_sum, int table_chunks,
                         float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream);
 
+// hga_route's selection stages from a given q_bar (it is read, not written).
+hipError_t launch_route_from_qbar(const hga_plan& plan, const float* qbar, int q_chunk0,
+                                  int n_q_chunks, const float* chunk_sum, const float* group_sum,
+                                  int table_chunks, int32_t* chunk_idx, int32_t* group_idx,
+                                  hipStream_t stream);
+
+// Summaries of [chunk_begin, chunk_end) and q_bar of the query chunks in one
+// launch (independent work items).
+hipError_t launch_summaries_qbar(const hga_plan& plan, const void* k_rot, int64_t k_tokens,
+                                 int k_chunk0, int chunk_begin, int chunk_end, float* chunk_sum,
+                                 float* group_sum, int table_chunks, const void* q_rot,
+                                 int q_chunk0, int n_q_chunks, float* qbar, hipStream_t stream);
+
 hipError_t launch_route_groups(const hga_plan& plan, const float* qbar, const int32_t* chunk_idx,
                                int q_chunk0, int n_q_chunks, const float* group_sum,
                                int table_chunks, int32_t* group_idx, hipStream_t stream);

@@ -10,6 +10,7 @@
 // reduction plus one rescan of the winning lane's share.
 #include "hga_device.hpp"
 #include "hga_internal.hpp"
+#include "qbar.hpp"
 
 namespace hga {
 namespace {
@@ -130,7 +131,7 @@ __device__ inline WaveLds carve(unsigned char* base, int d, int n_list, int topk
 // its top K_c.  With kGroups, the same wavefront goes on
 // to group refinement of its chosen chunks (the work of route_groups_kernel,
 // without a second launch or the q_bar/chunk_idx round trip through memory).
-template <typename T, int D, bool kGroups>
+template <typename T, int D, bool kGroups, bool kQbarIn>
 __global__ __launch_bounds__(256) void route_kernel(
     const T* __restrict__ q_rot, int q_chunk0, int n_q_chunks, const float* __restrict__ chunk_sum,
     const float* __restrict__ group_sum, int table_chunks, float* __restrict__ qbar,
@@ -138,16 +139,10 @@ __global__ __launch_bounds__(256) void route_kernel(
     int keep_first, int window, int topk, int topk_groups, int gpc_shift, int units_per_block,
     size_t wave_bytes) {
     constexpr int kThreads = 256;
-    constexpr int chunk = 64;
-    constexpr int V = elem<T>::kVec;
-    constexpr int VPR = D / V;              // 16-byte vectors per row
-    constexpr int NRS = 64 / VPR;           // row slots per wave
-    constexpr int UNROLL = 64 / NRS < 16 ? 64 / NRS : 16;  // NRS * UNROLL divides 64 rows
     constexpr int TB = 64;                  // table rows per LDS block
     constexpr int TS = D + 4;               // padded LDS row stride (floats)
     constexpr int F4 = D / 4;               // float4 per table row
     constexpr int PF = TB * F4 / kThreads;  // float4 per thread per table block
-    static_assert((NRS * UNROLL) <= 64 && 64 % (NRS * UNROLL) == 0, "q_bar row tiling");
     extern __shared__ __align__(16) unsigned char smem_raw[];
     float* s_tab = reinterpret_cast<float*>(smem_raw);
     unsigned char* wave_base = smem_raw + align16(sizeof(float) * TB * TS);
@@ -182,49 +177,21 @@ __global__ __launch_bounds__(256) void route_kernel(
     };
     if (keep_first < hi) fetch_block(keep_first);
 
-    // 1. q_bar: mean over the r heads x chunk tokens, fixed summation order.
+    // 1. q_bar: computed here (mean over the r heads x chunk tokens) or read.
     WaveLds L{};
     if (active) {
         L = carve(wave_base + wave * wave_bytes, D, kGroups ? topk : 0,
                   kGroups && topk_groups > topk ? topk_groups : topk);
-        const int cv = lane % VPR, rs = lane / VPR;
-        float acc[V];
-#pragma unroll
-        for (int e = 0; e < V; ++e) acc[e] = 0.f;
-        const int rows = r * chunk;
-        const int64_t qtok = static_cast<int64_t>(n_q_chunks) * chunk;
-        const T* qbase = q_rot + ((static_cast<int64_t>(b) * n_q_heads + j * r) * qtok +
-                                  static_cast<int64_t>(i) * chunk) * D + cv * V;
-        for (int row0 = rs; row0 < rows; row0 += NRS * UNROLL) {
-            vec16 x[UNROLL];
-#pragma unroll
-            for (int u = 0; u < UNROLL; ++u) {
-                const int row = row0 + u * NRS;
-                const int hh = row >> 6, tt = row & 63;
-                x[u] = load16(qbase + (hh * qtok + tt) * D);
+        if constexpr (kQbarIn) {
+            for (int x = lane; x < D; x += 64) L.q[x] = qbar[unit * D + x];
+            wave_sync_lds();
+        } else {
+            wave_query_mean<T, D>(q_rot, b, j, i, n_q_heads, r, n_q_chunks, L.q);
+            wave_sync_lds();
+            if (lane < D / 4) {
+                const float4 v = *reinterpret_cast<const float4*>(L.q + lane * 4);
+                *reinterpret_cast<float4*>(qbar + unit * D + lane * 4) = v;
             }
-#pragma unroll
-            for (int u = 0; u < UNROLL; ++u) {
-                float f[V];
-                elem<T>::unpack(x[u], f);
-#pragma unroll
-                for (int e = 0; e < V; ++e) acc[e] += f[e];
-            }
-        }
-#pragma unroll
-        for (int m = VPR; m < 64; m <<= 1)
-#pragma unroll
-            for (int e = 0; e < V; ++e) acc[e] += __shfl_xor(acc[e], m, 64);
-        const float inv = 1.0f / static_cast<float>(rows);
-        if (rs == 0) {
-#pragma unroll
-            for (int e = 0; e < V; ++e) L.q[cv * V + e] = acc[e] * inv;
-        }
-        wave_sync_lds();
-        if (lane < VPR) {
-            float* out = qbar + unit * D + cv * V;
-#pragma unroll
-            for (int e = 0; e < V; ++e) out[e] = L.q[cv * V + e];
         }
     }
 
@@ -359,7 +326,7 @@ inline RouteGeom route_geom(const hga_plan& plan, int n_max, bool groups) {
     return g;
 }
 
-template <typename T, int D, bool kGroups>
+template <typename T, int D, bool kGroups, bool kQbarIn>
 hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                           const float* chunk_sum, const float* group_sum, int table_chunks,
                           float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream) {
@@ -370,7 +337,8 @@ hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0,
     const int blocks = p.batch * p.n_kv_heads * ((n_q_chunks + upb - 1) / upb);
     const int gpc = p.chunk / p.group;
     const int gpc_shift = gpc == 8 ? 3 : (gpc == 4 ? 2 : 1);
-    hipLaunchKernelGGL((route_kernel<T, D, kGroups>), dim3(blocks), dim3(256), g.total, stream,
+    hipLaunchKernelGGL((route_kernel<T, D, kGroups, kQbarIn>), dim3(blocks), dim3(256), g.total,
+                       stream,
                        static_cast<const T*>(q_rot), q_chunk0, n_q_chunks, chunk_sum, group_sum,
                        table_chunks, qbar, chunk_idx, group_idx, p.n_q_heads, p.n_kv_heads,
                        p.keep_first, recent_window(p), p.topk_chunks, p.topk_groups, gpc_shift, upb,
@@ -378,7 +346,7 @@ hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0,
     return hipGetLastError();
 }
 
-template <bool kGroups>
+template <bool kGroups, bool kQbarIn>
 hipError_t launch_route_any(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                             const float* chunk_sum, const float* group_sum, int table_chunks,
                             float* qbar, int32_t* chunk_idx, int32_t* group_idx,
@@ -386,18 +354,18 @@ hipError_t launch_route_any(const hga_plan& plan, const void* q_rot, int q_chunk
     const hga_params& p = plan.p;
     if (p.dtype == HGA_F32) {
         if (p.head_dim == 64)
-            return launch_route_t<float, 64, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+            return launch_route_t<float, 64, kGroups, kQbarIn>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
                                                       group_sum, table_chunks, qbar, chunk_idx,
                                                       group_idx, stream);
-        return launch_route_t<float, 128, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+        return launch_route_t<float, 128, kGroups, kQbarIn>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
                                                    group_sum, table_chunks, qbar, chunk_idx,
                                                    group_idx, stream);
     }
     if (p.head_dim == 64)
-        return launch_route_t<bf16_t, 64, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+        return launch_route_t<bf16_t, 64, kGroups, kQbarIn>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
                                                    group_sum, table_chunks, qbar, chunk_idx,
                                                    group_idx, stream);
-    return launch_route_t<bf16_t, 128, kGroups>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
+    return launch_route_t<bf16_t, 128, kGroups, kQbarIn>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum,
                                                 group_sum, table_chunks, qbar, chunk_idx,
                                                 group_idx, stream);
 }
@@ -433,15 +401,24 @@ size_t route_lds_bytes(const hga_plan& plan, int n_max, bool groups) {
 hipError_t launch_route_chunks(const hga_plan& plan, const void* q_rot, int q_chunk0,
                                int n_q_chunks, const float* chunk_sum, int table_chunks,
                                float* qbar, int32_t* chunk_idx, hipStream_t stream) {
-    return launch_route_any<false>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, nullptr,
-                                   table_chunks, qbar, chunk_idx, nullptr, stream);
+    return launch_route_any<false, false>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, nullptr,
+                                          table_chunks, qbar, chunk_idx, nullptr, stream);
 }
 
 hipError_t launch_route(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                         const float* chunk_sum, const float* group_sum, int table_chunks,
                         float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream) {
-    return launch_route_any<true>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, group_sum,
-                                  table_chunks, qbar, chunk_idx, group_idx, stream);
+    return launch_route_any<true, false>(plan, q_rot, q_chunk0, n_q_chunks, chunk_sum, group_sum,
+                                         table_chunks, qbar, chunk_idx, group_idx, stream);
+}
+
+hipError_t launch_route_from_qbar(const hga_plan& plan, const float* qbar, int q_chunk0,
+                                  int n_q_chunks, const float* chunk_sum, const float* group_sum,
+                                  int table_chunks, int32_t* chunk_idx, int32_t* group_idx,
+                                  hipStream_t stream) {
+    return launch_route_any<true, true>(plan, nullptr, q_chunk0, n_q_chunks, chunk_sum, group_sum,
+                                        table_chunks, const_cast<float*>(qbar), chunk_idx,
+                                        group_idx, stream);
 }
 
 hipError_t launch_route_groups(const hga_plan& plan, const float* qbar, const int32_t* chunk_idx,

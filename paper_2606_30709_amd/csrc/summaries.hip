@@ -21,6 +21,7 @@
 // group phase table and the psi table live in LDS.
 #include "hga_device.hpp"
 #include "hga_internal.hpp"
+#include "qbar.hpp"
 
 namespace hga {
 namespace {
@@ -39,12 +40,14 @@ struct SumGeom {
     static constexpr int SLICES = 64 / NPB;         // token slices per chunk
 };
 
+// The summary work of workgroup `block` of `n_blocks` (a grid-stride loop
+// over the (batch, KV head, chunk) items).
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void build_summaries_kernel(
-    const T* __restrict__ k_rot, int64_t k_tokens, int k_chunk0, int chunk_begin, int n_chunks,
-    float* __restrict__ chunk_sum, float* __restrict__ group_sum, int table_chunks, int n_bh,
-    const float* __restrict__ phase_group, const float* __restrict__ phase_psi, int group,
-    int hf_chunk) {
+__device__ __forceinline__ void summaries_body(
+    int block, int n_blocks, const T* __restrict__ k_rot, int64_t k_tokens, int k_chunk0,
+    int chunk_begin, int n_chunks, float* __restrict__ chunk_sum, float* __restrict__ group_sum,
+    int table_chunks, int n_bh, const float* __restrict__ phase_group,
+    const float* __restrict__ phase_psi, int group, int hf_chunk) {
     using Gm = SumGeom<T, D>;
     constexpr int V = Gm::V, LV = Gm::LV, VPH = Gm::VPH, HALF = Gm::HALF, NPB = Gm::NPB,
                   TPL = Gm::TPL, SLICES = Gm::SLICES;
@@ -71,8 +74,8 @@ __global__ __launch_bounds__(kThreads) void build_summaries_kernel(
     float* red = s_red + wave * 2 * SLICES * RD;
     const int64_t total = static_cast<int64_t>(n_bh) * n_chunks;
 
-    for (int64_t item0 = static_cast<int64_t>(blockIdx.x) * kWaves; item0 < total;
-         item0 += static_cast<int64_t>(gridDim.x) * kWaves) {
+    for (int64_t item0 = static_cast<int64_t>(block) * kWaves; item0 < total;
+         item0 += static_cast<int64_t>(n_blocks) * kWaves) {
         const int64_t item = item0 + wave;
         const bool active = item < total;
         const int bh = active ? static_cast<int>(item / n_chunks) : 0;
@@ -152,6 +155,41 @@ __global__ __launch_bounds__(kThreads) void build_summaries_kernel(
 }
 
 template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void build_summaries_kernel(
+    const T* __restrict__ k_rot, int64_t k_tokens, int k_chunk0, int chunk_begin, int n_chunks,
+    float* __restrict__ chunk_sum, float* __restrict__ group_sum, int table_chunks, int n_bh,
+    const float* __restrict__ phase_group, const float* __restrict__ phase_psi, int group,
+    int hf_chunk) {
+    summaries_body<T, D>(blockIdx.x, gridDim.x, k_rot, k_tokens, k_chunk0, chunk_begin, n_chunks,
+                         chunk_sum, group_sum, table_chunks, n_bh, phase_group, phase_psi, group,
+                         hf_chunk);
+}
+
+// Summaries (workgroups [0, n_sum_blocks)) and, in the same launch, q_bar of
+// every query chunk (the other workgroups, one wavefront per (batch, KV head,
+// query chunk)): the two read different tensors (K and Q) and are
+// independent, so one launch streams both.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void summaries_qbar_kernel(
+    const T* __restrict__ k_rot, int64_t k_tokens, int k_chunk0, int chunk_begin, int n_chunks,
+    float* __restrict__ chunk_sum, float* __restrict__ group_sum, int table_chunks, int n_bh,
+    const float* __restrict__ phase_group, const float* __restrict__ phase_psi, int group,
+    int hf_chunk, int n_sum_blocks, const T* __restrict__ q_rot, int n_q_chunks,
+    float* __restrict__ qbar, int n_q_heads, int n_kv) {
+    if (static_cast<int>(blockIdx.x) < n_sum_blocks) {
+        summaries_body<T, D>(blockIdx.x, n_sum_blocks, k_rot, k_tokens, k_chunk0, chunk_begin,
+                             n_chunks, chunk_sum, group_sum, table_chunks, n_bh, phase_group,
+                             phase_psi, group, hf_chunk);
+        return;
+    }
+    const int unit = (static_cast<int>(blockIdx.x) - n_sum_blocks) * kWaves + (threadIdx.x >> 6);
+    if (unit >= n_bh * n_q_chunks) return;
+    const int i = unit % n_q_chunks, bh = unit / n_q_chunks;
+    wave_query_mean<T, D>(q_rot, bh / n_kv, bh % n_kv, i, n_q_heads, n_q_heads / n_kv, n_q_chunks,
+                          qbar + static_cast<int64_t>(unit) * D);
+}
+
+template <typename T, int D>
 hipError_t launch_t(const hga_plan& plan, const void* k_rot, int64_t k_tokens, int k_chunk0,
                     int chunk_begin, int chunk_end, float* chunk_sum, float* group_sum,
                     int table_chunks, hipStream_t stream) {
@@ -172,7 +210,57 @@ hipError_t launch_t(const hga_plan& plan, const void* k_rot, int64_t k_tokens, i
     return hipGetLastError();
 }
 
+template <typename T, int D>
+hipError_t launch_sq_t(const hga_plan& plan, const void* k_rot, int64_t k_tokens, int k_chunk0,
+                       int chunk_begin, int chunk_end, float* chunk_sum, float* group_sum,
+                       int table_chunks, const void* q_rot, int n_q_chunks, float* qbar,
+                       hipStream_t stream) {
+    using Gm = SumGeom<T, D>;
+    const hga_params& p = plan.p;
+    const int gpc = p.chunk / p.group;
+    const int n_chunks = chunk_end - chunk_begin;
+    const int n_bh = p.batch * p.n_kv_heads;
+    const int64_t items = static_cast<int64_t>(n_bh) * n_chunks;
+    int64_t sum_blocks = (items + kWaves - 1) / kWaves;
+    if (sum_blocks > 4096) sum_blocks = 4096;
+    const int64_t q_blocks = (static_cast<int64_t>(n_bh) * n_q_chunks + kWaves - 1) / kWaves;
+    if (sum_blocks + q_blocks > (int64_t(1) << 30)) return hipErrorInvalidConfiguration;
+    const size_t lds = sizeof(float) * (2 * p.group * (Gm::HALF + 4) + 2 * gpc * (Gm::HALF + 4) +
+                                        kWaves * 2 * Gm::SLICES * (D + 4));
+    hipLaunchKernelGGL((summaries_qbar_kernel<T, D>),
+                       dim3(static_cast<unsigned>(sum_blocks + q_blocks)), dim3(kThreads), lds,
+                       stream, static_cast<const T*>(k_rot), k_tokens, k_chunk0, chunk_begin,
+                       n_chunks, chunk_sum, group_sum, table_chunks, n_bh, plan.phase_group,
+                       plan.phase_psi, p.group, p.hf_pairs_chunk, static_cast<int>(sum_blocks),
+                       static_cast<const T*>(q_rot), n_q_chunks, qbar, p.n_q_heads, p.n_kv_heads);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_summaries_qbar(const hga_plan& plan, const void* k_rot, int64_t k_tokens,
+                                 int k_chunk0, int chunk_begin, int chunk_end, float* chunk_sum,
+                                 float* group_sum, int table_chunks, const void* q_rot,
+                                 int q_chunk0, int n_q_chunks, float* qbar, hipStream_t stream) {
+    (void)q_chunk0;  // q_bar depends on the query rows only
+    const hga_params& p = plan.p;
+    if (p.dtype == HGA_F32) {
+        if (p.head_dim == 64)
+            return launch_sq_t<float, 64>(plan, k_rot, k_tokens, k_chunk0, chunk_begin, chunk_end,
+                                          chunk_sum, group_sum, table_chunks, q_rot, n_q_chunks,
+                                          qbar, stream);
+        return launch_sq_t<float, 128>(plan, k_rot, k_tokens, k_chunk0, chunk_begin, chunk_end,
+                                       chunk_sum, group_sum, table_chunks, q_rot, n_q_chunks,
+                                       qbar, stream);
+    }
+    if (p.head_dim == 64)
+        return launch_sq_t<bf16_t, 64>(plan, k_rot, k_tokens, k_chunk0, chunk_begin, chunk_end,
+                                       chunk_sum, group_sum, table_chunks, q_rot, n_q_chunks, qbar,
+                                       stream);
+    return launch_sq_t<bf16_t, 128>(plan, k_rot, k_tokens, k_chunk0, chunk_begin, chunk_end,
+                                    chunk_sum, group_sum, table_chunks, q_rot, n_q_chunks, qbar,
+                                    stream);
+}
 
 hipError_t launch_build_summaries(const hga_plan& plan, const void* k_rot, int64_t k_tokens,
                                   int k_chunk0, int chunk_begin, int chunk_end, float* chunk_sum,

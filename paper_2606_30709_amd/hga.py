@@ -17,8 +17,8 @@ import torch
 __all__ = [
     "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
-    "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_status_string", "hga_last_error",
-    "hga_version",
+    "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
+    "hga_attend_timed", "hga_status_string", "hga_last_error", "hga_version",
     "EXPORTED_SYMBOLS",
 ]
 
@@ -27,8 +27,8 @@ _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 
 EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
-    "hga_route_chunks", "hga_route_groups", "hga_route", "hga_gather_kv", "hga_attend",
-    "hga_attend_timed", "hga_status_string", "hga_last_error", "hga_version",
+    "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
+    "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_status_string", "hga_last_error", "hga_version",
 )
 
 
@@ -75,6 +75,9 @@ def library() -> ctypes.CDLL:
             "hga_route_chunks": [vp, vp, i32, i32, vp, i32, vp, vp, vp],
             "hga_route_groups": [vp, vp, vp, i32, i32, vp, i32, vp, vp],
             "hga_route": [vp, vp, i32, i32, vp, vp, i32, vp, vp, vp, vp],
+            "hga_build_summaries_qbar": [vp, vp, i64, i32, i32, i32, vp, vp, i32, vp, i32, i32,
+                                         vp, vp],
+            "hga_route_qbar": [vp, vp, i32, i32, vp, vp, i32, vp, vp, vp],
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
@@ -213,6 +216,24 @@ def hga_route(plan: Plan, q_rot, q_chunk0: int, chunk_sum, group_sum, qbar, chun
     _check(library().hga_route(
         plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(chunk_sum), _ptr(group_sum),
         chunk_sum.shape[2], _ptr(qbar), _ptr(chunk_idx), _ptr(group_idx), _stream(stream)))
+
+
+def hga_build_summaries_qbar(plan: Plan, k_rot, k_chunk0: int, chunk_begin: int, chunk_end: int,
+                             chunk_sum, group_sum, q_rot, q_chunk0: int, qbar, stream=None):
+    """hga_build_summaries and the query means of q_rot in one launch."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_build_summaries_qbar(
+        plan.handle, _ptr(k_rot), k_rot.shape[2], k_chunk0, chunk_begin, chunk_end,
+        _ptr(chunk_sum), _ptr(group_sum), chunk_sum.shape[2], _ptr(q_rot), q_chunk0, nq,
+        _ptr(qbar), _stream(stream)))
+
+
+def hga_route_qbar(plan: Plan, qbar, q_chunk0: int, chunk_sum, group_sum, chunk_idx, group_idx,
+                   stream=None):
+    """hga_route's selection stages from a given qbar [B, Hkv, n_q_chunks, d]."""
+    _check(library().hga_route_qbar(
+        plan.handle, _ptr(qbar), q_chunk0, qbar.shape[2], _ptr(chunk_sum), _ptr(group_sum),
+        chunk_sum.shape[2], _ptr(chunk_idx), _ptr(group_idx), _stream(stream)))
 
 
 def hga_gather_kv(plan: Plan, group_idx, q_chunk0: int, k_src, v_src, k_routed, v_routed,

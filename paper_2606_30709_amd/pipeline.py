@@ -10,9 +10,11 @@ always-visible first and recent chunks and the current 64-token block.  One
 step routes the block, gathers only its routed groups over the host link,
 attends, and appends the block's summaries (the store's "append").
 
-Routing runs as the single fused call ``hga_route`` by default
-(``fused_route=False`` issues ``hga_route_chunks`` then ``hga_route_groups``;
-both write bit-identical indices).  Both pipelines only allocate with torch and
+Prefill routing has three equivalent forms (bit-identical summaries, query
+means and indices), chosen by ``route_mode``: "fused" (``hga_build_summaries``
+then ``hga_route``), "separate" (``hga_route_chunks`` then
+``hga_route_groups``), and "qbar" (``hga_build_summaries_qbar``, which also
+reduces the query means in the same launch, then ``hga_route_qbar``).  Both pipelines only allocate with torch and
 call the binding; all arithmetic runs in the HIP library.
 """
 
@@ -38,10 +40,11 @@ def to_device(arr: np.ndarray, dtype: str, device="cuda", pin=False) -> torch.Te
 
 class PrefillPipeline:
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 fused_route: bool = True):
+                 route_mode: str = "qbar"):
         assert not w.decode_block
+        assert route_mode in ("fused", "separate", "qbar")
         self.w = w
-        self.fused_route = fused_route
+        self.route_mode = route_mode
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
         nc = w.n_chunks
@@ -61,11 +64,20 @@ class PrefillPipeline:
         self.lse = torch.empty(B, w.n_q_heads, w.seq_len, dtype=f32, device=device)
 
     def summaries(self, stream=None):
+        if self.route_mode == "qbar":
+            hga.hga_build_summaries_qbar(self.plan, self.k, 0, 0, self.w.n_chunks,
+                                         self.chunk_sum, self.group_sum, self.q, 0, self.qbar,
+                                         stream=stream)
+            return
         hga.hga_build_summaries(self.plan, self.k, 0, self.w.n_chunks, self.chunk_sum,
                                 self.group_sum, stream=stream)
 
     def route(self, stream=None):
-        if self.fused_route:
+        if self.route_mode == "qbar":
+            hga.hga_route_qbar(self.plan, self.qbar, 0, self.chunk_sum, self.group_sum,
+                               self.chunk_idx, self.group_idx, stream=stream)
+            return
+        if self.route_mode == "fused":
             hga.hga_route(self.plan, self.q, 0, self.chunk_sum, self.group_sum, self.qbar,
                           self.chunk_idx, self.group_idx, stream=stream)
             return

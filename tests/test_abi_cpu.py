@@ -79,6 +79,9 @@ def test_calls_reject_null_plan():
     assert lib.hga_route_chunks(None, None, 0, 0, None, 0, None, None, None) == -1
     assert lib.hga_route_groups(None, None, None, 0, 0, None, 0, None, None) == -1
     assert lib.hga_route(None, None, 0, 0, None, None, 0, None, None, None, None) == -1
+    assert lib.hga_build_summaries_qbar(None, None, 0, 0, 0, 0, None, None, 0, None, 0, 0, None,
+                                        None) == -1
+    assert lib.hga_route_qbar(None, None, 0, 0, None, None, 0, None, None, None) == -1
     assert lib.hga_gather_kv(None, None, 0, 0, None, None, 0, 0, None, None, None) == -1
     assert lib.hga_attend(None, None, 0, 0, None, None, 0, None, None, None, None, None, None,
                           None) == -1

@@ -266,6 +266,63 @@ def test_fused_route_equals_separate_calls(hga, key):
     assert torch.equal(ga, ga_all[:, :, c0:c0 + n])
 
 
+def _split_route_check(hga, plan, k, k_chunk0, n_chunks, table_chunks, q, q_chunk0, w):
+    """hga_build_summaries_qbar + hga_route_qbar against hga_build_summaries +
+    hga_route, bit for bit."""
+    B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
+    nq = q.shape[2] // C
+    outs = []
+    for split in (False, True):
+        cs = torch.full((B, Hkv, table_chunks, d), float("nan"), device="cuda")
+        gs = torch.full((B, Hkv, table_chunks * (C // G), d), float("nan"), device="cuda")
+        qbar = torch.full((B, Hkv, nq, d), float("nan"), device="cuda")
+        ci = torch.full((B, Hkv, nq, w.topk_chunks), -7, dtype=torch.int32, device="cuda")
+        gi = torch.full((B, Hkv, nq, w.topk_groups), -7, dtype=torch.int32, device="cuda")
+        if split:
+            hga.hga_build_summaries_qbar(plan, k, k_chunk0, k_chunk0, k_chunk0 + n_chunks, cs, gs,
+                                         q, q_chunk0, qbar)
+            hga.hga_route_qbar(plan, qbar, q_chunk0, cs, gs, ci, gi)
+        else:
+            hga.hga_build_summaries(plan, k, k_chunk0, k_chunk0 + n_chunks, cs, gs)
+            hga.hga_route(plan, q, q_chunk0, cs, gs, qbar, ci, gi)
+        outs.append((cs, gs, qbar, ci, gi))
+    torch.cuda.synchronize()
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+@pytest.mark.parametrize("key", list(FUSED_CASES))
+def test_summaries_qbar_and_route_qbar_equal_fused(hga, key):
+    """The summaries + query means launch and the routing from that q_bar
+    write what the summaries call and hga_route write."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = FUSED_CASES[key]
+    _say(f"[split-route] {key}")
+    pipe = PrefillPipeline(w, W.generate(w))
+    _split_route_check(hga, pipe.plan, pipe.k, 0, w.n_chunks, w.n_chunks, pipe.q, 0, w)
+    # a query block mid-sequence, summaries of every chunk before its end
+    c0 = w.n_chunks // 2 + 1
+    n = min(5, w.n_chunks - c0)
+    qb = pipe.q[:, :, c0 * w.chunk:(c0 + n) * w.chunk].contiguous()
+    _split_route_check(hga, pipe.plan, pipe.k, 0, c0 + n, w.n_chunks, qb, c0, w)
+
+
+def test_summaries_qbar_decode_and_full_size(hga):
+    from paper_2606_30709_amd.pipeline import DecodePipeline, PrefillPipeline
+    w = W.preset("decode64k")
+    _say("[split-route] decode64k")
+    pipe = DecodePipeline(w, W.generate(w))
+    # the history's summaries from a device copy, then the block's routing
+    k_dev = pipe.k_hist.to("cuda")
+    _split_route_check(hga, pipe.plan, k_dev, 0, pipe.c, pipe.c + 1, pipe.q, pipe.c, w)
+    del k_dev
+    for key in ("smalllm", "qwen32k"):
+        w = W.preset(key)
+        _say(f"[split-route] {key}")
+        pipe = PrefillPipeline(w, W.generate(w))
+        _split_route_check(hga, pipe.plan, pipe.k, 0, w.n_chunks, w.n_chunks, pipe.q, 0, w)
+
+
 def test_fused_route_decode_and_full_size(hga):
     from paper_2606_30709_amd.pipeline import DecodePipeline, PrefillPipeline
     w = W.preset("decode64k")
