@@ -12,11 +12,11 @@ prefill (B4, 8/8 heads, d64, 8192 tokens, bf16, C64 G16, first chunk hot,
 K_c 3, K_g 4 -> 3.125% of the context fetched by the last chunk).
 
 Prints one JSON line.  The step rate comes from the wall clock between two
-synchronizations around the timed steps.  In every timed step the dominant
-kernel (attention) is launched through hga_attend_timed, whose dispatch
-records a pair of HIP events at the kernel's own start and end on the
-launch stream; its algorithmic bytes over the mean duration give the
-roofline entry.  A second pass with events between all calls gives the
+synchronizations around the timed steps.  In about ten of the timed steps,
+spread evenly over them, the dominant kernel (attention) is launched through
+hga_attend_timed, whose dispatch records a pair of HIP events at the
+kernel's own start and end on the launch stream; its algorithmic bytes over
+the mean duration give the roofline entry.  A second pass with events between all calls gives the
 per-stage breakdown of the other kernels.
 The float64 oracle timed on the host cores over a bounded sample of the same
 workload gives the CPU baseline.
@@ -181,8 +181,8 @@ def cpu_baseline(w, inp, max_seconds: float) -> dict:
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="smalllm",
                     help="workload preset (default smalllm, the SmallLM-shaped prefill)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
@@ -259,14 +259,20 @@ def main():
             f()
     torch.cuda.synchronize()
 
-    # Timed region: K steps; the dominant kernel (attention) records a pair of
-    # HIP events at its own dispatch start and end in every step; whole-step
-    # rate from the wall clock between two synchronizations.
+    # Timed region: K steps; in a sample of them spread evenly over the
+    # region (every `stride`-th step, at least ten, all of them for K <= 10)
+    # the dominant kernel (attention) records a pair of HIP events at its own
+    # dispatch start and end.  Recording events costs a few microseconds of
+    # dispatch per step, so timing every step would lower the rate measured
+    # for the whole region; whole-step rate from the wall clock between two
+    # synchronizations.
     K = args.steps
     att = len(calls) - 1
-    ev_a = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in range(K)]
-    for a, b in ev_a:  # events exist once recorded; the kernel dispatch re-records them
+    stride = max(1, K // 10)
+    timed_steps = set(range(0, K, stride))
+    ev_a = {s: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for s in timed_steps}
+    for a, b in ev_a.values():  # events exist once recorded; the dispatch re-records them
         a.record(stream)
         b.record(stream)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -275,14 +281,14 @@ def main():
     ev0.record(stream)
     for s in range(K):
         for n, f in enumerate(calls):
-            if n == att:
+            if n == att and s in timed_steps:
                 attend_timed(ev_a[s][0], ev_a[s][1])
             else:
                 f()
     ev1.record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    attend_ms = float(np.mean([a.elapsed_time(b) for a, b in ev_a]))
+    attend_ms = float(np.mean([a.elapsed_time(b) for a, b in ev_a.values()]))
     gpu_step_ms = ev0.elapsed_time(ev1) / K
 
     # Breakdown pass (same workload, right after): events between all calls.
@@ -322,7 +328,8 @@ def main():
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(w.key) if dominant == "attend" else None,
                 "alg_bytes_per_launch": abytes[dominant],
-                "mean_launch_us": round(stage_ms[dominant] * 1e3, 2)}
+                "mean_launch_us": round(stage_ms[dominant] * 1e3, 2),
+                "timed_launches": len(timed_steps) if dominant == "attend" else KB}
 
     res = {
         "metric": "routed-attn tokens/s per layer",
@@ -345,9 +352,9 @@ def main():
             "seed": inp["seed"],
         },
         "gpu_ms_per_step_events": round(gpu_step_ms, 4),
-        "stage_timing": ("attend: HIP events recorded by its own dispatch in every timed step; "
-                         "other stages: a second pass of the same steps with events between "
-                         "all calls"),
+        "stage_timing": (f"attend: HIP events recorded by its own dispatch in {len(timed_steps)} "
+                         f"of the {K} timed steps (every {stride}th); other stages: a second "
+                         "pass of the same steps with events between all calls"),
         "stages": stages,
         "route_calls": args.route,
         "roofline": roofline,
