@@ -39,6 +39,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
+VALU_FP32_PEAK_TFLOPS = 157.3   # fp32 vector peak (256 CUs at 2.4 GHz)
 
 STAGES = {
     "qbar": ("build_summaries_qbar", "route_qbar", "gather_kv", "attend"),
@@ -323,13 +324,28 @@ def main():
             ent["mfma_frac"] = round(flops / sec / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
         stages[sname] = ent
     dsec = stage_ms[dominant] * 1e-3
-    achieved = abytes[dominant] / dsec / 1e9
-    roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+    # Bound by arithmetic intensity: attention above the ridge point (peak
+    # compute / peak HBM bandwidth) is priced against the compute peak of its
+    # own arithmetic (bf16 matrix cores, or fp32 vector ALUs for the fp32
+    # kernel), everything else against HBM.
+    cpeak, cbound = ((MFMA_BF16_PEAK_TFLOPS, "mfma") if w.dtype == "bf16"
+                     else (VALU_FP32_PEAK_TFLOPS, "alu"))
+    compute_bound = (dominant == "attend" and
+                     flops / abytes[dominant] > cpeak * 1e12 / (HBM_PEAK_GBS * 1e9))
+    if compute_bound:
+        achieved = flops / dsec / 1e12
+        roofline = {"bound": cbound, "kernel": dominant, "achieved": round(achieved, 2),
+                    "peak": cpeak, "unit": "TFLOP/s", "frac": round(achieved / cpeak, 4),
+                    "alg_flops_per_launch": flops}
+    else:
+        achieved = abytes[dominant] / dsec / 1e9
+        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    roofline.update({
                 "traffic": measured_traffic(w.key) if dominant == "attend" else None,
                 "alg_bytes_per_launch": abytes[dominant],
                 "mean_launch_us": round(stage_ms[dominant] * 1e3, 2),
-                "timed_launches": len(timed_steps) if dominant == "attend" else KB}
+                "timed_launches": len(timed_steps) if dominant == "attend" else KB})
 
     res = {
         "metric": "routed-attn tokens/s per layer",

@@ -23,8 +23,9 @@
 // so no VGPRs stage the tiles.  The key tiles cycle through NS LDS stages:
 // when tile t is consumed, tiles t+1 .. t+NS-2 are already in flight and the
 // copy of tile t+NS-1 is issued into the stage tile t-1 has freed, with one
-// workgroup barrier per tile.  The workgroup's query rows and the unit's
-// group ids arrive the same way before the first tile.  Each copy lane
+// workgroup barrier per tile; the first NS tiles are requested together at
+// the start.  The unit's group ids arrive the same way; each wavefront
+// loads its query fragments straight into registers.  Each copy lane
 // picks its source 16 bytes so that K lands row-major with an XOR swizzle
 // and V in the order its transpose reads consume it (see swz_k and
 // v_slot_source): LDS reads are free of bank conflicts, and the V reads are
@@ -93,7 +94,7 @@ __device__ __forceinline__ void wait_loads() {
 }
 
 // LDS layout of a staged tile.
-// * K and the query rows are row-major, unpadded, with the 16-byte chunk j of
+// * K is row-major, unpadded, with the 16-byte chunk j of
 //   row r stored at j ^ swz_k(r): the 16-byte A/B fragments read by 32 lanes
 //   on 32 consecutive rows then fall in distinct banks, and each copy reads
 //   whole rows.  (For D = 128, 16 chunks per row, the map uses four bits.)
@@ -181,8 +182,9 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
     const int half = lane >> 5, col = lane & 31;
     const float scale = 1.4426950408889634f / sqrtf(static_cast<float>(D));  // log2(e)/sqrt(d)
 
-    // S^T of 32-key sub-tile st, masked
-    auto qk = [&](int st, f32x16_t& sacc) {
+    // S^T of 32-key sub-tile st, masked (`diag`: the current chunk's
+    // sub-tile holding this wave's own tokens, under the causal mask)
+    auto qk = [&](int st, f32x16_t& sacc, bool diag) {
         const int krow = st * 32 + col;
         bf16x8_t kf[NKS];
 #pragma unroll
@@ -194,10 +196,12 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
         for (int kk = 0; kk < NKS; ++kk)
             sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sacc, 0, 0, 0);
         if (kCurrent) {
+            if (diag) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
-                sacc[e] = key > t ? -INFINITY : sacc[e];
+                for (int e = 0; e < 16; ++e) {
+                    const int key = st * 32 + (e >> 2) * 8 + half * 4 + (e & 3);
+                    sacc[e] = key > t ? -INFINITY : sacc[e];
+                }
             }
         } else if (partial) {
 #pragma unroll
@@ -210,8 +214,11 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
             }
         }
     };
-    // online-softmax update with the scores of `n` sub-tiles; P as bf16
-    auto update = [&](const f32x16_t* sacc, int n, bf16x8_t* pf) {
+    // online-softmax update with the scores of `n` sub-tiles; P as bf16.
+    // kFirst: the wave's first scores (O and l still zero, and every lane
+    // has a visible key among them), so the reference point is simply set.
+    auto update = [&](const f32x16_t* sacc, int n, bf16x8_t* pf, auto first_tag) {
+        constexpr bool kFirst = decltype(first_tag)::value;
         float tmax = -INFINITY;
         for (int k = 0; k < n; ++k)
 #pragma unroll
@@ -225,7 +232,9 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
         // result is the softmax for any reference point.
         constexpr float kSlack = 8.0f;
         const bool grow = tmax > m_run + kSlack;  // false while the row is fully masked
-        if (__builtin_amdgcn_ballot_w64(grow)) {
+        if (kFirst) {
+            m_run = tmax;
+        } else if (__builtin_amdgcn_ballot_w64(grow)) {
             const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - tmax) : 1.0f;
             l_run *= alpha;
 #pragma unroll
@@ -266,20 +275,50 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
         }
     };
 
-    if constexpr (NST == 1) {
+    using First = BoolTag<true>;
+    using Later = BoolTag<false>;
+    if constexpr (kCurrent) {
+        // The current chunk: this wave's tokens t lie in 32-key sub-tile tq
+        // (the same for every lane).  Sub-tiles before tq are fully visible,
+        // tq is the diagonal, later ones are fully masked and skipped.
+        const int tq = __builtin_amdgcn_readfirstlane(t) >> 5;
+        if constexpr (NST == 1) {
+            if (ksplit > tq) return;
+            f32x16_t sacc[1];
+            bf16x8_t pf[2];
+            qk(ksplit, sacc[0], ksplit == tq);
+            update(sacc, 1, pf, First{});
+            pv(ksplit, pf);
+        } else if (tq == 0) {
+            f32x16_t s0[1];
+            bf16x8_t p0[2];
+            qk(0, s0[0], true);
+            update(s0, 1, p0, First{});
+            pv(0, p0);
+        } else {
+            f32x16_t s0[1], s1[1];
+            bf16x8_t p0[2], p1[2];
+            qk(0, s0[0], false);
+            qk(1, s1[0], true);
+            update(s0, 1, p0, First{});
+            pv(0, p0);
+            update(s1, 1, p1, Later{});
+            pv(1, p1);
+        }
+    } else if constexpr (NST == 1) {
         f32x16_t sacc[1];
         bf16x8_t pf[2];
-        qk(ksplit, sacc[0]);
-        update(sacc, 1, pf);
+        qk(ksplit, sacc[0], false);
+        update(sacc, 1, pf, Later{});
         pv(ksplit, pf);
     } else {
         f32x16_t s0[1], s1[1];
         bf16x8_t p0[2], p1[2];
-        qk(0, s0[0]);
-        qk(1, s1[0]);
-        update(s0, 1, p0);
+        qk(0, s0[0], false);
+        qk(1, s1[0], false);
+        update(s0, 1, p0, Later{});
         pv(0, p0);
-        update(s1, 1, p1);
+        update(s1, 1, p1, Later{});
         pv(1, p1);
     }
 }
@@ -300,6 +339,8 @@ __device__ __forceinline__ bool routed_tile_partial(int rt_row0, const int* s_gi
 // Combine the two key halves of a query tile (KS == 2) through LDS (`area`:
 // QT * 64 * NDT*16 floats, `ml`: QT * 128 floats, both free), then store the
 // normalised output and the log-sum-exp.  Every wave of the workgroup calls.
+// The normalisation 1/l is folded into the two merge factors, so each output
+// element costs one multiply and one fma.
 template <int D, int KS, int QT>
 __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_run, float l_run,
                                             float* area, float* ml_area, int qt_local, int ksplit,
@@ -307,9 +348,10 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
     constexpr int NDT = D / 32;
     const int lane = threadIdx.x & 63, half = lane >> 5;
     float l_tot = add_xor32(l_run);
+    // element k of the partner's accumulator at [qt_local][k][lane]: lanes contiguous
+    float* mine = area + qt_local * (NDT * 16 * 64) + lane;
+    float f_own = 1.f, f_other = 0.f;
     if (KS == 2) {
-        // element k of this lane at [qt_local][k][lane]: lanes contiguous
-        float* mine = area + qt_local * (NDT * 16 * 64) + lane;
         float* ml = ml_area + qt_local * 128 + lane;
         if (ksplit == 1) {
 #pragma unroll
@@ -324,18 +366,18 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
             const float mb = ml[0], lb = ml[64];
             const float m = fmaxf(m_run, mb);
             const float mu = m == -INFINITY ? 0.f : m;
-            const float fa = __builtin_amdgcn_exp2f(m_run - mu), fb = __builtin_amdgcn_exp2f(mb - mu);
-#pragma unroll
-            for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    oacc[dt][e] = oacc[dt][e] * fa + mine[(dt * 16 + e) * 64] * fb;
-            l_tot = l_tot * fa + lb * fb;
+            f_own = __builtin_amdgcn_exp2f(m_run - mu);
+            f_other = __builtin_amdgcn_exp2f(mb - mu);
+            l_tot = l_tot * f_own + lb * f_other;
             m_run = m;
         }
     }
     if (!qactive || ksplit != 0) return;
-    const float inv = bad ? NAN : 1.0f / l_tot;
+    // l_tot >= 1 (the key that set the reference point contributes exp2(0)),
+    // so the hardware reciprocal is within one ulp.
+    const float inv = bad ? NAN : __builtin_amdgcn_rcpf(l_tot);
+    f_own *= inv;
+    f_other *= inv;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
@@ -344,7 +386,13 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
             typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
             bf16x4_t o;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = static_cast<__bf16>(oacc[dt][g4 * 4 + e] * inv);
+            for (int e = 0; e < 4; ++e) {
+                const int k = g4 * 4 + e;
+                const float x = KS == 2 ? fmaf(mine[(dt * 16 + k) * 64], f_other,
+                                               oacc[dt][k] * f_own)
+                                        : oacc[dt][k] * f_own;
+                o[e] = static_cast<__bf16>(x);
+            }
             *reinterpret_cast<bf16x4_t*>(orow + d0) = o;
         }
     if (lse_at && half == 0) *lse_at = bad ? NAN : (m_run + log2f(l_tot)) * 0.6931471805599453f;
@@ -361,8 +409,9 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const bf16_t* __restrict__ k_res, const bf16_t* __restrict__ v_res, int64_t res_tokens,
     const int32_t* __restrict__ res_slot, const bf16_t* __restrict__ k_routed,
     const bf16_t* __restrict__ v_routed, const int32_t* __restrict__ group_idx,
-    bf16_t* __restrict__ out, float* __restrict__ lse, int n_q_heads, int n_kv, int group_shift,
-    int keep_first, int window, int topk_groups, int wg_per_unit, int n_blocks) {
+    bf16_t* __restrict__ out, float* __restrict__ lse, int r, FastDiv kv_div, int group_shift,
+    int keep_first, int window, int topk_groups, FastDiv wg_div, FastDiv chunk_div,
+    int n_blocks) {
     using Lay = Layout<D, NS>;
     constexpr uint32_t kRowBytes = Lay::kRowBytes, kTileBytes = Lay::kTileBytes,
                        kStageBytes = Lay::kStageBytes;
@@ -371,10 +420,8 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     constexpr int QT = NW / KS;                  // query tiles per workgroup
     constexpr int KI = kTileBytes / 1024 / NW;   // copies per wave per tile, for K (and V)
     constexpr int LPT = 2 * KI;                  // loads per wave per tile
-    constexpr int QI = QT * 32 * kRowBytes / 1024 / NW;  // copies per wave for the query rows
     constexpr int GI = kMaxGroupSlots * 4 / 256 / NW;    // copies per wave for the group ids
-    static_assert(KI >= 1 && QI >= 1 && GI >= 1, "copy split");
-    static_assert(QT * 32 * kRowBytes <= kStageBytes, "query rows fit one stage");
+    static_assert(KI >= 1 && GI >= 1, "copy split");
     static_assert(NS >= 2 && NS <= 4, "stages");
     static_assert(KS == 1 || QT * 64 * NDT * 16 * 4 <= NS * kStageBytes, "merge area");
 
@@ -388,16 +435,17 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const int per_xcd = (n_blocks + kXcds - 1) / kXcds;
     const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     if (logical >= n_blocks) return;
-    const int part = logical % wg_per_unit;
-    const int i = (logical / wg_per_unit) % n_q_chunks;
-    const int bh = logical / wg_per_unit / n_q_chunks;
+    const int unit_id = wg_div.div(logical);
+    const int part = logical - unit_id * wg_div.d;
+    const int bh = chunk_div.div(unit_id);
+    const int i = unit_id - bh * n_q_chunks;
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int half = lane >> 5, col = lane & 31;
-    const int r = n_q_heads / n_kv;
     const int nqt = 2 * r;
-    const int b = bh / n_kv, j = bh % n_kv;
+    const int n_kv = kv_div.d, n_q_heads = r * n_kv;
+    const int b = kv_div.div(bh), j = bh - b * n_kv;
     const int c = q_chunk0 + i;
     const int group = 1 << group_shift;
     const int gpc = KT >> group_shift;
@@ -405,7 +453,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const int qtile = part * QT + qt_local;
     const int ksplit = wave / QT;
     const bool qactive = qtile < nqt;
-    const int64_t unit = static_cast<int64_t>(bh) * n_q_chunks + i;
+    const int64_t unit = unit_id;
     const int routed_rows = topk_groups * group;
     const int64_t res_chunks = res_tokens / KT;
 
@@ -416,29 +464,8 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const u32x4 rk_rt = rsrc_words(k_routed + unit * routed_rows * D, routed_rows * kRowBytes);
     const u32x4 rv_rt = rsrc_words(v_routed + unit * routed_rows * D, routed_rows * kRowBytes);
 
-    // 1. The workgroup's query rows into the last stage (swizzled like K),
-    //    and the unit's group ids.
+    // The unit's group ids into LDS.
     {
-        const int64_t qtok = static_cast<int64_t>(n_q_chunks) * KT;
-        const int64_t q_head0 = (static_cast<int64_t>(b) * n_q_heads + j * r) * qtok;
-        const u32x4 rq =
-            rsrc_words(q_rot + q_head0 * D, static_cast<uint32_t>(r * qtok * kRowBytes));
-        const uint32_t qbase = lds0 + (NS - 1) * kStageBytes;
-#pragma unroll
-        for (int u = 0; u < QI; ++u) {
-            const int blk = u * NW + wave;
-            const int pch = blk * 64 + lane;
-            const int row = pch / (D / 8), pc = pch % (D / 8);
-            const int urow = part * QT * 32 + row;  // query row within the unit
-            uint32_t off = kAbsent;
-            if (urow < r * KT) {
-                const int qh = urow / KT, qt = urow % KT;
-                off = static_cast<uint32_t>((qh * qtok + static_cast<int64_t>(i) * KT + qt) *
-                                            kRowBytes) +
-                      (pc ^ swz_k<D>(row)) * 16;
-            }
-            copy16_to_lds(rq, off, qbase + blk * 1024);
-        }
         const u32x4 rg = rsrc_words(group_idx + unit * topk_groups, topk_groups * 4);
 #pragma unroll
         for (int u = 0; u < GI; ++u) {
@@ -453,6 +480,16 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const int64_t qrow = (static_cast<int64_t>(b) * n_q_heads + j * r + (qactive ? hh : 0)) *
                              (static_cast<int64_t>(n_q_chunks) * KT) +
                          static_cast<int64_t>(i) * KT + t;
+    // Query fragments (B operand of S^T = K.Q^T), straight from global
+    // memory into registers: row qrow, dimensions kk*16 + half*8 .. +8.
+    // They are requested before any key tile, so they have arrived once the
+    // first tile has.
+    bf16x8_t qf[NKS];
+    {
+        const bf16_t* qp = q_rot + qrow * D + half * 8;
+#pragma unroll
+        for (int kk = 0; kk < NKS; ++kk) qf[kk] = __builtin_bit_cast(bf16x8_t, load16(qp + kk * 16));
+    }
 
     // tile order: the current chunk, the visible closed chunks, the routed rows
     const VisibleChunks vis(c, keep_first, window);
@@ -499,7 +536,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
             copy16_to_lds(rv, base + voff[u], sk + kTileBytes + (u * NW + wave) * 1024);
     };
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
+    for (int s = 0; s < NS; ++s)
         if (s < n_tiles) issue(s, s);
 
     f32x16_t oacc[NDT];
@@ -508,34 +545,27 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
 #pragma unroll
         for (int e = 0; e < 16; ++e) oacc[dt][e] = 0.f;
     float m_run = -INFINITY, l_run = 0.f;  // m_run in scaled (log2) units
-    bf16x8_t qf[NKS];
 
     // One key tile: wait for its copies, issue a later tile's, then the
-    // tile's arithmetic.  The current chunk (tile 0, under the causal mask)
-    // is a separate instantiation so the other tiles carry no mask work.
+    // tile's arithmetic.  Tiles 0 .. NS-1 were issued up front; from tile 1
+    // on, tile + NS - 1 goes into the stage tile - 1 has freed.  The current
+    // chunk (tile 0, under the causal mask) is a separate instantiation so
+    // the other tiles carry no mask work.
     auto step = [&](int tile, auto current_tag) {
         constexpr bool kCurrent = decltype(current_tag)::value;
         // this wave's copies of `tile` are done once at most `ahead` later
-        // tiles' copies remain in flight
-        const int ahead = min(NS - 2, n_tiles - 1 - tile);
-        if (NS >= 4 && ahead >= 2)
-            wait_loads<(NS >= 4 ? 2 : 0) * LPT>();
-        else if (NS >= 3 && ahead >= 1)
-            wait_loads<(NS >= 3 ? 1 : 0) * LPT>();
+        // tiles' copies remain in flight (loads complete in issue order)
+        const int ahead = min(kCurrent ? NS - 1 : NS - 2, n_tiles - 1 - tile);
+        if (NS >= 4 && ahead >= 3)
+            wait_loads<(NS >= 4 ? 3 : 0) * LPT>();
+        else if (NS >= 3 && ahead >= 2)
+            wait_loads<(NS >= 3 ? 2 : 0) * LPT>();
+        else if (ahead >= 1)
+            wait_loads<LPT>();
         else
             wait_loads<0>();
         __syncthreads();
-        if (kCurrent) {
-            // query fragments (B operand of S^T = K.Q^T): row qt_local*32 + col,
-            // dimensions kk*16 + half*8 .. +8
-            const bf16_t* sq = reinterpret_cast<const bf16_t*>(smem + (NS - 1) * kStageBytes);
-            const int row = qt_local * 32 + col;
-#pragma unroll
-            for (int kk = 0; kk < NKS; ++kk)
-                qf[kk] = lds_frag(sq + row * D + ((2 * kk + half) ^ swz_k<D>(row)) * 8);
-            __syncthreads();  // the last stage is overwritten next
-        }
-        if (tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
+        if (!kCurrent && tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
 
         const int stage = tile % NS;
         const bf16_t* sK = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes);
@@ -578,8 +608,9 @@ hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev
     hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW>), dim3(grid), dim3(NW * 64), kLds,
                           stream, ev_start, ev_stop, 0, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
                           res_tokens, res_slot, k_routed, v_routed, group_idx, out, lse,
-                          p.n_q_heads, p.n_kv_heads, group_shift, p.keep_first, recent_window(p),
-                          p.topk_groups, wg_per_unit, n_items);
+                          p.n_q_heads / p.n_kv_heads, FastDiv(p.n_kv_heads), group_shift,
+                          p.keep_first, recent_window(p), p.topk_groups, FastDiv(wg_per_unit),
+                          FastDiv(n_q_chunks), n_items);
     return hipGetLastError();
 }
 

@@ -51,6 +51,25 @@ template <> struct elem<bf16_t> {
     __device__ static __forceinline__ bf16_t from_f32(float x) { return f32_to_bf16(x); }
 };
 
+// Division of n in [0, 2^31) by a divisor d in [1, 2^31) fixed for a whole
+// launch, by one high multiply, one add and one shift (Granlund and
+// Montgomery, "Division by invariant integers using multiplication", 1994):
+// with s = ceil(log2 d) and m = floor(2^32 (2^s - d) / d) + 1,
+// floor(n / d) = (mulhi(n, m) + n) >> s.  (m + 2^32 = floor(2^(32+s)/d) + 1
+// exceeds 2^(32+s)/d by at most 1, an error below 1/d for every n < 2^31;
+// the sum stays below 2^32.)  Built on the host, passed by value.
+struct FastDiv {
+    uint32_t d, m, s;
+    __host__ __device__ FastDiv() : d(1), m(1), s(0) {}
+    __host__ explicit FastDiv(uint32_t div) : d(div), m(0), s(0) {
+        while ((uint32_t(1) << s) < d) ++s;
+        m = static_cast<uint32_t>(((uint64_t(1) << 32) * ((uint64_t(1) << s) - d)) / d + 1);
+    }
+    __device__ __forceinline__ uint32_t div(uint32_t n) const {
+        return (__umulhi(n, m) + n) >> s;
+    }
+};
+
 __device__ __forceinline__ vec16 load16(const void* p) {
     return *reinterpret_cast<const vec16*>(p);
 }
