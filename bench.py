@@ -4,20 +4,23 @@
 One step = the whole hot path over one batch of synthetic input: chunk and
 group summaries, chunk routing, group refinement, gather of the routed K/V,
 and exact attention (inputs already resident in HBM).  By default a step is
-four C-ABI calls: hga_build_summaries_qbar (summaries and the routing query
-means in one launch), hga_route_qbar (chunk and group selection),
-hga_gather_kv and hga_attend; --route fused / separate use hga_route or the
-two routing calls instead (identical results).  The default workload is the SmallLM-shaped
-prefill (B4, 8/8 heads, d64, 8192 tokens, bf16, C64 G16, first chunk hot,
-K_c 3, K_g 4 -> 3.125% of the context fetched by the last chunk).
+three C-ABI calls: hga_build_summaries_qbar (summaries and the routing query
+means in one launch), hga_route_qbar (chunk and group selection) and
+hga_gather_attend (the attention stages each routed group's rows from the
+resident K/V and writes them to the routed buffers, the gather's output).
+--route fused / separate use hga_route or the two routing calls instead,
+--gather separate uses hga_gather_kv + hga_attend (identical results).  The
+default workload is the SmallLM-shaped prefill (B4, 8/8 heads, d64, 8192
+tokens, bf16, C64 G16, first chunk hot, K_c 3, K_g 4 -> 3.125% of the
+context fetched by the last chunk).
 
 Prints one JSON line.  The step rate comes from the wall clock between two
 synchronizations around the timed steps.  In about ten of the timed steps,
-spread evenly over them, the dominant kernel (attention) is launched through
-hga_attend_timed, whose dispatch records a pair of HIP events at the
-kernel's own start and end on the launch stream; its algorithmic bytes over
-the mean duration give the roofline entry.  A second pass with events between all calls gives the
-per-stage breakdown of the other kernels.
+spread evenly over them, the dominant kernel (the attention) is launched with
+a pair of HIP events that its dispatch records at the kernel's own start and
+end on the launch stream; its algorithmic bytes (or FLOPs, above the ridge
+point) over the mean duration give the roofline entry.  A second pass with
+events between all calls gives the per-stage breakdown of the other kernels.
 The float64 oracle timed on the host cores over a bounded sample of the same
 workload gives the CPU baseline.
 """
@@ -41,11 +44,16 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
 VALU_FP32_PEAK_TFLOPS = 157.3   # fp32 vector peak (256 CUs at 2.4 GHz)
 
-STAGES = {
-    "qbar": ("build_summaries_qbar", "route_qbar", "gather_kv", "attend"),
-    "fused": ("build_summaries", "route", "gather_kv", "attend"),
-    "separate": ("build_summaries", "route_chunks", "route_groups", "gather_kv", "attend"),
+ROUTE_STAGES = {
+    "qbar": ("build_summaries_qbar", "route_qbar"),
+    "fused": ("build_summaries", "route"),
+    "separate": ("build_summaries", "route_chunks", "route_groups"),
 }
+GATHER_STAGES = {
+    "fused": ("gather_attend",),
+    "separate": ("gather_kv", "attend"),
+}
+ATTENTION_STAGES = ("attend", "gather_attend")
 
 
 def algorithmic_bytes(w, n_valid_rows: int) -> dict:
@@ -71,6 +79,10 @@ def algorithmic_bytes(w, n_valid_rows: int) -> dict:
         "route_qbar": 2 * table_c + table_g + B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4,
         "gather_kv": 4 * routed + B * Hkv * nc * w.topk_groups * 4,
         "attend": q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4,
+        # the routed rows read from the resident K/V and written once to the
+        # routed buffers, never read back
+        "gather_attend": (q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4 +
+                          2 * routed + B * Hkv * nc * w.topk_groups * 4),
     }
 
 
@@ -92,7 +104,10 @@ def attention_flops(w, group_idx: np.ndarray) -> float:
 
 
 ATTEND_SOURCES = ("attend_mfma.hip", "attend_common.hpp", "hga_device.hpp", "hga_internal.hpp")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attend_smalllm_traffic.txt")
+
+
+def traffic_file(kernel: str, workload_key: str) -> str:
+    return os.path.join(ROOT, "profiles", f"{kernel}_{workload_key}_traffic.txt")
 COPY_BYTES = 256 << 20
 
 
@@ -105,12 +120,13 @@ def attend_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload_key: str):
-    """HBM bytes per attention launch from the committed counter summary, or
-    None when the kernel source changed since the counters were taken."""
+def measured_traffic(kernel: str, workload_key: str):
+    """HBM bytes per launch of the attention kernel (`kernel`: attend or
+    gather_attend) from the committed counter summary, or None when there is
+    none or the kernel source changed since the counters were taken."""
     try:
         vals = {}
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(kernel, workload_key)) as f:
             for line in f:
                 if "=" in line and not line.lstrip().startswith("#"):
                     k, v = (x.strip() for x in line.split("=", 1))
@@ -124,23 +140,28 @@ def measured_traffic(workload_key: str):
         return None
 
 
-def probe_traffic(w, inp):
-    """For counter collection: the pipeline once, attention 5 times, then 5
+def probe_traffic(w, inp, gather_mode: str):
+    """For counter collection: the pipeline once, the attention call 5 times
+    (hga_gather_attend, or hga_attend with gather_mode "separate"), then 5
     plain device copies of COPY_BYTES (the calibration for FETCH_SIZE and
     WRITE_SIZE)."""
     import torch
 
     from paper_2606_30709_amd.pipeline import PrefillPipeline
-    pipe = PrefillPipeline(w, inp)
+    pipe = PrefillPipeline(w, inp, gather_mode=gather_mode)
     pipe.step()
     for _ in range(5):
-        pipe.attend()
+        if gather_mode == "fused":
+            pipe.gather_attend()
+        else:
+            pipe.attend()
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
     for _ in range(5):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"probe": "traffic", "workload": w.key, "copy_bytes": COPY_BYTES,
+                      "kernel": "gather_attend" if gather_mode == "fused" else "attend",
                       "kernel_source_sha256": attend_source_hash()}), flush=True)
 
 
@@ -193,6 +214,10 @@ def main():
                     help="qbar: hga_build_summaries_qbar + hga_route_qbar; fused: "
                          "hga_build_summaries + hga_route; separate: hga_build_summaries + "
                          "hga_route_chunks + hga_route_groups (identical results)")
+    ap.add_argument("--gather", choices=("fused", "separate"), default="fused",
+                    help="fused: hga_gather_attend (the attention stages the routed rows and "
+                         "writes the routed buffers); separate: hga_gather_kv + hga_attend "
+                         "(identical results)")
     ap.add_argument("--probe-traffic", action="store_true",
                     help="run attention and a known-size copy for rocprofv3 --pmc, then exit")
     args = ap.parse_args()
@@ -215,9 +240,9 @@ def main():
     torch.cuda.set_device(0)
     inp = W.generate(w)
     if args.probe_traffic:
-        probe_traffic(w, inp)
+        probe_traffic(w, inp, args.gather)
         return
-    pipe = PrefillPipeline(w, inp)
+    pipe = PrefillPipeline(w, inp, route_mode=args.route, gather_mode=args.gather)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
     p = pipe.plan
@@ -226,34 +251,39 @@ def main():
                                                 pipe.group_sum, stream=sh)
     gather = lambda: hga.hga_gather_kv(p, pipe.group_idx, 0, pipe.k, pipe.v, pipe.k_routed,
                                        pipe.v_routed, stream=sh)
-    attend = lambda: hga.hga_attend(p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed,
-                                    pipe.group_idx, pipe.out, pipe.lse, stream=sh)
-    # the dominant kernel's own dispatch records these (hga_attend_timed)
-    attend_timed = lambda e0, e1: hga.hga_attend_timed(
-        p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed, pipe.group_idx, pipe.out,
-        e0, e1, lse=pipe.lse, stream=sh)
-    stage_names = STAGES[args.route]
+    if args.gather == "fused":
+        # the dominant kernel's own dispatch records e0/e1 when given
+        attend_timed = lambda e0, e1: hga.hga_gather_attend(
+            p, pipe.q, 0, pipe.k, pipe.v, pipe.group_idx, pipe.k_routed, pipe.v_routed, pipe.out,
+            pipe.lse, start_event=e0, stop_event=e1, stream=sh)
+        tail = (lambda: attend_timed(None, None),)
+    else:
+        attend_timed = lambda e0, e1: hga.hga_attend_timed(
+            p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed, pipe.v_routed, pipe.group_idx, pipe.out,
+            e0, e1, lse=pipe.lse, stream=sh)
+        tail = (gather, lambda: hga.hga_attend(p, pipe.q, 0, pipe.k, pipe.v, pipe.k_routed,
+                                               pipe.v_routed, pipe.group_idx, pipe.out,
+                                               pipe.lse, stream=sh))
+    stage_names = ROUTE_STAGES[args.route] + GATHER_STAGES[args.gather]
+    att_name = stage_names[-1]
     if args.route == "separate":
         calls = (
             summarise,
             lambda: hga.hga_route_chunks(p, pipe.q, 0, pipe.chunk_sum, pipe.qbar, pipe.chunk_idx,
                                          stream=sh),
             lambda: hga.hga_route_groups(p, pipe.qbar, pipe.chunk_idx, 0, pipe.group_sum,
-                                         pipe.group_idx, stream=sh),
-            gather, attend)
+                                         pipe.group_idx, stream=sh)) + tail
     elif args.route == "fused":
         calls = (
             summarise,
             lambda: hga.hga_route(p, pipe.q, 0, pipe.chunk_sum, pipe.group_sum, pipe.qbar,
-                                  pipe.chunk_idx, pipe.group_idx, stream=sh),
-            gather, attend)
+                                  pipe.chunk_idx, pipe.group_idx, stream=sh)) + tail
     else:
         calls = (
             lambda: hga.hga_build_summaries_qbar(p, pipe.k, 0, 0, w.n_chunks, pipe.chunk_sum,
                                                  pipe.group_sum, pipe.q, 0, pipe.qbar, stream=sh),
             lambda: hga.hga_route_qbar(p, pipe.qbar, 0, pipe.chunk_sum, pipe.group_sum,
-                                       pipe.chunk_idx, pipe.group_idx, stream=sh),
-            gather, attend)
+                                       pipe.chunk_idx, pipe.group_idx, stream=sh)) + tail
 
     for _ in range(args.warmup):
         for f in calls:
@@ -304,7 +334,7 @@ def main():
     torch.cuda.synchronize()
     stage_ms = {name: float(np.mean([ev[s][n].elapsed_time(ev[s][n + 1]) for s in range(KB)]))
                 for n, name in enumerate(stage_names)}
-    stage_ms["attend"] = attend_ms
+    stage_ms[att_name] = attend_ms
     wall_ms = (t1 - t0) * 1e3 / K
     tokens = w.batch * w.seq_len
     gi = pipe.group_idx.cpu().numpy()
@@ -319,7 +349,7 @@ def main():
         ent = {"us": round(stage_ms[sname] * 1e3, 2),
                "alg_bytes": abytes[sname], "GB_s": round(abytes[sname] / sec / 1e9, 1),
                "hbm_frac": round(abytes[sname] / sec / 1e9 / HBM_PEAK_GBS, 4)}
-        if sname == "attend":
+        if sname in ATTENTION_STAGES:
             ent["TFLOP_s"] = round(flops / sec / 1e12, 2)
             ent["mfma_frac"] = round(flops / sec / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
         stages[sname] = ent
@@ -330,7 +360,7 @@ def main():
     # kernel), everything else against HBM.
     cpeak, cbound = ((MFMA_BF16_PEAK_TFLOPS, "mfma") if w.dtype == "bf16"
                      else (VALU_FP32_PEAK_TFLOPS, "alu"))
-    compute_bound = (dominant == "attend" and
+    compute_bound = (dominant in ATTENTION_STAGES and
                      flops / abytes[dominant] > cpeak * 1e12 / (HBM_PEAK_GBS * 1e9))
     if compute_bound:
         achieved = flops / dsec / 1e12
@@ -342,10 +372,11 @@ def main():
         roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
     roofline.update({
-                "traffic": measured_traffic(w.key) if dominant == "attend" else None,
+                "traffic": (measured_traffic(dominant, w.key) if dominant in ATTENTION_STAGES
+                            else None),
                 "alg_bytes_per_launch": abytes[dominant],
                 "mean_launch_us": round(stage_ms[dominant] * 1e3, 2),
-                "timed_launches": len(timed_steps) if dominant == "attend" else KB})
+                "timed_launches": len(timed_steps) if dominant == att_name else KB})
 
     res = {
         "metric": "routed-attn tokens/s per layer",
@@ -368,11 +399,13 @@ def main():
             "seed": inp["seed"],
         },
         "gpu_ms_per_step_events": round(gpu_step_ms, 4),
-        "stage_timing": (f"attend: HIP events recorded by its own dispatch in {len(timed_steps)} "
-                         f"of the {K} timed steps (every {stride}th); other stages: a second "
-                         "pass of the same steps with events between all calls"),
+        "stage_timing": (f"{att_name}: HIP events recorded by its own dispatch in "
+                         f"{len(timed_steps)} of the {K} timed steps (every {stride}th); other "
+                         "stages: a second pass of the same steps with events between all "
+                         "calls"),
         "stages": stages,
         "route_calls": args.route,
+        "gather_calls": args.gather,
         "roofline": roofline,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }

@@ -276,6 +276,27 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
                             const void* v_routed, const int32_t* group_idx, void* out, float* lse,
                             void* start_event, void* stop_event, void* stream);
 
+/* hga_gather_kv followed by hga_attend, for the prefill layout (resident
+ * K/V indexed by token, no res_slot), as one pass: the attention copies each
+ * routed group's rows straight from k_res/v_res (Sec. 4.3 gather, Sec. 3.4
+ * attention), and the same staged rows are written to k_routed/v_routed.
+ * k_routed, v_routed, out and lse receive exactly what
+ *   hga_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_res, v_res,
+ *                 res_tokens, 0, k_routed, v_routed, stream);
+ *   hga_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+ *              NULL, k_routed, v_routed, group_idx, out, lse, stream);
+ * writes, without reading the routed rows back from k_routed/v_routed.
+ * start_event/stop_event (hipEvent_t, either may be NULL) are recorded by
+ * the attention kernel's dispatch as in hga_attend_timed (for the fp32 plan
+ * dtype the gather runs as its own kernel first, outside the events).
+ * Arguments, layouts, requirements and errors are those of the two calls;
+ * k_routed/v_routed must not overlap any input. */
+hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                             int32_t n_q_chunks, const void* k_res, const void* v_res,
+                             int64_t res_tokens, const int32_t* group_idx, void* k_routed,
+                             void* v_routed, void* out, float* lse, void* start_event,
+                             void* stop_event, void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* hga_status_string(int32_t status);
 

@@ -403,12 +403,18 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
 // ring; NW: wavefronts per workgroup (NW / KS query tiles per workgroup).
 // One workgroup per (unit, part); its query rows and group ids are copied
 // with the first tiles, then the key tiles stream through the ring.
-template <int D, int KS, int NS, int NW>
+// kGather: the routed rows are copied straight from the resident K/V (rows
+// g*G .. g*G+G-1 of each routed group g, zeros for a padded or future group,
+// as the gather step defines them), and the workgroup of part 0 of each unit
+// writes every routed tile it staged to k_routed / v_routed, so the call
+// also produces the gather step's output.  Otherwise the routed rows are
+// read from k_routed / v_routed.
+template <int D, int KS, int NS, int NW, bool kGather>
 __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
     const bf16_t* __restrict__ q_rot, int q_chunk0, int n_q_chunks,
     const bf16_t* __restrict__ k_res, const bf16_t* __restrict__ v_res, int64_t res_tokens,
-    const int32_t* __restrict__ res_slot, const bf16_t* __restrict__ k_routed,
-    const bf16_t* __restrict__ v_routed, const int32_t* __restrict__ group_idx,
+    const int32_t* __restrict__ res_slot, bf16_t* __restrict__ k_routed,
+    bf16_t* __restrict__ v_routed, const int32_t* __restrict__ group_idx,
     bf16_t* __restrict__ out, float* __restrict__ lse, int r, FastDiv kv_div, int group_shift,
     int keep_first, int window, int topk_groups, FastDiv wg_div, FastDiv chunk_div,
     int n_blocks) {
@@ -525,9 +531,32 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
         } else {
             base = static_cast<uint32_t>((tile - 1 - n_vis) * kTileBytes);
         }
+        const uint32_t sk = lds0 + stage * kStageBytes;
+        if (kGather && routed) {
+            // each copied row's source: row g*G + o of the resident slab,
+            // for routed row R = slot*G + o of the unit (g = its group id)
+            const int rt0 = (tile - 1 - n_vis) * KT;
+            auto src = [&](uint32_t off) {
+                const int row = static_cast<int>(off / kRowBytes);
+                const int R = rt0 + row;
+                const int slot = min(R >> group_shift, topk_groups - 1);
+                const int g = s_gid[slot];
+                const bool ok = R < routed_rows && g >= 0 && g < c * gpc;
+                return ok ? static_cast<uint32_t>(((g << group_shift) + (R & (group - 1))) *
+                                                  kRowBytes) +
+                                off - row * kRowBytes
+                          : kAbsent;
+            };
+#pragma unroll
+            for (int u = 0; u < KI; ++u)
+                copy16_to_lds(rk_res, src(koff[u]), sk + (u * NW + wave) * 1024);
+#pragma unroll
+            for (int u = 0; u < KI; ++u)
+                copy16_to_lds(rv_res, src(voff[u]), sk + kTileBytes + (u * NW + wave) * 1024);
+            return;
+        }
         const u32x4 rk = routed ? rk_rt : rk_res;
         const u32x4 rv = routed ? rv_rt : rv_res;
-        const uint32_t sk = lds0 + stage * kStageBytes;
 #pragma unroll
         for (int u = 0; u < KI; ++u)
             copy16_to_lds(rk, base + koff[u], sk + (u * NW + wave) * 1024);
@@ -535,9 +564,35 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
         for (int u = 0; u < KI; ++u)
             copy16_to_lds(rv, base + voff[u], sk + kTileBytes + (u * NW + wave) * 1024);
     };
+    // kGather: write the routed tile in `stage` (this lane's own copies, so
+    // its own wait suffices) to the routed buffers at the offsets it was
+    // copied from, rows past the unit's routed rows left out.
+    auto write_routed = [&](int tile, int stage) {
+        const int rt0 = (tile - 1 - n_vis) * KT;
+        bf16_t* kdst = k_routed + (unit * routed_rows + rt0) * D;
+        bf16_t* vdst = v_routed + (unit * routed_rows + rt0) * D;
+        const unsigned char* sk = smem + stage * kStageBytes;
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const vec16 x = *reinterpret_cast<const vec16*>(sk + (u * NW + wave) * 1024 + lane * 16);
+            if (rt0 + static_cast<int>(koff[u] / kRowBytes) < routed_rows)
+                store16(reinterpret_cast<unsigned char*>(kdst) + koff[u], x);
+        }
+#pragma unroll
+        for (int u = 0; u < KI; ++u) {
+            const vec16 x = *reinterpret_cast<const vec16*>(sk + kTileBytes + (u * NW + wave) * 1024 +
+                                                            lane * 16);
+            if (rt0 + static_cast<int>(voff[u] / kRowBytes) < routed_rows)
+                store16(reinterpret_cast<unsigned char*>(vdst) + voff[u], x);
+        }
+    };
+    // Tiles requested up front; with kGather a routed tile needs the group
+    // ids in LDS, so one among them waits for the first barrier.
+    const int n_up = min(NS, n_tiles);
+    const int n_pre = kGather ? min(n_up, n_vis + 1) : n_up;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-        if (s < n_tiles) issue(s, s);
+        if (s < n_pre) issue(s, s);
 
     f32x16_t oacc[NDT];
 #pragma unroll
@@ -555,7 +610,7 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
         constexpr bool kCurrent = decltype(current_tag)::value;
         // this wave's copies of `tile` are done once at most `ahead` later
         // tiles' copies remain in flight (loads complete in issue order)
-        const int ahead = min(kCurrent ? NS - 1 : NS - 2, n_tiles - 1 - tile);
+        const int ahead = kCurrent ? n_pre - 1 : min(NS - 2, n_tiles - 1 - tile);
         if (NS >= 4 && ahead >= 3)
             wait_loads<(NS >= 4 ? 3 : 0) * LPT>();
         else if (NS >= 3 && ahead >= 2)
@@ -565,7 +620,12 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
         else
             wait_loads<0>();
         __syncthreads();
-        if (!kCurrent && tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
+        if (kCurrent) {
+            for (int s = n_pre; s < n_up; ++s) issue(s, s);
+        } else {
+            if (kGather && tile > n_vis && part == 0) write_routed(tile, tile % NS);
+            if (tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
+        }
 
         const int stage = tile % NS;
         const bf16_t* sK = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes);
@@ -587,11 +647,11 @@ __global__ __launch_bounds__(NW * 64, 2) void attend_mfma_kernel(
                            qactive, bad, out + qrow * D, lse ? lse + qrow : nullptr);
 }
 
-template <int D, int KS, int NS, int NW>
+template <int D, int KS, int NS, int NW, bool kGather>
 hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev_start,
                          hipEvent_t ev_stop, const bf16_t* q_rot, int q_chunk0, int n_q_chunks,
                          const bf16_t* k_res, const bf16_t* v_res, int64_t res_tokens,
-                         const int32_t* res_slot, const bf16_t* k_routed, const bf16_t* v_routed,
+                         const int32_t* res_slot, bf16_t* k_routed, bf16_t* v_routed,
                          const int32_t* group_idx, bf16_t* out, float* lse, int group_shift,
                          int wg_per_unit, int n_items) {
     const hga_params& p = plan.p;
@@ -599,29 +659,27 @@ hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev
     static bool configured = false;  // per instantiation (the limit is a function attribute)
     if (!configured) {
         const hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attend_mfma_kernel<D, KS, NS, NW>),
+            reinterpret_cast<const void*>(&attend_mfma_kernel<D, KS, NS, NW, kGather>),
             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
         if (e != hipSuccess) return e;
         configured = true;
     }
     const int grid = (n_items + kXcds - 1) / kXcds * kXcds;
-    hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW>), dim3(grid), dim3(NW * 64), kLds,
-                          stream, ev_start, ev_stop, 0, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
-                          res_tokens, res_slot, k_routed, v_routed, group_idx, out, lse,
+    hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW, kGather>), dim3(grid), dim3(NW * 64),
+                          kLds, stream, ev_start, ev_stop, 0, q_rot, q_chunk0, n_q_chunks, k_res,
+                          v_res, res_tokens, res_slot, k_routed, v_routed, group_idx, out, lse,
                           p.n_q_heads / p.n_kv_heads, FastDiv(p.n_kv_heads), group_shift,
                           p.keep_first, recent_window(p), p.topk_groups, FastDiv(wg_per_unit),
                           FastDiv(n_q_chunks), n_items);
     return hipGetLastError();
 }
 
-}  // namespace
-
-hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chunk0,
-                              int n_q_chunks, const void* k_res, const void* v_res,
-                              int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
-                              const void* v_routed, const int32_t* group_idx, void* out,
-                              float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
-                              hipStream_t stream) {
+template <bool kGather>
+hipError_t launch_mfma_any(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
+                           const void* k_res, const void* v_res, int64_t res_tokens,
+                           const int32_t* res_slot, void* k_routed, void* v_routed,
+                           const int32_t* group_idx, void* out, float* lse, hipEvent_t ev_start,
+                           hipEvent_t ev_stop, hipStream_t stream) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int nqt = 2 * r;
@@ -637,20 +695,22 @@ hipError_t launch_attend_mfma(const hga_plan& plan, const void* q_rot, int q_chu
     const bf16_t* q = static_cast<const bf16_t*>(q_rot);
     const bf16_t* kr = static_cast<const bf16_t*>(k_res);
     const bf16_t* vr = static_cast<const bf16_t*>(v_res);
-    const bf16_t* kt = static_cast<const bf16_t*>(k_routed);
-    const bf16_t* vt = static_cast<const bf16_t*>(v_routed);
+    bf16_t* kt = static_cast<bf16_t*>(k_routed);
+    bf16_t* vt = static_cast<bf16_t*>(v_routed);
     bf16_t* o = static_cast<bf16_t*>(out);
 #define HGA_ARGS                                                                                 \
-    plan, stream, ev_start, ev_stop, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot, kt, vt, group_idx, o,   \
-        lse, group_shift, wg_per_unit, n_items
+    plan, stream, ev_start, ev_stop, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot, kt, \
+        vt, group_idx, o, lse, group_shift, wg_per_unit, n_items
     if (p.head_dim == 64) {
-        if (one_head) return launch_mfma_t<64, 2, 2, 4>(HGA_ARGS);
-        return launch_mfma_t<64, 1, 2, 4>(HGA_ARGS);
+        if (one_head) return launch_mfma_t<64, 2, 2, 4, kGather>(HGA_ARGS);
+        return launch_mfma_t<64, 1, 2, 4, kGather>(HGA_ARGS);
     }
-    if (one_head) return launch_mfma_t<128, 2, 2, 4>(HGA_ARGS);
-    return launch_mfma_t<128, 1, 2, 4>(HGA_ARGS);
+    if (one_head) return launch_mfma_t<128, 2, 2, 4, kGather>(HGA_ARGS);
+    return launch_mfma_t<128, 1, 2, 4, kGather>(HGA_ARGS);
 #undef HGA_ARGS
 }
+
+}  // namespace
 
 hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,
                               int n_q_chunks, const void* k_res, const void* v_res,
@@ -668,9 +728,30 @@ hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, 
         return launch_attend_valu(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
                                   res_slot, k_routed, v_routed, group_idx, out, lse, ev_start,
                                   ev_stop, stream);
-    return launch_attend_mfma(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
-                              res_slot, k_routed, v_routed, group_idx, out, lse, ev_start, ev_stop,
-                              stream);
+    // the routed buffers are only read on this path
+    return launch_mfma_any<false>(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                  res_slot, const_cast<void*>(k_routed),
+                                  const_cast<void*>(v_routed), group_idx, out, lse, ev_start,
+                                  ev_stop, stream);
+}
+
+hipError_t launch_gather_attend(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                                int n_q_chunks, const void* k_res, const void* v_res,
+                                int64_t res_tokens, const int32_t* group_idx, void* k_routed,
+                                void* v_routed, void* out, float* lse, hipEvent_t ev_start,
+                                hipEvent_t ev_stop, hipStream_t stream) {
+    if (plan.p.dtype == HGA_F32) {
+        // fp32: the gather kernel, then the attention kernel reading its output
+        hipError_t e = launch_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_res, v_res,
+                                        res_tokens, k_routed, v_routed, stream);
+        if (e != hipSuccess) return e;
+        return launch_attend_valu(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                  nullptr, k_routed, v_routed, group_idx, out, lse, ev_start,
+                                  ev_stop, stream);
+    }
+    return launch_mfma_any<true>(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                 nullptr, k_routed, v_routed, group_idx, out, lse, ev_start,
+                                 ev_stop, stream);
 }
 
 }  // namespace hga

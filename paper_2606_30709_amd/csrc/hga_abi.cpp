@@ -440,16 +440,16 @@ hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t
                     "hga_gather_kv launch");
 }
 
-hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
-                            int32_t n_q_chunks, const void* k_res, const void* v_res,
-                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
-                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
-                            void* start_event, void* stop_event, void* stream) {
-    HGA_TRY(check_plan(plan));
+namespace {
+
+// Checks shared by the attention calls (the plan is already checked and
+// n_q_chunks > 0).
+hga_status check_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                        int32_t n_q_chunks, const void* k_res, const void* v_res,
+                        int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                        const void* v_routed, const int32_t* group_idx, const void* out,
+                        const float* lse) {
     const hga_params& p = plan->p;
-    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
-        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
-    if (n_q_chunks == 0) return HGA_OK;
     if (!res_slot && (static_cast<int64_t>(q_chunk0) + n_q_chunks) * p.chunk > res_tokens)
         return fail(HGA_EINVAL, "without res_slot the resident K/V must cover chunks up to %d "
                     "(%lld tokens), have %lld", q_chunk0 + n_q_chunks - 1,
@@ -477,6 +477,22 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
     HGA_TRY(check_index(group_idx, "group_idx"));
     HGA_TRY(check_tensor(out, "out"));
     if (lse && !aligned(lse, 4)) return fail(HGA_EALIGN, "lse is not 4-byte aligned");
+    return HGA_OK;
+}
+
+}  // namespace
+
+hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const void* k_res, const void* v_res,
+                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                            void* start_event, void* stop_event, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                         k_routed, v_routed, group_idx, out, lse));
     clear_stale_error();
     return launched(hga::launch_attend(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
                                        res_tokens, res_slot, k_routed, v_routed, group_idx, out,
@@ -484,6 +500,26 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
                                        static_cast<hipEvent_t>(stop_event),
                                        static_cast<hipStream_t>(stream)),
                     "hga_attend launch");
+}
+
+hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                             int32_t n_q_chunks, const void* k_res, const void* v_res,
+                             int64_t res_tokens, const int32_t* group_idx, void* k_routed,
+                             void* v_routed, void* out, float* lse, void* start_event,
+                             void* stop_event, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, nullptr,
+                         k_routed, v_routed, group_idx, out, lse));
+    clear_stale_error();
+    return launched(hga::launch_gather_attend(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+                                              res_tokens, group_idx, k_routed, v_routed, out, lse,
+                                              static_cast<hipEvent_t>(start_event),
+                                              static_cast<hipEvent_t>(stop_event),
+                                              static_cast<hipStream_t>(stream)),
+                    "hga_gather_attend launch");
 }
 
 hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,

@@ -78,4 +78,13 @@ hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, 
                          const int32_t* group_idx, void* out, float* lse, hipEvent_t start,
                          hipEvent_t stop, hipStream_t stream);
 
+// The gather of the routed rows fused into the attention (prefill layout:
+// resident K/V indexed by token, no slot map); writes k_routed / v_routed as
+// launch_gather_kv does.  start/stop as for launch_attend.
+hipError_t launch_gather_attend(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                                int n_q_chunks, const void* k_res, const void* v_res,
+                                int64_t res_tokens, const int32_t* group_idx, void* k_routed,
+                                void* v_routed, void* out, float* lse, hipEvent_t start,
+                                hipEvent_t stop, hipStream_t stream);
+
 }  // namespace hga

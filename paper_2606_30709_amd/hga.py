@@ -18,8 +18,8 @@ __all__ = [
     "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
-    "hga_attend_timed", "hga_status_string", "hga_last_error", "hga_version",
-    "EXPORTED_SYMBOLS",
+    "hga_attend_timed", "hga_gather_attend", "hga_status_string", "hga_last_error",
+    "hga_version", "EXPORTED_SYMBOLS",
 ]
 
 F32, BF16 = 0, 1
@@ -28,7 +28,8 @@ _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
-    "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_status_string", "hga_last_error", "hga_version",
+    "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_gather_attend",
+    "hga_status_string", "hga_last_error", "hga_version",
 )
 
 
@@ -81,6 +82,7 @@ def library() -> ctypes.CDLL:
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
+            "hga_gather_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
@@ -267,3 +269,17 @@ def hga_attend_timed(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v
         plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
         _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
         start_event.cuda_event, stop_event.cuda_event, _stream(stream)))
+
+
+def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx, k_routed,
+                      v_routed, out, lse=None, start_event=None, stop_event=None, stream=None):
+    """hga_gather_kv + hga_attend in one pass (prefill layout: k_res/v_res
+    [B, Hkv, res_tokens, d] indexed by token); k_routed/v_routed
+    [B, Hkv, n_q_chunks, K_g*G, d] are written.  start/stop_event: recorded
+    torch.cuda.Event objects or None."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_gather_attend(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse),
+        start_event.cuda_event if start_event is not None else None,
+        stop_event.cuda_event if stop_event is not None else None, _stream(stream)))

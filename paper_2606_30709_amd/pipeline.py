@@ -14,8 +14,13 @@ Prefill routing has three equivalent forms (bit-identical summaries, query
 means and indices), chosen by ``route_mode``: "fused" (``hga_build_summaries``
 then ``hga_route``), "separate" (``hga_route_chunks`` then
 ``hga_route_groups``), and "qbar" (``hga_build_summaries_qbar``, which also
-reduces the query means in the same launch, then ``hga_route_qbar``).  Both pipelines only allocate with torch and
-call the binding; all arithmetic runs in the HIP library.
+reduces the query means in the same launch, then ``hga_route_qbar``).  The
+gather and the attention are either one call, ``hga_gather_attend``
+(``gather_mode="fused"``, the default: the attention stages the routed rows
+from the resident K/V and writes the routed buffers), or the two calls
+``hga_gather_kv`` and ``hga_attend`` (``gather_mode="separate"``); the
+results are identical.  Both pipelines only allocate with torch and call the
+binding; all arithmetic runs in the HIP library.
 """
 
 from __future__ import annotations
@@ -40,11 +45,13 @@ def to_device(arr: np.ndarray, dtype: str, device="cuda", pin=False) -> torch.Te
 
 class PrefillPipeline:
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 route_mode: str = "qbar"):
+                 route_mode: str = "qbar", gather_mode: str = "fused"):
         assert not w.decode_block
         assert route_mode in ("fused", "separate", "qbar")
+        assert gather_mode in ("fused", "separate")
         self.w = w
         self.route_mode = route_mode
+        self.gather_mode = gather_mode
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
         nc = w.n_chunks
@@ -94,11 +101,19 @@ class PrefillPipeline:
         hga.hga_attend(self.plan, self.q, 0, self.k, self.v, self.k_routed, self.v_routed,
                        self.group_idx, self.out, self.lse, stream=stream)
 
+    def gather_attend(self, stream=None, start_event=None, stop_event=None):
+        hga.hga_gather_attend(self.plan, self.q, 0, self.k, self.v, self.group_idx,
+                              self.k_routed, self.v_routed, self.out, self.lse,
+                              start_event=start_event, stop_event=stop_event, stream=stream)
+
     def step(self, stream=None):
         self.summaries(stream)
         self.route(stream)
-        self.gather(stream)
-        self.attend(stream)
+        if self.gather_mode == "fused":
+            self.gather_attend(stream)
+        else:
+            self.gather(stream)
+            self.attend(stream)
 
 
 class DecodePipeline:

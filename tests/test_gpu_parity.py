@@ -266,6 +266,77 @@ def test_fused_route_equals_separate_calls(hga, key):
     assert torch.equal(ga, ga_all[:, :, c0:c0 + n])
 
 
+# ------------------------------------------------- fused gather + attention ---
+
+def _bits(t):
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+def _gather_attend_both_ways(hga, plan, w, q, q_chunk0, k, v, gi):
+    """hga_gather_kv + hga_attend and hga_gather_attend on the same inputs,
+    every output pre-filled with NaN so that an unwritten element shows."""
+    B, Hkv, d, G = w.batch, w.n_kv_heads, w.head_dim, w.group
+    nq = gi.shape[2]
+    outs = []
+    for fused in (False, True):
+        kr = torch.full((B, Hkv, nq, w.topk_groups * G, d), float("nan"), dtype=k.dtype,
+                        device="cuda")
+        vr = torch.full_like(kr, float("nan"))
+        out = torch.full_like(q, float("nan"))
+        lse = torch.full(q.shape[:3], float("nan"), device="cuda")
+        if fused:
+            hga.hga_gather_attend(plan, q, q_chunk0, k, v, gi, kr, vr, out, lse)
+        else:
+            hga.hga_gather_kv(plan, gi, q_chunk0, k, v, kr, vr)
+            hga.hga_attend(plan, q, q_chunk0, k, v, kr, vr, gi, out, lse)
+        outs.append((kr, vr, out, lse))
+    torch.cuda.synchronize()
+    for a, b, name in zip(outs[0], outs[1], ("k_routed", "v_routed", "out", "lse")):
+        assert torch.equal(_bits(a), _bits(b)), name
+    assert not torch.isnan(outs[1][2]).any()
+
+
+@pytest.mark.parametrize("key", list(FUSED_CASES))
+def test_gather_attend_equals_separate_calls(hga, key):
+    """hga_gather_attend writes exactly what hga_gather_kv + hga_attend write:
+    the routed buffers, the output and the LSE, bit for bit; for the whole
+    sequence, with padded and out-of-range group ids planted, and for a query
+    block starting mid-sequence."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = FUSED_CASES[key]
+    _say(f"[gather-attend] {key}")
+    pipe = PrefillPipeline(w, W.generate(w), gather_mode="separate")
+    pipe.summaries()
+    pipe.route()
+    _gather_attend_both_ways(hga, pipe.plan, w, pipe.q, 0, pipe.k, pipe.v, pipe.group_idx)
+    gi = pipe.group_idx.clone()
+    c = w.n_chunks - 1
+    gi[0, 0, c, 0] = -1
+    gi[0, w.n_kv_heads - 1, c, w.topk_groups - 1] = 10 ** 6  # beyond the causal past
+    gi[-1, 0, c // 2, w.topk_groups // 2] = -1
+    _gather_attend_both_ways(hga, pipe.plan, w, pipe.q, 0, pipe.k, pipe.v, gi)
+    c0 = w.n_chunks // 3
+    n = min(5, w.n_chunks - c0)
+    C = w.chunk
+    q_blk = pipe.q[:, :, c0 * C:(c0 + n) * C].contiguous()
+    gi_blk = pipe.group_idx[:, :, c0:c0 + n].contiguous()
+    _gather_attend_both_ways(hga, pipe.plan, w, q_blk, c0, pipe.k, pipe.v, gi_blk)
+
+
+def test_gather_attend_full_size(hga):
+    """The fused call equals the two calls at the full prefill sizes."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    for key in ("smalllm", "train12k", "qwen32k"):
+        w = W.preset(key)
+        _say(f"[gather-attend] {key} full size")
+        pipe = PrefillPipeline(w, W.generate(w), gather_mode="separate")
+        pipe.summaries()
+        pipe.route()
+        _gather_attend_both_ways(hga, pipe.plan, w, pipe.q, 0, pipe.k, pipe.v, pipe.group_idx)
+        del pipe
+        torch.cuda.empty_cache()
+
+
 def _split_route_check(hga, plan, k, k_chunk0, n_chunks, table_chunks, q, q_chunk0, w):
     """hga_build_summaries_qbar + hga_route_qbar against hga_build_summaries +
     hga_route, bit for bit."""
