@@ -138,11 +138,18 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
 }
 
 // Wave-wide maximum of a 64-bit key: the high words first, then the low
-// words of the lanes holding that high word.
+// words of the lanes holding that high word -- read straight from that lane
+// when only one holds it, the usual case.
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
     const uint32_t hi = static_cast<uint32_t>(x >> 32);
     const uint32_t top_hi = wave_max_u32(hi);
-    const uint32_t top_lo = wave_max_u32(hi == top_hi ? static_cast<uint32_t>(x) : 0u);
+    const uint64_t holders = __builtin_amdgcn_ballot_w64(hi == top_hi);
+    uint32_t top_lo;
+    if ((holders & (holders - 1)) == 0)
+        top_lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(
+            static_cast<int>(static_cast<uint32_t>(x)), static_cast<int>(__builtin_ctzll(holders))));
+    else
+        top_lo = wave_max_u32(hi == top_hi ? static_cast<uint32_t>(x) : 0u);
     return (static_cast<uint64_t>(top_hi) << 32) | top_lo;
 }
 
@@ -210,7 +217,11 @@ __device__ inline void wave_select_topk_regs(const uint64_t* keys, int n, int k,
 
 // Dispatch on size; every form selects the same keys.
 __device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, int* scratch) {
-    if (k <= 64 && n <= 64 * 4)
+    if (k <= 64 && n <= 64)
+        wave_select_topk_regs<1>(keys, n, k, sel);
+    else if (k <= 64 && n <= 64 * 2)
+        wave_select_topk_regs<2>(keys, n, k, sel);
+    else if (k <= 64 && n <= 64 * 4)
         wave_select_topk_regs<4>(keys, n, k, sel);
     else if (k <= 64 && n <= 64 * 8)
         wave_select_topk_regs<8>(keys, n, k, sel);

@@ -15,6 +15,12 @@
 namespace hga {
 namespace {
 
+// Chunk-summary rows staged per LDS block: for D = 64 one block covers the
+// middle chunks of every query chunk up to 128 chunks in, so short contexts
+// need a single round trip for the table; D = 128 rows stay at 64 per block
+// (measured faster: half the registers and LDS per block).
+constexpr int table_rows(int d) { return d == 64 ? 128 : 64; }
+
 __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -123,11 +129,12 @@ __device__ inline WaveLds carve(unsigned char* base, int d, int n_list, int topk
 // Query-chunk routing for up to four consecutive query chunks of one
 // (batch, KV head), in a workgroup of four wavefronts.  Wavefront w < units
 // owns query chunk w of the group and computes its q_bar; all four stage the
-// chunk-summary table in LDS, 64 rows at a time (the next block's rows are
-// loaded into registers while the current block is scored, and the first
-// block's while q_bar is formed), and each owning wavefront scores its own
-// middle chunks (one table row per lane; four partial dot products over the
-// dimensions d = 0, 1, 2, 3 mod 4, each in order, added pairwise) and selects
+// chunk-summary table in LDS, table_rows(D) rows at a time (the next block's
+// rows are loaded into registers while the current block is scored, and the
+// first block's while q_bar is formed), and each owning wavefront scores its
+// own middle chunks (one table row per lane and 64 rows; four partial dot
+// products over the dimensions d = 0, 1, 2, 3 mod 4, each in order, added
+// pairwise) and selects
 // its top K_c.  With kGroups, the same wavefront goes on
 // to group refinement of its chosen chunks (the work of route_groups_kernel,
 // without a second launch or the q_bar/chunk_idx round trip through memory).
@@ -139,7 +146,7 @@ __global__ __launch_bounds__(256) void route_kernel(
     int keep_first, int window, int topk, int topk_groups, int gpc_shift, int units_per_block,
     size_t wave_bytes) {
     constexpr int kThreads = 256;
-    constexpr int TB = 64;                  // table rows per LDS block
+    constexpr int TB = table_rows(D);       // table rows per LDS block
     constexpr int TS = D + 4;               // padded LDS row stride (floats)
     constexpr int F4 = D / 4;               // float4 per table row
     constexpr int PF = TB * F4 / kThreads;  // float4 per thread per table block
@@ -207,20 +214,23 @@ __global__ __launch_bounds__(256) void route_kernel(
         }
         __syncthreads();
         if (r0 + TB < hi) fetch_block(r0 + TB);
-        const int m = r0 - keep_first + lane;            // candidate ordinal of this lane
-        if (m < n) {
-            const float* row = s_tab + lane * TS;
-            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
-            for (int f = 0; f < F4; ++f) {
-                const float4 q = *reinterpret_cast<const float4*>(L.q + f * 4);
-                const float4 x = *reinterpret_cast<const float4*>(row + f * 4);
-                a0 = fmaf(q.x, x.x, a0);
-                a1 = fmaf(q.y, x.y, a1);
-                a2 = fmaf(q.z, x.z, a2);
-                a3 = fmaf(q.w, x.w, a3);
+        for (int h = 0; h < TB / 64; ++h) {
+            const int m = r0 - keep_first + h * 64 + lane;  // candidate ordinal of this lane
+            if (m < n) {
+                const float* row = s_tab + (h * 64 + lane) * TS;
+                float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+                for (int f = 0; f < F4; ++f) {
+                    const float4 q = *reinterpret_cast<const float4*>(L.q + f * 4);
+                    const float4 x = *reinterpret_cast<const float4*>(row + f * 4);
+                    a0 = fmaf(q.x, x.x, a0);
+                    a1 = fmaf(q.y, x.y, a1);
+                    a2 = fmaf(q.z, x.z, a2);
+                    a3 = fmaf(q.w, x.w, a3);
+                }
+                L.keys[m] = select_key((a0 + a1) + (a2 + a3), keep_first + m);
             }
-            L.keys[m] = select_key((a0 + a1) + (a2 + a3), keep_first + m);
         }
     }
     if (!active) return;
@@ -317,7 +327,7 @@ inline RouteGeom route_geom(const hga_plan& plan, int n_max, bool groups) {
     const int ntop = groups && p.topk_groups > p.topk_chunks ? p.topk_groups : p.topk_chunks;
     RouteGeom g;
     g.wave_bytes = wave_lds_bytes(p.head_dim, groups ? p.topk_chunks : 0, ntop, nk);
-    const size_t tab = align16(sizeof(float) * 64 * (p.head_dim + 4));
+    const size_t tab = align16(sizeof(float) * table_rows(p.head_dim) * (p.head_dim + 4));
     g.units_per_block = 4;
     while (g.units_per_block > 1 &&
            tab + g.units_per_block * g.wave_bytes > static_cast<size_t>(plan.max_lds))
@@ -394,7 +404,7 @@ size_t route_lds_bytes(const hga_plan& plan, int n_max, bool groups) {
     const int gpc = p.chunk / p.group;
     const int nk = groups && p.topk_chunks * gpc > n_max ? p.topk_chunks * gpc : n_max;
     const int ntop = groups && p.topk_groups > p.topk_chunks ? p.topk_groups : p.topk_chunks;
-    return align16(sizeof(float) * 64 * (p.head_dim + 4)) +
+    return align16(sizeof(float) * table_rows(p.head_dim) * (p.head_dim + 4)) +
            wave_lds_bytes(p.head_dim, groups ? p.topk_chunks : 0, ntop, nk);
 }
 

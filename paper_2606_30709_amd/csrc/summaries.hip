@@ -38,6 +38,7 @@ struct SumGeom {
     static constexpr int NPB = HALF / V;            // pair-blocks per token
     static constexpr int TPL = NPB;                 // tokens per lane (64 lanes per chunk)
     static constexpr int SLICES = 64 / NPB;         // token slices per chunk
+    static constexpr int RD = D + 1;                // reduction row stride (floats)
 };
 
 // The summary work of workgroup `block` of `n_blocks` (a grid-stride loop
@@ -52,10 +53,11 @@ __device__ __forceinline__ void summaries_body(
     constexpr int V = Gm::V, LV = Gm::LV, VPH = Gm::VPH, HALF = Gm::HALF, NPB = Gm::NPB,
                   TPL = Gm::TPL, SLICES = Gm::SLICES;
     constexpr int C = 64;
-    // LDS rows padded by 4 words so lanes reading or writing the same column
-    // of different rows hit different banks.
+    // LDS rows padded so lanes reading or writing the same column of
+    // different rows hit different banks (the reduction rows by one word:
+    // they are only accessed a word at a time).
     constexpr int PH = HALF + 4;                   // phase-table row stride
-    constexpr int RD = D + 4;                      // reduction row stride
+    constexpr int RD = Gm::RD;                     // reduction row stride
     extern __shared__ __align__(16) float smem[];
     const int gpc = C / group;
     float* s_pg = smem;                            // [2][group][PH]
@@ -63,8 +65,34 @@ __device__ __forceinline__ void summaries_body(
     float* s_red = s_psi + 2 * gpc * PH;           // [kWaves][2][SLICES][RD]
 
     const int tid = threadIdx.x;
-    for (int x = tid; x < 2 * group * HALF; x += kThreads) s_pg[(x / HALF) * PH + x % HALF] = phase_group[x];
-    for (int x = tid; x < 2 * gpc * HALF; x += kThreads) s_psi[(x / HALF) * PH + x % HALF] = phase_psi[x];
+    {
+        // the phase tables: 16-byte pieces, every load issued before any store
+        constexpr int H4 = HALF / 4;
+        constexpr int MAXG = (2 * 32 * H4 + kThreads - 1) / kThreads;  // group <= 32
+        constexpr int MAXP = (2 * 8 * H4 + kThreads - 1) / kThreads;   // gpc <= 8
+        const int ng4 = 2 * group * H4, np4 = 2 * gpc * H4;
+        float4 tg[MAXG], tp[MAXP];
+#pragma unroll
+        for (int u = 0; u < MAXG; ++u) {
+            const int x = tid + u * kThreads;
+            tg[u] = reinterpret_cast<const float4*>(phase_group)[min(x, ng4 - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < MAXP; ++u) {
+            const int x = tid + u * kThreads;
+            tp[u] = reinterpret_cast<const float4*>(phase_psi)[min(x, np4 - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < MAXG; ++u) {
+            const int x = tid + u * kThreads;
+            if (x < ng4) *reinterpret_cast<float4*>(s_pg + (x / H4) * PH + (x % H4) * 4) = tg[u];
+        }
+#pragma unroll
+        for (int u = 0; u < MAXP; ++u) {
+            const int x = tid + u * kThreads;
+            if (x < np4) *reinterpret_cast<float4*>(s_psi + (x / H4) * PH + (x % H4) * 4) = tp[u];
+        }
+    }
     __syncthreads();
 
     const int wave = tid >> 6, lane = tid & 63;
@@ -202,7 +230,7 @@ hipError_t launch_t(const hga_plan& plan, const void* k_rot, int64_t k_tokens, i
     int64_t blocks = (items + kWaves - 1) / kWaves;
     if (blocks > 4096) blocks = 4096;
     const size_t lds = sizeof(float) * (2 * p.group * (Gm::HALF + 4) + 2 * gpc * (Gm::HALF + 4) +
-                                        kWaves * 2 * Gm::SLICES * (D + 4));
+                                        kWaves * 2 * Gm::SLICES * Gm::RD);
     hipLaunchKernelGGL((build_summaries_kernel<T, D>), dim3(static_cast<unsigned>(blocks)),
                        dim3(kThreads), lds, stream, static_cast<const T*>(k_rot), k_tokens,
                        k_chunk0, chunk_begin, n_chunks, chunk_sum, group_sum, table_chunks, n_bh,
@@ -226,7 +254,7 @@ hipError_t launch_sq_t(const hga_plan& plan, const void* k_rot, int64_t k_tokens
     const int64_t q_blocks = (static_cast<int64_t>(n_bh) * n_q_chunks + kWaves - 1) / kWaves;
     if (sum_blocks + q_blocks > (int64_t(1) << 30)) return hipErrorInvalidConfiguration;
     const size_t lds = sizeof(float) * (2 * p.group * (Gm::HALF + 4) + 2 * gpc * (Gm::HALF + 4) +
-                                        kWaves * 2 * Gm::SLICES * (D + 4));
+                                        kWaves * 2 * Gm::SLICES * Gm::RD);
     hipLaunchKernelGGL((summaries_qbar_kernel<T, D>),
                        dim3(static_cast<unsigned>(sum_blocks + q_blocks)), dim3(kThreads), lds,
                        stream, static_cast<const T*>(k_rot), k_tokens, k_chunk0, chunk_begin,
