@@ -79,9 +79,10 @@ def algorithmic_bytes(w, n_valid_rows: int) -> dict:
         "route_qbar": 2 * table_c + table_g + B * Hkv * nc * (w.topk_chunks + w.topk_groups) * 4,
         "gather_kv": 4 * routed + B * Hkv * nc * w.topk_groups * 4,
         "attend": q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4,
-        # the routed rows read from the resident K/V and written once to the
-        # routed buffers, never read back
-        "gather_attend": (q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4 +
+        # the routed rows are rows of the resident K/V, which is read once
+        # as a whole (every chunk is some unit's current chunk); they are
+        # written once to the routed buffers and never read back
+        "gather_attend": (q_tok + 2 * kv_tok + q_tok + B * Hq * N * 4 +
                           2 * routed + B * Hkv * nc * w.topk_groups * 4),
     }
 
