@@ -201,6 +201,94 @@ def cpu_baseline(w, inp, max_seconds: float) -> dict:
             "cpu": platform.processor() or platform.machine(), "host_cpus": os.cpu_count()}
 
 
+def measured_copy_bandwidth(nbytes: int = 1 << 30, reps: int = 10) -> float:
+    """Achievable HBM bandwidth on this device: GB/s of a streaming copy of
+    nbytes (each byte read once and written once), well beyond the 256 MB
+    Infinity Cache.  torch's vectorized elementwise kernel (x * 1 over fp32)
+    is used: it streams faster here than the runtime's blit copy."""
+    import torch
+    src = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)
+    e1.record()
+    torch.cuda.synchronize()
+    sec = e0.elapsed_time(e1) * 1e-3 / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes / sec / 1e9
+
+
+def dense_comparator(w, pipe, reps: int = 20):
+    """Dense causal attention over the same Q/K/V with PyTorch's fused SDPA
+    (a comparator only: flash or memory-efficient kernels, never the
+    unfused math path), or None where no fused kernel is available."""
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    q, k, v = pipe.q, pipe.k, pipe.v
+    if w.n_q_heads != w.n_kv_heads:
+        r = w.gqa_ratio
+        k = k.repeat_interleave(r, dim=1)
+        v = v.repeat_interleave(r, dim=1)
+    try:
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+            out = F.scaled_dot_product_attention(q, k, v, is_causal=True)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                out = F.scaled_dot_product_attention(q, k, v, is_causal=True)
+            e1.record()
+            torch.cuda.synchronize()
+    except RuntimeError as e:
+        return {"available": False, "reason": str(e).splitlines()[0][:200]}
+    ms = e0.elapsed_time(e1) / reps
+    del out
+    return {"available": True, "kernel": "torch SDPA (flash / memory-efficient), causal",
+            "ms": round(ms, 4), "tokens_per_s": round(w.batch * w.seq_len / (ms * 1e-3), 1)}
+
+
+def decode_bench(w, inp, args):
+    """The 64-token decode block: route, gather of the routed groups from the
+    pinned host history, attention, append; one block per step."""
+    import torch
+
+    from paper_2606_30709_amd.pipeline import DecodePipeline
+    pipe = DecodePipeline(w, inp)
+    for _ in range(args.warmup):
+        pipe.step()
+    torch.cuda.synchronize()
+    K = args.steps
+    t0 = time.perf_counter()
+    for _ in range(K):
+        pipe.step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / K
+    pcie = pipe.pcie_bytes_per_step()
+    res = {
+        "metric": "routed-attn decode tokens/s (64-token block)",
+        "value": round(w.chunk * w.batch / dt, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": (f"{w.key}: decode block B{w.batch} H{w.n_q_heads}/{w.n_kv_heads} "
+                                f"d{w.head_dim} position {w.q_chunk0 * w.chunk} {w.dtype} "
+                                f"F{w.keep_first} L{w.keep_last} Kc{w.topk_chunks} "
+                                f"Kg{w.topk_groups}, history in pinned host memory"),
+                   "seed": inp["seed"]},
+        "pcie_bytes_per_block": pcie,
+        "pcie_gbs_at_block_rate": round(pcie / dt / 1e9, 2),
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,6 +299,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dense", action="store_true",
+                    help="also time dense causal attention (torch SDPA) on the same Q/K/V; "
+                         "on by default for train12k")
     ap.add_argument("--route", choices=("qbar", "fused", "separate"), default="qbar",
                     help="qbar: hga_build_summaries_qbar + hga_route_qbar; fused: "
                          "hga_build_summaries + hga_route; separate: hga_build_summaries + "
@@ -234,12 +325,11 @@ def main():
     from paper_2606_30709_amd.pipeline import PrefillPipeline
 
     w = W.preset(args.workload)
-    if w.decode_block:
-        print("bench.py times the prefill workloads; the decode block is covered by the tests",
-              file=sys.stderr)
-        sys.exit(2)
     torch.cuda.set_device(0)
     inp = W.generate(w)
+    if w.decode_block:
+        decode_bench(w, inp, args)
+        return
     if args.probe_traffic:
         probe_traffic(w, inp, args.gather)
         return
@@ -333,8 +423,10 @@ def main():
             f()
             ev[s][n + 1].record(stream)
     torch.cuda.synchronize()
-    stage_ms = {name: float(np.mean([ev[s][n].elapsed_time(ev[s][n + 1]) for s in range(KB)]))
-                for n, name in enumerate(stage_names)}
+    stage_samples = {name: [ev[s][n].elapsed_time(ev[s][n + 1]) for s in range(KB)]
+                     for n, name in enumerate(stage_names)}
+    stage_samples[att_name] = [a.elapsed_time(b) for a, b in ev_a.values()]
+    stage_ms = {name: float(np.mean(x)) for name, x in stage_samples.items()}
     stage_ms[att_name] = attend_ms
     wall_ms = (t1 - t0) * 1e3 / K
     tokens = w.batch * w.seq_len
@@ -343,13 +435,18 @@ def main():
     abytes = algorithmic_bytes(w, n_valid_rows)
     flops = attention_flops(w, gi)
 
+    # achievable HBM bandwidth on this device, measured by a plain copy
+    copy_gbs = measured_copy_bandwidth()
     dominant = max(stage_names, key=lambda s: stage_ms[s])
     stages = {}
     for sname in stage_names:
         sec = stage_ms[sname] * 1e-3
+        p10, p50, p90 = np.percentile(stage_samples[sname], [10, 50, 90]) * 1e3
         ent = {"us": round(stage_ms[sname] * 1e3, 2),
+               "p10_p50_p90_us": [round(float(p10), 2), round(float(p50), 2), round(float(p90), 2)],
                "alg_bytes": abytes[sname], "GB_s": round(abytes[sname] / sec / 1e9, 1),
-               "hbm_frac": round(abytes[sname] / sec / 1e9 / HBM_PEAK_GBS, 4)}
+               "hbm_frac": round(abytes[sname] / sec / 1e9 / HBM_PEAK_GBS, 4),
+               "hbm_frac_of_copy": round(abytes[sname] / sec / 1e9 / copy_gbs, 4)}
         if sname in ATTENTION_STAGES:
             ent["TFLOP_s"] = round(flops / sec / 1e12, 2)
             ent["mfma_frac"] = round(flops / sec / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
@@ -371,7 +468,9 @@ def main():
     else:
         achieved = abytes[dominant] / dsec / 1e9
         roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "copy_measured_GB_s": round(copy_gbs, 1),
+                    "frac_of_copy": round(achieved / copy_gbs, 4)}
     roofline.update({
                 "traffic": (measured_traffic(dominant, w.key) if dominant in ATTENTION_STAGES
                             else None),
@@ -410,6 +509,11 @@ def main():
         "roofline": roofline,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }
+    if args.dense or w.key == "train12k":
+        dense = dense_comparator(w, pipe)
+        if dense.get("available"):
+            dense["routed_speedup"] = round(res["value"] / dense["tokens_per_s"], 3)
+        res["dense_comparator"] = dense
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, inp, args.cpu_seconds)
     print(json.dumps(res), flush=True)
