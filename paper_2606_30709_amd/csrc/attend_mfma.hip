@@ -215,27 +215,26 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
             }
         }
     };
-    // online-softmax update with the scores of `n` sub-tiles; P as bf16.
-    // kFirst: the wave's first scores (O and l still zero, and every lane
-    // has a visible key among them), so the reference point is simply set.
-    auto update = [&](const f32x16_t* sacc, int n, bf16x8_t* pf, auto first_tag) {
-        constexpr bool kFirst = decltype(first_tag)::value;
+    // The online softmax in three pieces.  The reference point m_run of the
+    // exponentials moves only when a sub-tile's maximum exceeds it by more
+    // than kSlack (log2 units): the weights exp2(s - m_run) then stay below
+    // 2^kSlack, exact in fp32 and in bf16's range, and the rescale of the
+    // output is rarely needed.  The normalisation and the log-sum-exp use
+    // the same m_run, so the result is the softmax for any reference point.
+    constexpr float kSlack = 8.0f;
+    // row maximum of one sub-tile's scores (scaled: log2 units), uniform over
+    // the two lanes of a query column
+    auto row_max = [&](const f32x16_t& sacc) {
         float tmax = -INFINITY;
-        for (int k = 0; k < n; ++k)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[k][e]);
-        tmax = max_xor32(tmax) * scale;
-        // The reference point m_run of the exponentials moves only when the
-        // tile's maximum exceeds it by more than kSlack (log2 units): the
-        // weights exp2(s - m_run) then stay below 2^kSlack, exact in fp32 and
-        // in bf16's range, and the rescale of the output is rarely needed.
-        // The normalisation and the log-sum-exp use the same m_run, so the
-        // result is the softmax for any reference point.
-        constexpr float kSlack = 8.0f;
-        const bool grow = tmax > m_run + kSlack;  // false while the row is fully masked
-        if (kFirst) {
-            m_run = tmax;
-        } else if (__builtin_amdgcn_ballot_w64(grow)) {
+        for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, sacc[e]);
+        return max_xor32(tmax) * scale;
+    };
+    // move the reference point to tmax where it exceeds it by more than
+    // kSlack (never while the row is fully masked), rescaling O and l
+    auto rebase = [&](float tmax) {
+        const bool grow = tmax > m_run + kSlack;
+        if (__builtin_amdgcn_ballot_w64(grow)) {
             const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - tmax) : 1.0f;
             l_run *= alpha;
 #pragma unroll
@@ -244,17 +243,29 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
                 for (int e = 0; e < 16; ++e) oacc[dt][e] *= alpha;
             m_run = grow ? tmax : m_run;
         }
-        const float m_use = m_run == -INFINITY ? 0.f : m_run;
-        for (int k = 0; k < n; ++k)
+    };
+    // weights of one sub-tile against reference m_use, added to l; P as bf16
+    auto exps = [&](const f32x16_t& sacc, float m_use, bf16x8_t* pf) {
 #pragma unroll
-            for (int kap = 0; kap < 2; ++kap)
+        for (int kap = 0; kap < 2; ++kap)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float pv =
-                        __builtin_amdgcn_exp2f(fmaf(sacc[k][kap * 8 + e], scale, -m_use));
-                    l_run += pv;
-                    pf[2 * k + kap][e] = static_cast<__bf16>(pv);
-                }
+            for (int e = 0; e < 8; ++e) {
+                const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[kap * 8 + e], scale, -m_use));
+                l_run += pv;
+                pf[kap][e] = static_cast<__bf16>(pv);
+            }
+    };
+    auto m_use = [&]() { return m_run == -INFINITY ? 0.f : m_run; };
+    // kFirst: the wave's first scores (O and l still zero, and every lane
+    // has a visible key among them), so the reference point is simply set.
+    auto update = [&](const f32x16_t& sacc, bf16x8_t* pf, auto first_tag) {
+        constexpr bool kFirst = decltype(first_tag)::value;
+        const float tmax = row_max(sacc);
+        if (kFirst)
+            m_run = tmax;
+        else
+            rebase(tmax);
+        exps(sacc, m_use(), pf);
     };
     // O^T += V^T.P^T for 32-key sub-tile st
     auto pv = [&](int st, const bf16x8_t* pf) {
@@ -288,38 +299,48 @@ __device__ __forceinline__ void tile_math(const bf16_t* sK, const bf16_t* sV,
             f32x16_t sacc[1];
             bf16x8_t pf[2];
             qk(ksplit, sacc[0], ksplit == tq);
-            update(sacc, 1, pf, First{});
+            update(sacc[0], pf, First{});
             pv(ksplit, pf);
         } else if (tq == 0) {
             f32x16_t s0[1];
             bf16x8_t p0[2];
             qk(0, s0[0], true);
-            update(s0, 1, p0, First{});
+            update(s0[0], p0, First{});
             pv(0, p0);
         } else {
             f32x16_t s0[1], s1[1];
             bf16x8_t p0[2], p1[2];
             qk(0, s0[0], false);
             qk(1, s1[0], true);
-            update(s0, 1, p0, First{});
+            update(s0[0], p0, First{});
             pv(0, p0);
-            update(s1, 1, p1, Later{});
+            update(s1[0], p1, Later{});
             pv(1, p1);
         }
     } else if constexpr (NST == 1) {
         f32x16_t sacc[1];
         bf16x8_t pf[2];
         qk(ksplit, sacc[0], false);
-        update(sacc, 1, pf, Later{});
+        update(sacc[0], pf, Later{});
         pv(ksplit, pf);
     } else {
-        f32x16_t s0[1], s1[1];
+        // The steps of update-then-product per sub-tile, ordered so that
+        // each sub-tile's exponentials sit beside the other sub-tile's
+        // matrix products (qk(1) beside the weights of sub-tile 0, pv(0)
+        // beside the maximum of sub-tile 1); every value is the one the
+        // plain order gives.  Masked scores (partial routed tiles) are -inf
+        // and weigh zero.
+        f32x16_t s0, s1;
         bf16x8_t p0[2], p1[2];
-        qk(0, s0[0], false);
-        qk(1, s1[0], false);
-        update(s0, 1, p0, Later{});
+        qk(0, s0, false);
+        rebase(row_max(s0));
+        const float mu0 = m_use();
+        qk(1, s1, false);
+        exps(s0, mu0, p0);
+        const float t1 = row_max(s1);
         pv(0, p0);
-        update(s1, 1, p1, Later{});
+        rebase(t1);
+        exps(s1, m_use(), p1);
         pv(1, p1);
     }
 }
