@@ -429,9 +429,10 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
 // with the first tiles, then the key tiles stream through the ring.
 // kGather: the routed rows are copied straight from the resident K/V (rows
 // g*G .. g*G+G-1 of each routed group g, zeros for a padded or future group,
-// as the gather step defines them), and the workgroup of part 0 of each unit
-// writes every routed tile it staged to k_routed / v_routed, so the call
-// also produces the gather step's output.  Otherwise the routed rows are
+// as the gather step defines them), and the unit's first workgroup writes
+// every routed tile it staged to k_routed / v_routed (with two or more
+// workgroups per unit the first writes K and the second V), so the call also
+// produces the gather step's output.  Otherwise the routed rows are
 // read from k_routed / v_routed.
 template <int D, int KS, int NS, int NW, bool kGather>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2))) void attend_mfma_kernel(
@@ -606,24 +607,32 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     };
     // kGather: write the routed tile in `stage` (this lane's own copies, so
     // its own wait suffices) to the routed buffers at the offsets it was
-    // copied from, rows past the unit's routed rows left out.
+    // copied from, rows past the unit's routed rows left out.  With several
+    // workgroups per unit, part 0 writes K and part 1 writes V.
+    const bool write_k = kGather && part == 0;
+    const bool write_v = kGather && part == (wg_div.d == 1 ? 0 : 1);
     auto write_routed = [&](int tile, int stage) {
         const int rt0 = (tile - 1 - n_vis) * KT;
-        bf16_t* kdst = k_routed + (unit * routed_rows + rt0) * D;
-        bf16_t* vdst = v_routed + (unit * routed_rows + rt0) * D;
         const unsigned char* sk = smem + stage * kStageBytes;
+        if (write_k) {
+            bf16_t* kdst = k_routed + (unit * routed_rows + rt0) * D;
 #pragma unroll
-        for (int u = 0; u < KI; ++u) {
-            const vec16 x = *reinterpret_cast<const vec16*>(sk + (u * NW + wave) * 1024 + lane * 16);
-            if (rt0 + static_cast<int>(koff[u] / kRowBytes) < routed_rows)
-                store16(reinterpret_cast<unsigned char*>(kdst) + koff[u], x);
+            for (int u = 0; u < KI; ++u) {
+                const vec16 x =
+                    *reinterpret_cast<const vec16*>(sk + (u * NW + wave) * 1024 + lane * 16);
+                if (rt0 + static_cast<int>(koff[u] / kRowBytes) < routed_rows)
+                    store16(reinterpret_cast<unsigned char*>(kdst) + koff[u], x);
+            }
         }
+        if (write_v) {
+            bf16_t* vdst = v_routed + (unit * routed_rows + rt0) * D;
 #pragma unroll
-        for (int u = 0; u < KI; ++u) {
-            const vec16 x = *reinterpret_cast<const vec16*>(sk + kTileBytes + (u * NW + wave) * 1024 +
-                                                            lane * 16);
-            if (rt0 + static_cast<int>(voff[u] / kRowBytes) < routed_rows)
-                store16(reinterpret_cast<unsigned char*>(vdst) + voff[u], x);
+            for (int u = 0; u < KI; ++u) {
+                const vec16 x = *reinterpret_cast<const vec16*>(sk + kTileBytes +
+                                                                (u * NW + wave) * 1024 + lane * 16);
+                if (rt0 + static_cast<int>(voff[u] / kRowBytes) < routed_rows)
+                    store16(reinterpret_cast<unsigned char*>(vdst) + voff[u], x);
+            }
         }
     };
     // Tiles requested up front; with kGather a routed tile needs the group
@@ -663,7 +672,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
         if (kCurrent) {
             for (int s = n_pre; s < n_up; ++s) issue(s, s);
         } else {
-            if (kGather && tile > n_vis && part == 0) write_routed(tile, tile % NS);
+            if (kGather && tile > n_vis && (write_k || write_v)) write_routed(tile, tile % NS);
             if (tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
         }
 
