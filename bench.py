@@ -289,6 +289,39 @@ def decode_bench(w, inp, args):
     print(json.dumps(res), flush=True)
 
 
+def blockwise_bench(w, inp, args):
+    """The prompt as a sequence of 64-token blocks (hga_prefill_blocks: per
+    block, routing against the chunks closed so far, gather + attention,
+    then the append of the block's summaries); one step = the whole prompt."""
+    import torch
+
+    from paper_2606_30709_amd.pipeline import BlockPrefillPipeline
+    pipe = BlockPrefillPipeline(w, inp)
+    for _ in range(args.warmup):
+        pipe.step()
+    torch.cuda.synchronize()
+    K = args.steps
+    t0 = time.perf_counter()
+    for _ in range(K):
+        pipe.step()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / K
+    tokens = w.batch * w.seq_len
+    res = {
+        "metric": "routed-attn block-sequential prefill tokens/s",
+        "value": round(tokens / dt, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": (f"{w.key}: block-sequential prefill B{w.batch} "
+                                f"H{w.n_q_heads}/{w.n_kv_heads} d{w.head_dim} N{w.seq_len} "
+                                f"{w.dtype}, {w.n_chunks} blocks of {w.chunk} tokens"),
+                   "seed": inp["seed"]},
+        "us_per_block": round(dt * 1e6 / w.n_chunks, 2),
+        "launches_per_block": 3,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -310,6 +343,8 @@ def main():
                     help="fused: hga_gather_attend (the attention stages the routed rows and "
                          "writes the routed buffers); separate: hga_gather_kv + hga_attend "
                          "(identical results)")
+    ap.add_argument("--blockwise", action="store_true",
+                    help="time the block-sequential prefill (hga_prefill_blocks) instead")
     ap.add_argument("--probe-traffic", action="store_true",
                     help="run attention and a known-size copy for rocprofv3 --pmc, then exit")
     args = ap.parse_args()
@@ -329,6 +364,9 @@ def main():
     inp = W.generate(w)
     if w.decode_block:
         decode_bench(w, inp, args)
+        return
+    if args.blockwise:
+        blockwise_bench(w, inp, args)
         return
     if args.probe_traffic:
         probe_traffic(w, inp, args.gather)

@@ -297,6 +297,55 @@ hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_
                              void* v_routed, void* out, float* lse, void* start_event,
                              void* stop_event, void* stream);
 
+/* One 64-token block of a block-sequential prefill (the paper's block
+ * processing with incremental store appends, Sec. 4.3): for query chunk c,
+ *   hga_route(plan, q_block, c, 1, chunk_sum, group_sum, table_chunks,
+ *             qbar, chunk_idx, group_idx, stream);
+ *   hga_gather_attend(plan, q_block, c, 1, k_res, v_res, res_tokens,
+ *                     group_idx, k_routed, v_routed, out, lse, NULL, NULL, stream);
+ *   hga_build_summaries(plan, k_res, res_tokens, 0, c, c + 1, chunk_sum,
+ *                       group_sum, table_chunks, stream);
+ * i.e. the block routes against the summaries of the chunks closed before
+ * it, attends, and then appends its own chunk's summaries.  Every argument
+ * is checked before the first launch.
+ *
+ *   q_block      [batch, n_q_heads, chunk, head_dim] plan dtype: the block's
+ *                queries (query chunk c)
+ *   k_res, v_res [batch, n_kv_heads, res_tokens, head_dim], token-indexed
+ *                (res_tokens >= (c + 1) * chunk)
+ *   chunk_sum, group_sum  as for hga_build_summaries, table_chunks >= c + 1;
+ *                rows of chunks < c are read, the rows of chunk c written
+ *   qbar, chunk_idx, group_idx, k_routed, v_routed, out, lse  the outputs of
+ *                the three calls for one query chunk ([.., 1, ..] shapes)
+ * Errors: those of the three calls. */
+hga_status hga_block_step(const hga_plan* plan, const void* q_block, int32_t c,
+                          const void* k_res, const void* v_res, int64_t res_tokens,
+                          float* chunk_sum, float* group_sum, int32_t table_chunks, float* qbar,
+                          int32_t* chunk_idx, int32_t* group_idx, void* k_routed, void* v_routed,
+                          void* out, float* lse, void* stream);
+
+/* A block-sequential prefill of blocks 0 .. n_blocks-1: hga_block_step for
+ * c = 0, 1, ... in order, all enqueued on `stream`.  Block c reads and
+ * writes the c-th slice of each block-major buffer:
+ *   q_blocks, out   [n_blocks][batch, n_q_heads, chunk, head_dim]
+ *   lse             [n_blocks][batch, n_q_heads, chunk] fp32 or NULL
+ *   qbar            [n_blocks][batch, n_kv_heads, 1, head_dim] fp32
+ *   chunk_idx       [n_blocks][batch, n_kv_heads, 1, topk_chunks] int32
+ *   group_idx       [n_blocks][batch, n_kv_heads, 1, topk_groups] int32
+ *   k_routed, v_routed  [n_blocks][batch, n_kv_heads, 1, topk_groups*group, head_dim]
+ * k_res/v_res hold the whole prompt's keys and values (token-indexed,
+ * res_tokens >= n_blocks * chunk); the summary tables are built as the
+ * blocks close.  Every block's outputs equal what the bulk prefill
+ * (hga_build_summaries, then hga_route and hga_gather_attend over all chunks)
+ * writes for the same query chunk.  Arguments are checked before the first
+ * launch; an error returned by a later launch leaves the earlier blocks done. */
+hga_status hga_prefill_blocks(const hga_plan* plan, const void* q_blocks, int32_t n_blocks,
+                              const void* k_res, const void* v_res, int64_t res_tokens,
+                              float* chunk_sum, float* group_sum, int32_t table_chunks,
+                              float* qbar, int32_t* chunk_idx, int32_t* group_idx,
+                              void* k_routed, void* v_routed, void* out, float* lse,
+                              void* stream);
+
 /* Static description of a status code (never NULL). */
 const char* hga_status_string(int32_t status);
 

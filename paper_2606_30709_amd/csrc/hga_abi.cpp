@@ -522,6 +522,114 @@ hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_
                     "hga_gather_attend launch");
 }
 
+namespace {
+
+// Checks of one block step on chunk c (nothing launched).
+hga_status check_block_step(const hga_plan* plan, const void* q_block, int32_t c,
+                            const void* k_res, const void* v_res, int64_t res_tokens,
+                            float* chunk_sum, float* group_sum, int32_t table_chunks, float* qbar,
+                            int32_t* chunk_idx, int32_t* group_idx, void* k_routed,
+                            void* v_routed, void* out, float* lse) {
+    HGA_TRY(check_plan(plan));
+    const hga_params& p = plan->p;
+    if (c < 0 || res_tokens < 0 || table_chunks < 0)
+        return fail(HGA_EINVAL, "c, res_tokens and table_chunks must be >= 0");
+    if (table_chunks < c + 1)
+        return fail(HGA_EINVAL, "the block's chunk %d needs table_chunks > %d (got %d)", c, c,
+                    table_chunks);
+    int n_max = 0;
+    HGA_TRY(check_route_chunks(plan, q_block, c, 1, chunk_sum, table_chunks, qbar, chunk_idx,
+                               true, &n_max, "q_block"));
+    HGA_TRY(check_tensor(group_sum, "group_sum"));
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    HGA_TRY(check_attend(plan, q_block, c, 1, k_res, v_res, res_tokens, nullptr, k_routed,
+                         v_routed, group_idx, out, lse));
+    bool empty = false;
+    HGA_TRY(check_summaries(plan, k_res, res_tokens, 0, c, c + 1, chunk_sum, group_sum,
+                            table_chunks, &empty));
+    (void)p;
+    return HGA_OK;
+}
+
+// The three launches of one block step (checks done).
+hipError_t launch_block_step(const hga_plan& plan, const void* q_block, int32_t c,
+                             const void* k_res, const void* v_res, int64_t res_tokens,
+                             float* chunk_sum, float* group_sum, int32_t table_chunks,
+                             float* qbar, int32_t* chunk_idx, int32_t* group_idx, void* k_routed,
+                             void* v_routed, void* out, float* lse, hipStream_t stream) {
+    hipError_t e = hga::launch_route(plan, q_block, c, 1, chunk_sum, group_sum, table_chunks,
+                                     qbar, chunk_idx, group_idx, stream);
+    if (e != hipSuccess) return e;
+    e = hga::launch_gather_attend(plan, q_block, c, 1, k_res, v_res, res_tokens, group_idx,
+                                  k_routed, v_routed, out, lse, nullptr, nullptr, stream);
+    if (e != hipSuccess) return e;
+    return hga::launch_build_summaries(plan, k_res, res_tokens, 0, c, c + 1, chunk_sum,
+                                       group_sum, table_chunks, stream);
+}
+
+}  // namespace
+
+hga_status hga_block_step(const hga_plan* plan, const void* q_block, int32_t c,
+                          const void* k_res, const void* v_res, int64_t res_tokens,
+                          float* chunk_sum, float* group_sum, int32_t table_chunks, float* qbar,
+                          int32_t* chunk_idx, int32_t* group_idx, void* k_routed, void* v_routed,
+                          void* out, float* lse, void* stream) {
+    HGA_TRY(check_block_step(plan, q_block, c, k_res, v_res, res_tokens, chunk_sum, group_sum,
+                             table_chunks, qbar, chunk_idx, group_idx, k_routed, v_routed, out,
+                             lse));
+    clear_stale_error();
+    return launched(launch_block_step(*plan, q_block, c, k_res, v_res, res_tokens, chunk_sum,
+                                      group_sum, table_chunks, qbar, chunk_idx, group_idx,
+                                      k_routed, v_routed, out, lse,
+                                      static_cast<hipStream_t>(stream)),
+                    "hga_block_step launch");
+}
+
+hga_status hga_prefill_blocks(const hga_plan* plan, const void* q_blocks, int32_t n_blocks,
+                              const void* k_res, const void* v_res, int64_t res_tokens,
+                              float* chunk_sum, float* group_sum, int32_t table_chunks,
+                              float* qbar, int32_t* chunk_idx, int32_t* group_idx,
+                              void* k_routed, void* v_routed, void* out, float* lse,
+                              void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (n_blocks < 0) return fail(HGA_EINVAL, "n_blocks must be >= 0");
+    if (n_blocks == 0) return HGA_OK;
+    const hga_params& p = plan->p;
+    const int64_t eb = p.dtype == HGA_BF16 ? 2 : 4;
+    const int64_t bq = static_cast<int64_t>(p.batch) * p.n_q_heads * p.chunk;  // rows per block
+    const int64_t bkv = static_cast<int64_t>(p.batch) * p.n_kv_heads;
+    const int64_t q_bytes = bq * p.head_dim * eb;
+    const int64_t qbar_elems = bkv * p.head_dim;
+    const int64_t ci_elems = bkv * p.topk_chunks;
+    const int64_t gi_elems = bkv * p.topk_groups;
+    const int64_t rt_bytes = bkv * p.topk_groups * p.group * p.head_dim * eb;
+    auto at = [](const void* base, int64_t bytes) {
+        return static_cast<const void*>(static_cast<const unsigned char*>(base) + bytes);
+    };
+    auto atw = [](void* base, int64_t bytes) {
+        return static_cast<void*>(static_cast<unsigned char*>(base) + bytes);
+    };
+    // every block is checked before the first launch (the last block is the
+    // most demanding, block 0 the one with no candidates)
+    for (int32_t c : {0, n_blocks - 1}) {
+        HGA_TRY(check_block_step(
+            plan, at(q_blocks, c * q_bytes), c, k_res, v_res, res_tokens, chunk_sum, group_sum,
+            table_chunks, qbar + c * qbar_elems, chunk_idx + c * ci_elems,
+            group_idx + c * gi_elems, atw(k_routed, c * rt_bytes), atw(v_routed, c * rt_bytes),
+            atw(out, c * q_bytes), lse ? lse + c * bq : nullptr));
+    }
+    clear_stale_error();
+    for (int32_t c = 0; c < n_blocks; ++c) {
+        const hipError_t e = launch_block_step(
+            *plan, at(q_blocks, c * q_bytes), c, k_res, v_res, res_tokens, chunk_sum, group_sum,
+            table_chunks, qbar + c * qbar_elems, chunk_idx + c * ci_elems,
+            group_idx + c * gi_elems, atw(k_routed, c * rt_bytes), atw(v_routed, c * rt_bytes),
+            atw(out, c * q_bytes), lse ? lse + c * bq : nullptr, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return launched(e, "hga_prefill_blocks launch");
+    }
+    return HGA_OK;
+}
+
 hga_status hga_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                       int32_t n_q_chunks, const void* k_res, const void* v_res,
                       int64_t res_tokens, const int32_t* res_slot, const void* k_routed,

@@ -244,20 +244,28 @@ __global__ __launch_bounds__(256) void route_kernel(
     for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
     if constexpr (!kGroups) return;
 
-    // 4. group refinement of the chosen chunks.
+    // 4. group refinement of the chosen chunks.  When every candidate is
+    // kept (K_g >= the candidates: the chunk-only variant, all groups of the
+    // chosen chunks opened) the selection is the candidates in ascending
+    // order, written without scoring.
+    const int ng = k * gpc;
+    int32_t* gout = group_idx + unit * topk_groups;
+    if (ng <= topk_groups) {
+        for (int t = lane; t < topk_groups; t += 64)
+            gout[t] = t < ng ? L.sel[t >> gpc_shift] * gpc + (t & (gpc - 1)) : -1;
+        return;
+    }
     for (int t = lane; t < k; t += 64) L.list[t] = L.sel[t];
     wave_sync_lds();
-    const int ng = k * gpc;
     const float* gtab = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
     score_candidates<D>(
         L.q, gtab, [&](int m) { return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1)); }, ng,
         L.keys);
     wave_sync_lds();
-    const int kg = ng < topk_groups ? ng : topk_groups;
+    const int kg = topk_groups;
     wave_select_topk(L.keys, ng, kg, L.sel, L.scr);
     wave_sync_lds();
-    int32_t* gout = group_idx + unit * topk_groups;
-    for (int t = lane; t < topk_groups; t += 64) gout[t] = t < kg ? L.sel[t] : -1;
+    for (int t = lane; t < topk_groups; t += 64) gout[t] = L.sel[t];
 }
 
 template <int D>
@@ -293,16 +301,20 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
     wave_sync_lds();
 
     const int n = nv * gpc;
+    int32_t* out = group_idx + static_cast<int64_t>(unit) * topk_groups;
+    if (n <= topk_groups) {  // every candidate kept: ascending, no scores needed
+        for (int t = lane; t < topk_groups; t += 64)
+            out[t] = t < n ? L.list[t >> gpc_shift] * gpc + (t & (gpc - 1)) : -1;
+        return;
+    }
     const float* table = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
     score_candidates<D>(
         L.q, table, [&](int m) { return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1)); }, n,
         L.keys);
     wave_sync_lds();
-    const int k = n < topk_groups ? n : topk_groups;
-    wave_select_topk(L.keys, n, k, L.sel, L.scr);
+    wave_select_topk(L.keys, n, topk_groups, L.sel, L.scr);
     wave_sync_lds();
-    int32_t* out = group_idx + static_cast<int64_t>(unit) * topk_groups;
-    for (int t = lane; t < topk_groups; t += 64) out[t] = t < k ? L.sel[t] : -1;
+    for (int t = lane; t < topk_groups; t += 64) out[t] = L.sel[t];
 }
 
 // Up to four waves per workgroup, as many as the LDS budget allows.

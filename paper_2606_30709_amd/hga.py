@@ -18,8 +18,8 @@ __all__ = [
     "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
-    "hga_attend_timed", "hga_gather_attend", "hga_status_string", "hga_last_error",
-    "hga_version", "EXPORTED_SYMBOLS",
+    "hga_attend_timed", "hga_gather_attend", "hga_block_step", "hga_prefill_blocks",
+    "hga_status_string", "hga_last_error", "hga_version", "EXPORTED_SYMBOLS",
 ]
 
 F32, BF16 = 0, 1
@@ -29,7 +29,7 @@ EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
     "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_gather_attend",
-    "hga_status_string", "hga_last_error", "hga_version",
+    "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error", "hga_version",
 )
 
 
@@ -83,6 +83,10 @@ def library() -> ctypes.CDLL:
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
             "hga_gather_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp],
+            "hga_block_step": [vp, vp, i32, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp, vp,
+                               vp, vp],
+            "hga_prefill_blocks": [vp, vp, i32, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp,
+                                   vp, vp, vp],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
@@ -283,3 +287,25 @@ def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx,
         _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse),
         start_event.cuda_event if start_event is not None else None,
         stop_event.cuda_event if stop_event is not None else None, _stream(stream)))
+
+
+def hga_block_step(plan: Plan, q_block, c: int, k_res, v_res, chunk_sum, group_sum, qbar,
+                   chunk_idx, group_idx, k_routed, v_routed, out, lse=None, stream=None):
+    """One block of a block-sequential prefill: route query chunk c, gather +
+    attend it, append chunk c's summaries.  q_block/out [B, Hq, C, d];
+    k_res/v_res [B, Hkv, res_tokens, d]; the per-chunk outputs have a
+    query-chunk dimension of 1."""
+    _check(library().hga_block_step(
+        plan.handle, _ptr(q_block), c, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(chunk_sum), _ptr(group_sum), chunk_sum.shape[2], _ptr(qbar), _ptr(chunk_idx),
+        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def hga_prefill_blocks(plan: Plan, q_blocks, k_res, v_res, chunk_sum, group_sum, qbar,
+                       chunk_idx, group_idx, k_routed, v_routed, out, lse=None, stream=None):
+    """hga_block_step for blocks 0 .. n_blocks-1 in order; block-major
+    buffers (first dimension n_blocks)."""
+    _check(library().hga_prefill_blocks(
+        plan.handle, _ptr(q_blocks), q_blocks.shape[0], _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(chunk_sum), _ptr(group_sum), chunk_sum.shape[2], _ptr(qbar), _ptr(chunk_idx),
+        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse), _stream(stream)))

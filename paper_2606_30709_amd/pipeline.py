@@ -30,7 +30,7 @@ import torch
 
 from . import hga
 
-__all__ = ["PrefillPipeline", "DecodePipeline", "to_device"]
+__all__ = ["PrefillPipeline", "BlockPrefillPipeline", "DecodePipeline", "to_device"]
 
 
 def to_device(arr: np.ndarray, dtype: str, device="cuda", pin=False) -> torch.Tensor:
@@ -114,6 +114,43 @@ class PrefillPipeline:
         else:
             self.gather(stream)
             self.attend(stream)
+
+
+class BlockPrefillPipeline:
+    """The prompt processed as a sequence of 64-token blocks, each routed
+    against the summaries of the chunks closed before it, attended, and then
+    appended to the tables (``hga_prefill_blocks``: one native loop of
+    ``hga_block_step``).  Queries, outputs and the per-block routing results
+    are block-major ([n_blocks, ...]); K/V are the whole prompt's,
+    token-indexed, as in the bulk prefill."""
+
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None):
+        assert not w.decode_block
+        self.w = w
+        self.plan = plan or hga.Plan.for_workload(w)
+        B, Hq, Hkv, d, C, G = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.chunk, w.group
+        nc = w.n_chunks
+        f32, i32 = torch.float32, torch.int32
+        q = np.ascontiguousarray(
+            inputs["q"].reshape(B, Hq, nc, C, d).transpose(2, 0, 1, 3, 4))
+        self.q_blocks = to_device(q, w.dtype, device)            # [nc, B, Hq, C, d]
+        self.k = to_device(inputs["k"], w.dtype, device)
+        self.v = to_device(inputs["v"], w.dtype, device)
+        dt = self.k.dtype
+        self.chunk_sum = torch.zeros(B, Hkv, nc, d, dtype=f32, device=device)
+        self.group_sum = torch.zeros(B, Hkv, nc * (C // G), d, dtype=f32, device=device)
+        self.qbar = torch.empty(nc, B, Hkv, 1, d, dtype=f32, device=device)
+        self.chunk_idx = torch.empty(nc, B, Hkv, 1, w.topk_chunks, dtype=i32, device=device)
+        self.group_idx = torch.empty(nc, B, Hkv, 1, w.topk_groups, dtype=i32, device=device)
+        self.k_routed = torch.empty(nc, B, Hkv, 1, w.topk_groups * G, d, dtype=dt, device=device)
+        self.v_routed = torch.empty_like(self.k_routed)
+        self.out = torch.empty_like(self.q_blocks)
+        self.lse = torch.empty(nc, B, Hq, C, dtype=f32, device=device)
+
+    def step(self, stream=None):
+        hga.hga_prefill_blocks(self.plan, self.q_blocks, self.k, self.v, self.chunk_sum,
+                               self.group_sum, self.qbar, self.chunk_idx, self.group_idx,
+                               self.k_routed, self.v_routed, self.out, self.lse, stream=stream)
 
 
 class DecodePipeline:

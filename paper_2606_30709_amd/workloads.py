@@ -7,7 +7,7 @@ are already-rotated queries and keys, Sec. 2 "RoPE" and Sec. 4.1), plants
 the routing method's arithmetic (no summaries, scores, selection or
 attention), so both the float64 oracle and the HIP path can consume its bytes.
 
-The five presets mirror the paper's shapes:
+The presets mirror the paper's shapes:
 
 * ``tiny``      B1 H1/1 d64 N1024 fp32 (oracle-sized prefill)
 * ``smalllm``   B4 H8/8 d64 N8192 bf16 (the 40M SmallLM head shape, Sec. 4.2;
@@ -19,6 +19,9 @@ The five presets mirror the paper's shapes:
 * ``decode64k`` one 64-token query block after 65,536 history tokens at the
   Qwen3 shape (the 64K needle-in-a-haystack setting, Sec. 5.3), history in
   pinned host memory
+* ``qwen32k_chunks`` the qwen32k shape with the chunk-only routing variant
+  of the exact-token Qwen3 wrapper (Sec. 4.1: 16 chunks routed, every group
+  of each opened; two sink and eight recent chunks)
 
 Draw order for every preset (seed recorded in the returned dict): raw Q, raw
 K, V, then needle placements, then needle directions.  RoPE is applied in
@@ -108,6 +111,13 @@ PRESETS = {
         head_dim=128, seq_len=32768, dtype="bf16", rope_base=1e6, keep_first=1,
         keep_last=2, topk_chunks=30, topk_groups=48, needle_mode="pairs",
         needle_count=16, needle_shift=1.5, seed=1004),
+    # the chunk-only variant (the paper's exact-token Qwen3 wrapper): 16 chunks
+    # routed, every group of each opened, at the qwen32k shape
+    "qwen32k_chunks": Workload(
+        key="qwen32k_chunks", number=6, batch=1, n_q_heads=32, n_kv_heads=4,
+        head_dim=128, seq_len=32768, dtype="bf16", rope_base=1e6, keep_first=2,
+        keep_last=8, topk_chunks=16, topk_groups=64, needle_mode="pairs",
+        needle_count=16, needle_shift=1.5, seed=1006),
     "decode64k": Workload(
         key="decode64k", number=5, batch=1, n_q_heads=32, n_kv_heads=4,
         head_dim=128, seq_len=65536 + 64, dtype="bf16", rope_base=1e6,

@@ -89,6 +89,10 @@ def test_calls_reject_null_plan():
                                 None, None, None, None) == -1
     assert lib.hga_gather_attend(None, None, 0, 0, None, None, 0, None, None, None, None, None,
                                  None, None, None) == -1
+    assert lib.hga_block_step(None, None, 0, None, None, 0, None, None, 0, None, None, None,
+                              None, None, None, None, None) == -1
+    assert lib.hga_prefill_blocks(None, None, 0, None, None, 0, None, None, 0, None, None, None,
+                                  None, None, None, None, None) == -1
     assert lib.hga_plan_destroy(None) == 0
 
 

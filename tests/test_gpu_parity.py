@@ -64,6 +64,8 @@ SMALL = {
     "tiny_noforce": W_("tiny", force_prev=0),
     "f32_d128_gqa": W_("tiny", seq_len=1024, n_q_heads=4, n_kv_heads=2, head_dim=128,
                        rope_base=1e6, topk_chunks=3, topk_groups=5, keep_last=2),
+    # the chunk-only variant: every group of the routed chunks opened
+    "qwen_chunks_4k": W_("qwen32k_chunks", seq_len=4096),
 }
 
 
@@ -337,6 +339,46 @@ def test_gather_attend_full_size(hga):
         torch.cuda.empty_cache()
 
 
+# ------------------------------------------------ block-sequential prefill ---
+
+BLOCK_CASES = {k: SMALL[k] for k in ("tiny", "smalllm_2k", "qwen_4k_ragged", "qwen_g8",
+                                      "gqa3_d64", "qwen_chunks_4k")}
+
+
+@pytest.mark.parametrize("key", list(BLOCK_CASES))
+def test_block_sequential_prefill_equals_bulk(hga, key):
+    """Prefill as a sequence of 64-token blocks (route against the chunks
+    closed so far, attend, append) writes, block by block, exactly what the
+    bulk prefill writes for the same query chunk: prefill = decode."""
+    from paper_2606_30709_amd.pipeline import BlockPrefillPipeline, PrefillPipeline
+    w = BLOCK_CASES[key]
+    _say(f"[block-prefill] {key}")
+    inp = W.generate(w)
+    bulk = PrefillPipeline(w, inp)
+    bulk.step()
+    blk = BlockPrefillPipeline(w, inp)
+    for t in (blk.out, blk.lse, blk.qbar):
+        t.fill_(float("nan"))
+    blk.chunk_idx.fill_(-7)
+    blk.group_idx.fill_(-7)
+    blk.step()
+    torch.cuda.synchronize()
+    nc, C = w.n_chunks, w.chunk
+    B, Hq, d = w.batch, w.n_q_heads, w.head_dim
+    same = lambda a, b: torch.equal(_bits(a.contiguous()), _bits(b.contiguous()))
+    assert same(blk.chunk_sum, bulk.chunk_sum) and same(blk.group_sum, bulk.group_sum)
+    # block-major -> bulk layouts
+    assert same(blk.qbar[:, :, :, 0].permute(1, 2, 0, 3), bulk.qbar)
+    assert torch.equal(blk.chunk_idx[:, :, :, 0].permute(1, 2, 0, 3), bulk.chunk_idx)
+    assert torch.equal(blk.group_idx[:, :, :, 0].permute(1, 2, 0, 3), bulk.group_idx)
+    assert same(blk.k_routed[:, :, :, 0].permute(1, 2, 0, 3, 4), bulk.k_routed)
+    assert same(blk.v_routed[:, :, :, 0].permute(1, 2, 0, 3, 4), bulk.v_routed)
+    out_bulk = bulk.out.reshape(B, Hq, nc, C, d).permute(2, 0, 1, 3, 4)
+    assert same(blk.out, out_bulk)
+    lse_bulk = bulk.lse.reshape(B, Hq, nc, C).permute(2, 0, 1, 3)
+    assert same(blk.lse, lse_bulk)
+
+
 def _split_route_check(hga, plan, k, k_chunk0, n_chunks, table_chunks, q, q_chunk0, w):
     """hga_build_summaries_qbar + hga_route_qbar against hga_build_summaries +
     hga_route, bit for bit."""
@@ -506,7 +548,7 @@ def test_decode_block_parity_full(hga):
 
 # -------------------------------------------------------------- full size ---
 
-@pytest.mark.parametrize("key", ["smalllm", "train12k", "qwen32k"])
+@pytest.mark.parametrize("key", ["smalllm", "train12k", "qwen32k", "qwen32k_chunks"])
 def test_prefill_parity_full_size_sampled(hga, key):
     """Full sizes, launched exactly as the benchmark does; the oracle checks
     every summary and query mean, the routing of sampled query chunks, and
