@@ -195,7 +195,8 @@ __device__ inline void wave_select_topk_lds(uint64_t* keys, int n, int k, int* s
 // share of the keys held in registers: a round is one wave maximum and a
 // register rescan, and winner `round` is kept by lane `round`.
 template <int R>
-__device__ inline void wave_select_topk_regs(const uint64_t* keys, int n, int k, int* sel) {
+__device__ __forceinline__ void wave_select_topk_regs(const uint64_t* keys, int n, int k,
+                                                      int* sel) {
     const int lane = threadIdx.x & 63;
     uint64_t v[R];
 #pragma unroll
@@ -215,9 +216,69 @@ __device__ inline void wave_select_topk_regs(const uint64_t* keys, int n, int k,
     if (lane < k) sel[rank] = mine;
 }
 
-// Dispatch on size; every form selects the same keys.
-__device__ inline void wave_select_topk(uint64_t* keys, int n, int k, int* sel, int* scratch) {
-    if (k <= 64 && n <= 64)
+// The same selection by a threshold instead of k rounds, for larger k: the
+// k-th largest score T (the high words) is found bit by bit from the most
+// significant one -- T grows by a bit while at least k keys stay >= T, a
+// ballot count per bit -- then every key above T is taken and, of the keys
+// equal to T, the first k - (#above) in position order (equal scores go to
+// the lower index).  Positions are then compacted in order, so the output is
+// ascending by position; callers whose ids increase with the position (both
+// routing stages) get ascending ids, as from the rounds.  n <= 64 * R keys,
+// k <= n.
+template <int R>
+__device__ __forceinline__ void wave_select_topk_threshold(const uint64_t* keys, int n, int k,
+                                                           int* sel) {
+    const int lane = threadIdx.x & 63;
+    uint32_t hi[R], id[R];
+#pragma unroll
+    for (int t = 0; t < R; ++t) {
+        const uint64_t v = lane + 64 * t < n ? keys[lane + 64 * t] : 0;
+        hi[t] = static_cast<uint32_t>(v >> 32);  // 0 marks no key; real keys are above 0
+        id[t] = static_cast<uint32_t>(key_index(v));
+    }
+    uint32_t T = 0;
+    for (int b = 31; b >= 0; --b) {
+        const uint32_t cand = T | (1u << b);
+        int cnt = 0;
+#pragma unroll
+        for (int t = 0; t < R; ++t) cnt += __popcll(__builtin_amdgcn_ballot_w64(hi[t] >= cand));
+        if (cnt >= k) T = cand;
+    }
+    int need = k;
+#pragma unroll
+    for (int t = 0; t < R; ++t) need -= __popcll(__builtin_amdgcn_ballot_w64(hi[t] > T));
+    int base = 0;
+    const uint64_t below = (uint64_t(1) << lane) - 1;
+#pragma unroll
+    for (int t = 0; t < R; ++t) {
+        // a tied key is taken when fewer than `need` ties precede it
+        const bool eq = hi[t] == T;
+        const uint64_t eqm = __builtin_amdgcn_ballot_w64(eq);
+        const bool pick = hi[t] > T || (eq && __popcll(eqm & below) < need);
+        const uint64_t m = __builtin_amdgcn_ballot_w64(pick);
+        if (pick) sel[base + __popcll(m & below)] = static_cast<int>(id[t]);
+        base += __popcll(m);
+        const int ne = __popcll(eqm);
+        need -= ne < need ? ne : need;
+    }
+}
+
+// Dispatch on size; every form selects the same keys and writes them in
+// ascending id order.  The threshold form (for k >= 8, where k rounds cost
+// more than its 32 steps) needs ids that increase with the position
+// (`ids_by_position`); the others sort by id themselves.
+__device__ __forceinline__ void wave_select_topk(uint64_t* keys, int n, int k, int* sel,
+                                                 int* scratch, bool ids_by_position = false) {
+    if (ids_by_position && k >= 8 && n <= 64 * 16) {
+        if (n <= 64 * 2)
+            wave_select_topk_threshold<2>(keys, n, k, sel);
+        else if (n <= 64 * 4)
+            wave_select_topk_threshold<4>(keys, n, k, sel);
+        else if (n <= 64 * 8)
+            wave_select_topk_threshold<8>(keys, n, k, sel);
+        else
+            wave_select_topk_threshold<16>(keys, n, k, sel);
+    } else if (k <= 64 && n <= 64)
         wave_select_topk_regs<1>(keys, n, k, sel);
     else if (k <= 64 && n <= 64 * 2)
         wave_select_topk_regs<2>(keys, n, k, sel);

@@ -238,7 +238,7 @@ __global__ __launch_bounds__(256) void route_kernel(
 
     // 3. top-k chunks, ascending, -1 padded.
     const int k = n < topk ? n : topk;
-    wave_select_topk(L.keys, n, k, L.sel, L.scr);
+    wave_select_topk(L.keys, n, k, L.sel, L.scr, true);  // ids keep_first + m
     wave_sync_lds();
     int32_t* out = chunk_idx + unit * topk;
     for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
@@ -263,7 +263,7 @@ __global__ __launch_bounds__(256) void route_kernel(
         L.keys);
     wave_sync_lds();
     const int kg = topk_groups;
-    wave_select_topk(L.keys, ng, kg, L.sel, L.scr);
+    wave_select_topk(L.keys, ng, kg, L.sel, L.scr, true);  // groups of ascending chunks
     wave_sync_lds();
     for (int t = lane; t < topk_groups; t += 64) gout[t] = L.sel[t];
 }
