@@ -317,6 +317,279 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
     for (int t = lane; t < topk_groups; t += 64) out[t] = L.sel[t];
 }
 
+// Top-k by a whole workgroup of kThreads threads, for keys whose ids ascend
+// with their position: writes the k ids with the largest keys to sel[0 .. k)
+// in ascending order (0 < k <= n); sel is complete when it returns.  Every
+// thread must call it.  Short lists (and lists longer than the workgroup)
+// go to wave 0's wave_select_topk.  Otherwise thread t holds key t and:
+// 1. each wave finds T_w, the k-th largest score word among its own keys
+//    (bit-by-bit bisection on ballot counts; 0 if it holds fewer than k);
+//    the k-th largest word of all keys is at least L = max_w T_w, so every
+//    key of the top k has a word >= L;
+// 2. the keys with word >= L (usually a few times k) are compacted in
+//    position order, which keeps ids ascending;
+// 3. wave 0 selects the top k of those with wave_select_topk.
+// The result is the exact top k with wave_select_topk's tie rule.
+template <int kThreads>
+struct WgSelect {
+    uint32_t wave_t[kThreads / 64];
+    int wave_cnt[kThreads / 64];
+    uint64_t surv[kThreads];
+};
+
+template <int kThreads>
+__device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int* sel, int* scr,
+                                               WgSelect<kThreads>* S) {
+    constexpr int NW = kThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (n <= 256 || n > kThreads) {
+        if (wave == 0) wave_select_topk(keys, n, k, sel, scr, true);
+        __syncthreads();
+        return;
+    }
+    const uint64_t key = tid < n ? keys[tid] : 0;
+    const uint32_t hi = static_cast<uint32_t>(key >> 32);
+    const bool valid = tid < n;
+    uint32_t t_w = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t cand = t_w | (1u << bit);
+        if (__popcll(__ballot(valid && hi >= cand)) >= k) t_w = cand;
+    }
+    if (lane == 0) S->wave_t[wave] = t_w;
+    __syncthreads();
+    uint32_t bound = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) bound = S->wave_t[w] > bound ? S->wave_t[w] : bound;
+    const bool keep = valid && hi >= bound;
+    const uint64_t km = __ballot(keep);
+    if (lane == 0) S->wave_cnt[wave] = __popcll(km);
+    __syncthreads();
+    int pos = __popcll(km & ((uint64_t(1) << lane) - 1)), n_keep = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        const int cw = S->wave_cnt[w];
+        n_keep += cw;
+        if (w < wave) pos += cw;
+    }
+    if (keep) S->surv[pos] = key;
+    __syncthreads();
+    if (wave == 0) wave_select_topk(S->surv, n_keep, k, sel, scr, true);
+    __syncthreads();
+}
+
+// q_bar from the chunk's r*64 query rows staged in LDS (row-major, D
+// elements of T per row; rows a multiple of 64), by the first NRS * D
+// threads of the workgroup:
+// thread (rs, d) adds element d of rows rs, rs + NRS, ... in ascending order,
+// the chain one lane of wave_mean_rows keeps for that element, then thread d
+// adds the NRS partial sums in the same pairwise tree as its butterfly.  So
+// the result is bit-identical to wave_mean_rows<T, D> over the same rows.
+// `part` is LDS scratch of NRS * D floats; every thread must call it.
+template <typename T, int D>
+__device__ __forceinline__ void wg_mean_rows(const T* rows_lds, int rows, float* part, float* out) {
+    constexpr int VPR = D / elem<T>::kVec;
+    constexpr int NRS = 64 / VPR;
+    constexpr int kU = 8;
+    static_assert(64 % (NRS * kU) == 0, "rows (a multiple of 64) split evenly");
+    const int tid = threadIdx.x;
+    if (tid < NRS * D) {
+        const int rs = tid / D, d = tid % D;
+        float acc = 0.f;
+        for (int row0 = rs; row0 < rows; row0 += NRS * kU) {
+            float f[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) f[u] = elem<T>::to_f32(rows_lds[(row0 + u * NRS) * D + d]);
+#pragma unroll
+            for (int u = 0; u < kU; ++u) acc += f[u];
+        }
+        part[rs * D + d] = acc;
+    }
+    __syncthreads();
+    if (tid < D) {
+        float v[NRS];
+#pragma unroll
+        for (int x = 0; x < NRS; ++x) v[x] = part[x * D + tid];
+#pragma unroll
+        for (int step = 1; step < NRS; step <<= 1)
+#pragma unroll
+            for (int x = 0; x < NRS; x += 2 * step) v[x] = v[x] + v[x + step];
+        out[tid] = v[0] * (1.0f / static_cast<float>(rows));
+    }
+}
+
+// Routing of one unit by a whole workgroup of 16 wavefronts, for launches
+// with too few units to fill the chip (a decode block, a block-sequential
+// prefill step).  The outputs are bit-identical to route_kernel's: every
+// score has the same arithmetic, only the work is spread wider.
+// * q_bar: the chunk's r*64 query rows are staged in LDS by all threads at
+//   once (one round trip instead of one per 16 rows), then wave 0 reduces
+//   them with the shared fixed-order code.  The first table block is
+//   requested before that, so it arrives while q_bar is formed.
+// * chunk scores: the table goes through LDS in blocks of kWideRows rows
+//   (coalesced 16-byte loads, the next block in registers while the current
+//   one is scored).  Four lanes score one row: lane qd sums the dimensions
+//   d = qd mod 4 in order, and the quad adds the four partial sums pairwise,
+//   ((s0 + s1) + (s2 + s3)), the same operations as one lane doing all four.
+//   Wave 0 selects the top K_c.
+// * group scores: wave w scores candidates 16w .. 16w + 15 (+ 256 per
+//   pass) with batch_keys, whose per-candidate arithmetic does not depend on
+//   the batch; wave 0 selects the top K_g.
+// LDS: the WaveLds pieces (keys for the larger candidate list), then one
+// region at big_off that holds the staged query rows and then table blocks.
+constexpr int kWideRows = 256;
+
+template <typename T, int D, bool kGroups, bool kQbarIn>
+__global__ __launch_bounds__(1024) void route_wide_kernel(
+    const T* __restrict__ q_rot, int q_chunk0, int n_q_chunks, const float* __restrict__ chunk_sum,
+    const float* __restrict__ group_sum, int table_chunks, float* __restrict__ qbar,
+    int32_t* __restrict__ chunk_idx, int32_t* __restrict__ group_idx, int n_q_heads, int n_kv,
+    int keep_first, int window, int topk, int topk_groups, int gpc_shift, int big_off) {
+    constexpr int kThreads = 1024;
+    constexpr int F4 = D / 4;                     // float4 per table row
+    constexpr int TS = D + 4;                     // padded LDS row stride (floats)
+    constexpr int PF = kWideRows * F4 / kThreads; // float4 per thread per table block
+    constexpr int VPR = D / elem<T>::kVec;        // 16-byte vectors per query row
+    constexpr int QU = 8;                         // query-row loads in flight per thread
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int unit = blockIdx.x;
+    const int bh = unit / n_q_chunks, i = unit % n_q_chunks;
+    const int b = bh / n_kv, j = bh % n_kv, r = n_q_heads / n_kv;
+    const int c = q_chunk0 + i;
+    const int gpc = 1 << gpc_shift;
+    WaveLds L = carve(smem_raw, D, kGroups ? topk : 0,
+                      kGroups && topk_groups > topk ? topk_groups : topk);
+    unsigned char* big = smem_raw + big_off;
+
+    // the middle chunks [keep_first, keep_first + n); loads past them read zeros
+    int n = c - window - keep_first;
+    if (n < 0) n = 0;
+    const float* table = chunk_sum + (static_cast<int64_t>(bh) * table_chunks + keep_first) * D;
+    const buf_rsrc t_rsrc = make_rsrc(table, static_cast<uint32_t>(n) * D * sizeof(float));
+    float4 pf[PF];
+    auto fetch_block = [&](int r0) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int x = tid + u * kThreads;
+            const uint32_t off =
+                (static_cast<uint32_t>(r0 + x / F4) * D + (x % F4) * 4) * sizeof(float);
+            pf[u] = __builtin_bit_cast(float4, buf_load16(t_rsrc, off));
+        }
+    };
+    if (n > 0) fetch_block(0);
+
+    // 1. q_bar
+    if constexpr (kQbarIn) {
+        if (tid < D / 4)
+            *reinterpret_cast<float4*>(L.q + tid * 4) =
+                *reinterpret_cast<const float4*>(qbar + static_cast<int64_t>(unit) * D + tid * 4);
+    } else {
+        constexpr int V = elem<T>::kVec;
+        const int64_t qtok = static_cast<int64_t>(n_q_chunks) * 64;
+        const T* qbase = query_chunk_base<T, D>(q_rot, b, j, i, n_q_heads, r, n_q_chunks);
+        // the r heads' 64-token slices, from the first row of head 0 to the
+        // last row of head r - 1
+        const buf_rsrc q_rsrc = make_rsrc(
+            qbase, static_cast<uint32_t>(((r - 1) * qtok + 64) * D * sizeof(T)));
+        vec16* s_rows = reinterpret_cast<vec16*>(big);
+        const int n_vec = r * 64 * VPR;
+        for (int x = tid; x < n_vec; x += kThreads * QU) {
+            vec16 t[QU];
+#pragma unroll
+            for (int u = 0; u < QU; ++u) {
+                const int y = x + u * kThreads;
+                const int row = y / VPR, cv = y % VPR;
+                t[u] = buf_load16(q_rsrc, static_cast<uint32_t>(
+                                              (((row >> 6) * qtok + (row & 63)) * D + cv * V) *
+                                              sizeof(T)));
+            }
+#pragma unroll
+            for (int u = 0; u < QU; ++u)
+                if (x + u * kThreads < n_vec) s_rows[x + u * kThreads] = t[u];
+        }
+        __syncthreads();
+        // partial sums after the staged rows, inside the same region
+        wg_mean_rows<T, D>(reinterpret_cast<const T*>(s_rows), r * 64,
+                           reinterpret_cast<float*>(s_rows + n_vec), L.q);
+        __syncthreads();
+        if (tid < D / 4)
+            *reinterpret_cast<float4*>(qbar + static_cast<int64_t>(unit) * D + tid * 4) =
+                *reinterpret_cast<const float4*>(L.q + tid * 4);
+    }
+    __syncthreads();  // q_bar in LDS; the staged rows are dead
+
+    // 2. chunk scores, a block of kWideRows table rows at a time
+    float* s_tab = reinterpret_cast<float*>(big);
+    const int qd = lane & 3;
+    const int rl = wave * 16 + (lane >> 2);  // this quad's row within a block
+    float qv[F4];
+#pragma unroll
+    for (int f = 0; f < F4; ++f) qv[f] = L.q[4 * f + qd];
+    for (int r0 = 0; r0 < n; r0 += kWideRows) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int x = tid + u * kThreads;
+            *reinterpret_cast<float4*>(s_tab + (x / F4) * TS + (x % F4) * 4) = pf[u];
+        }
+        __syncthreads();
+        if (r0 + kWideRows < n) fetch_block(r0 + kWideRows);
+#pragma unroll
+        for (int h = 0; h < kWideRows / 256; ++h) {
+            const float* row = s_tab + (h * 256 + rl) * TS + qd;
+            float a = 0.f;
+#pragma unroll
+            for (int f = 0; f < F4; ++f) a = fmaf(qv[f], row[4 * f], a);
+            a = add_quad<0xb1>(a);  // (s0 + s1), (s2 + s3)
+            a = add_quad<0x4e>(a);  // (s0 + s1) + (s2 + s3)
+            const int m = r0 + h * 256 + rl;
+            if (qd == 0 && m < n) L.keys[m] = select_key(a, keep_first + m);
+        }
+        __syncthreads();  // the block is scored before the next one is stored
+    }
+
+    // 3. top-k chunks, ascending, -1 padded (the select's histograms reuse
+    // the table region)
+    auto* S = reinterpret_cast<WgSelect<kThreads>*>(big);
+    const int k = n < topk ? n : topk;
+    int32_t* out = chunk_idx + static_cast<int64_t>(unit) * topk;
+    if (k > 0) wg_select_topk<kThreads>(L.keys, n, k, L.sel, L.scr, S);  // ids keep_first + m
+    if (wave == 0) {
+        for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
+        if constexpr (kGroups)
+            for (int t = lane; t < k; t += 64) L.list[t] = L.sel[t];
+    }
+    if constexpr (!kGroups) return;
+
+    // 4. group refinement (the chunk-only variant keeps every candidate:
+    // ascending, written without scoring)
+    const int ng = k * gpc;
+    int32_t* gout = group_idx + static_cast<int64_t>(unit) * topk_groups;
+    if (ng <= topk_groups) {
+        if (wave == 0)
+            for (int t = lane; t < topk_groups; t += 64)
+                gout[t] = t < ng ? L.sel[t >> gpc_shift] * gpc + (t & (gpc - 1)) : -1;
+        return;
+    }
+    __syncthreads();  // the chunk list is visible to every wave
+    const float* gtab = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
+    for (int m0 = wave * 16; m0 < ng; m0 += 16 * (kThreads / 64)) {
+        const int rem = ng - m0;
+        batch_keys<D, 1>(
+            L.q, gtab,
+            [&](int kk) {
+                const int m = m0 + (kk < rem ? kk : rem - 1);
+                return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1));
+            },
+            rem, L.keys + m0);
+    }
+    __syncthreads();
+    wg_select_topk<kThreads>(L.keys, ng, topk_groups, L.sel, L.scr, S);  // groups of ascending chunks
+    if (wave == 0)
+        for (int t = lane; t < topk_groups; t += 64) gout[t] = L.sel[t];
+}
+
 // Up to four waves per workgroup, as many as the LDS budget allows.
 int waves_per_block(size_t wave_bytes, int max_lds) {
     int w = static_cast<int>(static_cast<size_t>(max_lds) / wave_bytes);
@@ -348,12 +621,57 @@ inline RouteGeom route_geom(const hga_plan& plan, int n_max, bool groups) {
     return g;
 }
 
+// Launches with at most this many units route each unit with a whole
+// workgroup (route_wide_kernel); larger ones pack four units per workgroup.
+constexpr int kWideMaxUnits = 128;
+
+// LDS of route_wide_kernel: the WaveLds pieces (keys for the larger
+// candidate list), then one region (at the returned offset) for the staged
+// query rows of the chunk and then the table blocks.
+struct WideGeom {
+    size_t big_off;
+    size_t total;
+};
+
+inline WideGeom route_wide_geom(const hga_plan& plan, int n_max, bool groups, bool qbar_in) {
+    const hga_params& p = plan.p;
+    const int gpc = p.chunk / p.group;
+    const int nk = groups && p.topk_chunks * gpc > n_max ? p.topk_chunks * gpc : n_max;
+    const int ntop = groups && p.topk_groups > p.topk_chunks ? p.topk_groups : p.topk_chunks;
+    const size_t elem_bytes = p.dtype == HGA_F32 ? 4 : 2;
+    const size_t rows = qbar_in ? 0
+                                : static_cast<size_t>(p.n_q_heads / p.n_kv_heads) * p.chunk *
+                                      p.head_dim * elem_bytes;
+    const size_t part = qbar_in ? 0 : sizeof(float) * 8 * p.head_dim;  // wg_mean_rows partials
+    const size_t tab = sizeof(float) * kWideRows * (p.head_dim + 4);
+    size_t big = rows + part > tab ? rows + part : tab;
+    if (big < sizeof(WgSelect<1024>)) big = sizeof(WgSelect<1024>);
+    WideGeom g;
+    g.big_off = wave_lds_bytes(p.head_dim, groups ? p.topk_chunks : 0, ntop, nk);
+    g.total = g.big_off + align16(big);
+    return g;
+}
+
 template <typename T, int D, bool kGroups, bool kQbarIn>
 hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                           const float* chunk_sum, const float* group_sum, int table_chunks,
                           float* qbar, int32_t* chunk_idx, int32_t* group_idx, hipStream_t stream) {
     const hga_params& p = plan.p;
     const int n_max = middle_count(p, q_chunk0 + n_q_chunks - 1);
+    const int units = p.batch * p.n_kv_heads * n_q_chunks;
+    if (units <= kWideMaxUnits) {
+        const WideGeom wg = route_wide_geom(plan, n_max, kGroups, kQbarIn);
+        if (wg.total <= static_cast<size_t>(plan.max_lds)) {
+            const int gpc = p.chunk / p.group;
+            hipLaunchKernelGGL((route_wide_kernel<T, D, kGroups, kQbarIn>), dim3(units),
+                               dim3(1024), wg.total, stream, static_cast<const T*>(q_rot),
+                               q_chunk0, n_q_chunks, chunk_sum, group_sum, table_chunks, qbar,
+                               chunk_idx, group_idx, p.n_q_heads, p.n_kv_heads, p.keep_first,
+                               recent_window(p), p.topk_chunks, p.topk_groups,
+                               gpc == 8 ? 3 : (gpc == 4 ? 2 : 1), static_cast<int>(wg.big_off));
+            return hipGetLastError();
+        }
+    }
     const RouteGeom g = route_geom(plan, n_max, kGroups);
     const int upb = g.units_per_block < n_q_chunks ? g.units_per_block : n_q_chunks;
     const int blocks = p.batch * p.n_kv_heads * ((n_q_chunks + upb - 1) / upb);
