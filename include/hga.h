@@ -276,6 +276,36 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
                             const void* v_routed, const int32_t* group_idx, void* out, float* lse,
                             void* start_event, void* stop_event, void* stream);
 
+/* hga_attend for launches with few units (a decode block, one block of a
+ * block-sequential prefill), Sec. 3.4: each unit's key tiles (current chunk,
+ * visible chunks, routed rows) are divided among up to 16 workgroups, each
+ * of which leaves an unnormalised partial result (fp32 output sums, running
+ * maximum and weight sum per query row) in `workspace`; a second kernel
+ * merges them with the usual softmax rescaling.  The number of splits is
+ * chosen from the unit count, the tile count and what the workspace holds.
+ * out and lse equal hga_attend's up to fp32 summation order (the softmax is
+ * the same; its sums are formed in a different order); with one split
+ * (workspace_bytes below two splits' worth, the fp32 plan dtype, or one
+ * query head per KV head) this runs hga_attend itself, bit for bit.
+ *   workspace        device memory owned by the caller, 16-byte aligned,
+ *                    not read before it is written; NULL with
+ *                    workspace_bytes = 0 is allowed (one split)
+ *   workspace_bytes  its size; hga_attend_split_workspace gives the most
+ *                    any call with n_q_chunks query chunks uses
+ * Other arguments, layouts, requirements and errors as hga_attend.  Calls
+ * that share a workspace must not overlap in time. */
+hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const void* k_res, const void* v_res,
+                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                            void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Workspace bytes hga_attend_split uses at most for n_q_chunks query chunks
+ * (16 splits of batch x n_kv_heads x n_q_chunks units, each
+ * (n_q_heads/n_kv_heads)*chunk rows of head_dim + 2 floats).  -1 on a
+ * NULL or invalid plan or n_q_chunks < 0. */
+int64_t hga_attend_split_workspace(const hga_plan* plan, int32_t n_q_chunks);
+
 /* hga_gather_kv followed by hga_attend, for the prefill layout (resident
  * K/V indexed by token, no res_slot), as one pass: the attention copies each
  * routed group's rows straight from k_res/v_res (Sec. 4.3 gather, Sec. 3.4

@@ -13,14 +13,14 @@ struct VisibleChunks {
     int a;      // sinks [0, a)
     int start;  // recent window [start, c)
     int count;  // |D_c|
-    __device__ VisibleChunks(int c, int keep_first, int window) {
+    __host__ __device__ VisibleChunks(int c, int keep_first, int window) {
         a = keep_first < c ? keep_first : c;
         int w0 = c - window;
         if (w0 < 0) w0 = 0;
         start = w0 > a ? w0 : a;
         count = a + (c - start);
     }
-    __device__ int chunk(int idx) const { return idx < a ? idx : start + (idx - a); }
+    __host__ __device__ int chunk(int idx) const { return idx < a ? idx : start + (idx - a); }
 };
 
 // Kinds of key tiles.

@@ -434,7 +434,12 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
 // workgroups per unit the first writes K and the second V), so the call also
 // produces the gather step's output.  Otherwise the routed rows are
 // read from k_routed / v_routed.
-template <int D, int KS, int NS, int NW, bool kGather>
+// kSplit: the unit's key tiles are divided among split_div.d workgroups
+// (split s takes tiles [ceil(s T / S), ceil((s+1) T / S)) of the T tiles, so
+// split 0 holds the current chunk); each writes its unnormalised partial
+// result to `partial_ws` instead of the output, and
+// attend_combine_kernel merges them.
+template <int D, int KS, int NS, int NW, bool kGather, bool kSplit = false>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2))) void attend_mfma_kernel(
     const bf16_t* __restrict__ q_rot, int q_chunk0, int n_q_chunks,
     const bf16_t* __restrict__ k_res, const bf16_t* __restrict__ v_res, int64_t res_tokens,
@@ -442,7 +447,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     bf16_t* __restrict__ v_routed, const int32_t* __restrict__ group_idx,
     bf16_t* __restrict__ out, float* __restrict__ lse, int r, FastDiv kv_div, int group_shift,
     int keep_first, int window, int topk_groups, FastDiv wg_div, FastDiv chunk_div,
-    int n_blocks) {
+    int n_blocks, float* __restrict__ partial_ws, FastDiv split_div) {
+    static_assert(!kSplit || (KS == 1 && !kGather), "split form: one wave per query tile, no gather");
     using Lay = Layout<D, NS>;
     constexpr uint32_t kRowBytes = Lay::kRowBytes, kTileBytes = Lay::kTileBytes,
                        kStageBytes = Lay::kStageBytes;
@@ -468,8 +474,13 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     const int per_xcd = (n_blocks + kXcds - 1) / kXcds;
     const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
     if (logical >= n_blocks) return;
-    const int unit_id = wg_div.div(logical);
-    const int part = logical - unit_id * wg_div.d;
+    int item = logical, split = 0;
+    if constexpr (kSplit) {
+        item = split_div.div(logical);
+        split = logical - item * split_div.d;
+    }
+    const int unit_id = wg_div.div(item);
+    const int part = item - unit_id * wg_div.d;
     const int bh = chunk_div.div(unit_id);
     const int i = unit_id - bh * n_q_chunks;
 
@@ -529,6 +540,12 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     const int n_vis = vis.count;
     const int n_rt = (routed_rows + KT - 1) / KT;
     const int n_tiles = 1 + n_vis + n_rt;
+    int t0 = 0, t1 = n_tiles;  // this workgroup's tiles
+    if constexpr (kSplit) {
+        const int ns = split_div.d;
+        t0 = (split * n_tiles + ns - 1) / ns;
+        t1 = ((split + 1) * n_tiles + ns - 1) / ns;
+    }
     bool bad = false;
 
     // per-lane source offsets of this wave's copies inside a tile
@@ -637,11 +654,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     };
     // Tiles requested up front; with kGather a routed tile needs the group
     // ids in LDS, so one among them waits for the first barrier.
-    const int n_up = min(NS, n_tiles);
+    const int n_up = min(NS, t1 - t0);
     const int n_pre = kGather ? min(n_up, n_vis + 1) : n_up;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-        if (s < n_pre) issue(s, s);
+        if (s < n_pre) issue(t0 + s, s);
 
     f32x16_t oacc[NDT];
 #pragma unroll
@@ -657,9 +674,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     // the other tiles carry no mask work.
     auto step = [&](int tile, auto current_tag) {
         constexpr bool kCurrent = decltype(current_tag)::value;
+        const int lt = tile - t0;  // position in this workgroup's tiles
         // this wave's copies of `tile` are done once at most `ahead` later
         // tiles' copies remain in flight (loads complete in issue order)
-        const int ahead = kCurrent ? n_pre - 1 : min(NS - 2, n_tiles - 1 - tile);
+        const int ahead = lt == 0 ? n_pre - 1 : min(NS - 2, t1 - 1 - tile);
         if (NS >= 4 && ahead >= 3)
             wait_loads<(NS >= 4 ? 3 : 0) * LPT>();
         else if (NS >= 3 && ahead >= 2)
@@ -669,14 +687,14 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
         else
             wait_loads<0>();
         __syncthreads();
-        if (kCurrent) {
-            for (int s = n_pre; s < n_up; ++s) issue(s, s);
+        if (lt == 0) {
+            for (int s = n_pre; s < n_up; ++s) issue(t0 + s, s);
         } else {
-            if (kGather && tile > n_vis && (write_k || write_v)) write_routed(tile, tile % NS);
-            if (tile + NS - 1 < n_tiles) issue(tile + NS - 1, (tile + NS - 1) % NS);
+            if (kGather && tile > n_vis && (write_k || write_v)) write_routed(tile, lt % NS);
+            if (tile + NS - 1 < t1) issue(tile + NS - 1, (lt + NS - 1) % NS);
         }
 
-        const int stage = tile % NS;
+        const int stage = lt % NS;
         const bf16_t* sK = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes);
         const bf16_t* sV = reinterpret_cast<const bf16_t*>(smem + stage * kStageBytes + kTileBytes);
         const int rt_row0 = (tile - 1 - n_vis) * KT;
@@ -687,39 +705,130 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
             tile_math<D, KS, kCurrent>(sK, sV, qf, oacc, m_run, l_run, ksplit, t, partial, rt_row0,
                                        s_gid, routed_rows, topk_groups, group_shift, c * gpc);
     };
-    step(0, BoolTag<true>{});
-    for (int tile = 1; tile < n_tiles; ++tile) step(tile, BoolTag<false>{});
+    if (t0 == 0) step(0, BoolTag<true>{});
+    for (int tile = t0 > 1 ? t0 : 1; tile < t1; ++tile) step(tile, BoolTag<false>{});
 
+    if constexpr (kSplit) {
+        // Partial result of query row qrow_in_unit over this split's keys:
+        // block (unit, split) of partial_ws holds rows x D unnormalised output
+        // sums, then rows x (m, l) (m in log2 units, l the sum of the
+        // weights exp2(s - m); m = -inf, l = 0 when the split saw no key).
+        // A split with no tile never waited for its group-id copies: every
+        // LDS copy is complete before the workgroup ends.
+        wait_loads<0>();
+        if (!qactive) return;
+        const int rows = nqt * 32;
+        float* blk = partial_ws + (unit * split_div.d + split) * static_cast<int64_t>(rows) * (D + 2);
+        float* po = blk + static_cast<int64_t>(qrow_in_unit) * D;
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4)
+                *reinterpret_cast<float4*>(po + dt * 32 + g4 * 8 + half * 4) =
+                    make_float4(oacc[dt][g4 * 4], oacc[dt][g4 * 4 + 1], oacc[dt][g4 * 4 + 2],
+                                oacc[dt][g4 * 4 + 3]);
+        const float l_tot = add_xor32(l_run);
+        if (half == 0)
+            *reinterpret_cast<float2*>(blk + static_cast<int64_t>(rows) * D + 2 * qrow_in_unit) =
+                make_float2(m_run, bad ? NAN : l_tot);
+        return;
+    }
     __syncthreads();  // LDS stages are dead from here on (every copy was waited for)
     finish_rows<D, KS, QT>(oacc, m_run, l_run, reinterpret_cast<float*>(smem),
                            reinterpret_cast<float*>(smem) + QT * 64 * NDT * 16, qt_local, ksplit,
                            qactive, bad, out + qrow * D, lse ? lse + qrow : nullptr);
 }
 
-template <int D, int KS, int NS, int NW, bool kGather>
+// Merge of the split partial results: thread (row, 4 dimensions) of one
+// unit weighs split s by w_s = exp2(m_s - M), M = max_s m_s, and writes
+// out = (sum_s w_s O_s) / L and lse = (M + log2 L) ln 2, L = sum_s w_s l_s
+// (the same normalisation the single-workgroup kernel applies, with the
+// partial sums added in split order).  All of a thread's reads are issued
+// before any is used (kMaxSplit slots, the unused ones skipped).
+
+template <int D>
+__global__ __launch_bounds__(256) void attend_combine_kernel(
+    const float* __restrict__ part, int n_split, int rows, int n_units, int n_q_chunks, int n_kv,
+    int r, bf16_t* __restrict__ out, float* __restrict__ lse) {
+    constexpr int TPR = D / 4;  // threads per row
+    const int64_t gt = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t row_g = gt / TPR;
+    if (row_g >= static_cast<int64_t>(n_units) * rows) return;
+    const int d0 = static_cast<int>(gt % TPR) * 4;
+    const int unit = static_cast<int>(row_g / rows), qr = static_cast<int>(row_g % rows);
+    const int64_t blk_floats = static_cast<int64_t>(rows) * (D + 2);
+    const float* base = part + static_cast<int64_t>(unit) * n_split * blk_floats;
+    float2 ml[kMaxSplit];
+    float4 x[kMaxSplit];
+#pragma unroll
+    for (int s = 0; s < kMaxSplit; ++s) {
+        if (s < n_split) {
+            const float* blk = base + s * blk_floats;
+            ml[s] = *reinterpret_cast<const float2*>(blk + static_cast<int64_t>(rows) * D + 2 * qr);
+            x[s] = *reinterpret_cast<const float4*>(blk + static_cast<int64_t>(qr) * D + d0);
+        }
+    }
+    float m_max = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < kMaxSplit; ++s)
+        if (s < n_split) m_max = fmaxf(m_max, ml[s].x);
+    // a split that saw no key (m = -inf, l = 0) weighs exp2(-inf) = 0; M is
+    // finite (split 0 holds each row's own token)
+    float l_sum = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int s = 0; s < kMaxSplit; ++s) {
+        if (s < n_split) {
+            const float w = __builtin_amdgcn_exp2f(ml[s].x - m_max);
+            l_sum = fmaf(ml[s].y, w, l_sum);
+            o.x = fmaf(x[s].x, w, o.x);
+            o.y = fmaf(x[s].y, w, o.y);
+            o.z = fmaf(x[s].z, w, o.z);
+            o.w = fmaf(x[s].w, w, o.w);
+        }
+    }
+    const float inv = __builtin_amdgcn_rcpf(l_sum);
+    // output row: query head j*r + qr/64, token i*64 + qr%64 of the unit's chunk
+    const int bh = unit / n_q_chunks, i = unit % n_q_chunks;
+    const int b = bh / n_kv, j = bh % n_kv;
+    const int64_t qrow = (static_cast<int64_t>(b) * n_kv * r + j * r + qr / KT) *
+                             (static_cast<int64_t>(n_q_chunks) * KT) +
+                         static_cast<int64_t>(i) * KT + qr % KT;
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    bf16x4_t v;
+    v[0] = static_cast<__bf16>(o.x * inv);
+    v[1] = static_cast<__bf16>(o.y * inv);
+    v[2] = static_cast<__bf16>(o.z * inv);
+    v[3] = static_cast<__bf16>(o.w * inv);
+    *reinterpret_cast<bf16x4_t*>(out + qrow * D + d0) = v;
+    if (lse && d0 == 0) lse[qrow] = (m_max + log2f(l_sum)) * 0.6931471805599453f;
+}
+
+template <int D, int KS, int NS, int NW, bool kGather, bool kSplit = false>
 hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev_start,
                          hipEvent_t ev_stop, const bf16_t* q_rot, int q_chunk0, int n_q_chunks,
                          const bf16_t* k_res, const bf16_t* v_res, int64_t res_tokens,
                          const int32_t* res_slot, bf16_t* k_routed, bf16_t* v_routed,
                          const int32_t* group_idx, bf16_t* out, float* lse, int group_shift,
-                         int wg_per_unit, int n_items) {
+                         int wg_per_unit, int n_items, float* part = nullptr, int n_split = 1) {
     const hga_params& p = plan.p;
     constexpr uint32_t kLds = Layout<D, NS>::kBytes;
     static bool configured = false;  // per instantiation (the limit is a function attribute)
     if (!configured) {
         const hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attend_mfma_kernel<D, KS, NS, NW, kGather>),
+            reinterpret_cast<const void*>(&attend_mfma_kernel<D, KS, NS, NW, kGather, kSplit>),
             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
         if (e != hipSuccess) return e;
         configured = true;
     }
     const int grid = (n_items + kXcds - 1) / kXcds * kXcds;
-    hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW, kGather>), dim3(grid), dim3(NW * 64),
-                          kLds, stream, ev_start, ev_stop, 0, q_rot, q_chunk0, n_q_chunks, k_res,
-                          v_res, res_tokens, res_slot, k_routed, v_routed, group_idx, out, lse,
-                          p.n_q_heads / p.n_kv_heads, FastDiv(p.n_kv_heads), group_shift,
-                          p.keep_first, recent_window(p), p.topk_groups, FastDiv(wg_per_unit),
-                          FastDiv(n_q_chunks), n_items);
+    hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW, kGather, kSplit>), dim3(grid),
+                          dim3(NW * 64), kLds, stream, ev_start, ev_stop, 0, q_rot, q_chunk0,
+                          n_q_chunks, k_res, v_res, res_tokens, res_slot, k_routed, v_routed,
+                          group_idx, out, lse, p.n_q_heads / p.n_kv_heads, FastDiv(p.n_kv_heads),
+                          group_shift, p.keep_first, recent_window(p), p.topk_groups,
+                          FastDiv(wg_per_unit), FastDiv(n_q_chunks), n_items, part,
+                          FastDiv(n_split));
     return hipGetLastError();
 }
 
@@ -769,7 +878,91 @@ hipError_t launch_mfma_any(const hga_plan& plan, const void* q_rot, int q_chunk0
 #undef HGA_ARGS
 }
 
+// Split form (GQA configurations, r >= 2): the launch shape of
+// launch_mfma_any, each workgroup repeated for n_split key ranges, then the
+// merge.  `part` holds units x n_split x rows x (D + 2) floats.
+hipError_t launch_split_any(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                            int n_q_chunks, const void* k_res, const void* v_res,
+                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                            float* part, int n_split, hipStream_t stream) {
+    const hga_params& p = plan.p;
+    const int r = p.n_q_heads / p.n_kv_heads;
+    const int qt_per_wg = p.head_dim == 128 ? kD128Waves : 4;
+    const int wg_per_unit = (2 * r + qt_per_wg - 1) / qt_per_wg;
+    const int n_units = p.batch * p.n_kv_heads * n_q_chunks;
+    const int n_items = n_units * wg_per_unit * n_split;
+    const int group_shift = p.group == 8 ? 3 : (p.group == 16 ? 4 : 5);
+    const bf16_t* q = static_cast<const bf16_t*>(q_rot);
+    const bf16_t* kr = static_cast<const bf16_t*>(k_res);
+    const bf16_t* vr = static_cast<const bf16_t*>(v_res);
+    bf16_t* kt = const_cast<bf16_t*>(static_cast<const bf16_t*>(k_routed));
+    bf16_t* vt = const_cast<bf16_t*>(static_cast<const bf16_t*>(v_routed));
+    bf16_t* o = static_cast<bf16_t*>(out);
+    hipError_t e;
+    if (p.head_dim == 64)
+        e = launch_mfma_t<64, 1, 2, 4, false, true>(
+            plan, stream, nullptr, nullptr, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot,
+            kt, vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, part, n_split);
+    else
+        e = launch_mfma_t<128, 1, kD128Stages, kD128Waves, false, true>(
+            plan, stream, nullptr, nullptr, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot,
+            kt, vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, part, n_split);
+    if (e != hipSuccess) return e;
+    const int rows = 64 * r;
+    const int64_t threads = static_cast<int64_t>(n_units) * rows * (p.head_dim / 4);
+    const int blocks = static_cast<int>((threads + 255) / 256);
+    if (p.head_dim == 64)
+        hipLaunchKernelGGL((attend_combine_kernel<64>), dim3(blocks), dim3(256), 0, stream, part,
+                           n_split, rows, n_units, n_q_chunks, p.n_kv_heads, r, o, lse);
+    else
+        hipLaunchKernelGGL((attend_combine_kernel<128>), dim3(blocks), dim3(256), 0, stream, part,
+                           n_split, rows, n_units, n_q_chunks, p.n_kv_heads, r, o, lse);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks) {
+    const hga_params& p = plan.p;
+    const int64_t rows = 64 * (p.n_q_heads / p.n_kv_heads);
+    return static_cast<int64_t>(p.batch) * p.n_kv_heads * n_q_chunks * rows * (p.head_dim + 2) *
+           static_cast<int64_t>(sizeof(float));
+}
+
+hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                               int n_q_chunks, const void* k_res, const void* v_res,
+                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                               const void* v_routed, const int32_t* group_idx, void* out,
+                               float* lse, void* workspace, int64_t workspace_bytes,
+                               hipStream_t stream) {
+    const hga_params& p = plan.p;
+    const int r = p.n_q_heads / p.n_kv_heads;
+    int n_split = 1;
+    if (p.dtype == HGA_BF16 && r >= 2) {
+        // enough workgroups to give every compute unit one, at least two key
+        // tiles per split, at most what the workspace holds
+        const int qt_per_wg = p.head_dim == 128 ? kD128Waves : 4;
+        const int wg_per_unit = (2 * r + qt_per_wg - 1) / qt_per_wg;
+        const int64_t items = static_cast<int64_t>(p.batch) * p.n_kv_heads * n_q_chunks * wg_per_unit;
+        const int c_last = q_chunk0 + n_q_chunks - 1;
+        const int n_rt = (p.topk_groups * p.group + KT - 1) / KT;
+        const int n_tiles = 1 + VisibleChunks(c_last, p.keep_first, recent_window(p)).count + n_rt;
+        int64_t want = (plan.n_cu + items - 1) / items;
+        want = want < (n_tiles + 1) / 2 ? want : (n_tiles + 1) / 2;
+        want = want < kMaxSplit ? want : kMaxSplit;
+        const int64_t per = attend_split_bytes_per_split(plan, n_q_chunks);
+        const int64_t fit = per > 0 ? workspace_bytes / per : 0;
+        n_split = static_cast<int>(want < fit ? want : fit);
+    }
+    if (n_split <= 1)
+        return launch_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                             res_slot, k_routed, v_routed, group_idx, out, lse, nullptr, nullptr,
+                             stream);
+    return launch_split_any(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                            k_routed, v_routed, group_idx, out, lse,
+                            static_cast<float*>(workspace), n_split, stream);
+}
 
 hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,
                               int n_q_chunks, const void* k_res, const void* v_res,

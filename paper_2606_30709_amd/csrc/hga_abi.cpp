@@ -502,6 +502,35 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
                     "hga_attend launch");
 }
 
+int64_t hga_attend_split_workspace(const hga_plan* plan, int32_t n_q_chunks) {
+    if (check_plan(plan) != HGA_OK || n_q_chunks < 0) return -1;
+    return hga::kMaxSplit * hga::attend_split_bytes_per_split(*plan, n_q_chunks);
+}
+
+hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                            int32_t n_q_chunks, const void* k_res, const void* v_res,
+                            int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                            const void* v_routed, const int32_t* group_idx, void* out, float* lse,
+                            void* workspace, int64_t workspace_bytes, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0 || workspace_bytes < 0)
+        return fail(HGA_EINVAL,
+                    "q_chunk0, n_q_chunks, res_tokens and workspace_bytes must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                         k_routed, v_routed, group_idx, out, lse));
+    if (workspace_bytes > 0) {
+        if (!workspace) return fail(HGA_EINVAL, "workspace is NULL with workspace_bytes > 0");
+        if (!aligned(workspace, 16)) return fail(HGA_EALIGN, "workspace is not 16-byte aligned");
+    }
+    clear_stale_error();
+    return launched(hga::launch_attend_split(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+                                             res_tokens, res_slot, k_routed, v_routed, group_idx,
+                                             out, lse, workspace, workspace ? workspace_bytes : 0,
+                                             static_cast<hipStream_t>(stream)),
+                    "hga_attend_split launch");
+}
+
 hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                              int32_t n_q_chunks, const void* k_res, const void* v_res,
                              int64_t res_tokens, const int32_t* group_idx, void* k_routed,

@@ -78,6 +78,19 @@ hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, 
                          const int32_t* group_idx, void* out, float* lse, hipEvent_t start,
                          hipEvent_t stop, hipStream_t stream);
 
+// Attention with each unit's key tiles divided among several workgroups
+// (bf16, r >= 2) whose partial results go to `workspace` and are merged by a
+// second kernel; other configurations, or a workspace too small for two
+// splits, run launch_attend.
+constexpr int kMaxSplit = 16;  // at most the merge kernel's slots
+int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks);
+hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                               int n_q_chunks, const void* k_res, const void* v_res,
+                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                               const void* v_routed, const int32_t* group_idx, void* out,
+                               float* lse, void* workspace, int64_t workspace_bytes,
+                               hipStream_t stream);
+
 // The gather of the routed rows fused into the attention (prefill layout:
 // resident K/V indexed by token, no slot map); writes k_routed / v_routed as
 // launch_gather_kv does.  start/stop as for launch_attend.

@@ -18,8 +18,9 @@ __all__ = [
     "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
-    "hga_attend_timed", "hga_gather_attend", "hga_block_step", "hga_prefill_blocks",
-    "hga_status_string", "hga_last_error", "hga_version", "EXPORTED_SYMBOLS",
+    "hga_attend_timed", "hga_attend_split", "hga_attend_split_workspace", "hga_gather_attend",
+    "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error",
+    "hga_version", "EXPORTED_SYMBOLS",
 ]
 
 F32, BF16 = 0, 1
@@ -28,8 +29,9 @@ _TORCH_DTYPE = {F32: torch.float32, BF16: torch.bfloat16}
 EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
-    "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_gather_attend",
-    "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error", "hga_version",
+    "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_attend_split",
+    "hga_attend_split_workspace", "hga_gather_attend", "hga_block_step", "hga_prefill_blocks",
+    "hga_status_string", "hga_last_error", "hga_version",
 )
 
 
@@ -82,6 +84,8 @@ def library() -> ctypes.CDLL:
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
+            "hga_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, i64,
+                                 vp],
             "hga_gather_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp],
             "hga_block_step": [vp, vp, i32, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp, vp,
                                vp, vp],
@@ -92,6 +96,8 @@ def library() -> ctypes.CDLL:
             fn = getattr(lib, name)
             fn.argtypes = args
             fn.restype = i32
+        lib.hga_attend_split_workspace.argtypes = [vp, i32]
+        lib.hga_attend_split_workspace.restype = i64
         lib.hga_status_string.argtypes = [i32]
         lib.hga_status_string.restype = ctypes.c_char_p
         lib.hga_last_error.argtypes = []
@@ -273,6 +279,27 @@ def hga_attend_timed(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v
         plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
         _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
         start_event.cuda_event, stop_event.cuda_event, _stream(stream)))
+
+
+def hga_attend_split_workspace(plan: Plan, n_q_chunks: int) -> int:
+    """Bytes of workspace hga_attend_split uses at most for n_q_chunks chunks."""
+    n = library().hga_attend_split_workspace(plan.handle, n_q_chunks)
+    if n < 0:
+        raise HgaError(-1, "hga_attend_split_workspace: invalid plan or n_q_chunks")
+    return n
+
+
+def hga_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v_routed,
+                     group_idx, out, workspace, lse=None, res_slot=None, stream=None):
+    """hga_attend with each unit's key tiles spread over several workgroups;
+    workspace: a device tensor (any dtype) of at least
+    hga_attend_split_workspace bytes for the most splits, or None."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(library().hga_attend_split(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
+        _ptr(workspace), nbytes, _stream(stream)))
 
 
 def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx, k_routed,

@@ -157,7 +157,7 @@ class DecodePipeline:
     """One query block (the last chunk of the workload) after a host-resident history."""
 
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 fused_route: bool = True):
+                 fused_route: bool = True, split_attend: bool = True):
         assert w.decode_block
         self.w = w
         self.fused_route = fused_route
@@ -196,6 +196,13 @@ class DecodePipeline:
         self.v_routed = torch.empty_like(self.k_routed)
         self.out = torch.empty_like(self.q)
         self.lse = torch.empty(B, w.n_q_heads, C, dtype=f32, device=device)
+        # The block's four units would leave most of the chip idle in one
+        # workgroup each: hga_attend_split spreads their key tiles (its
+        # partial results live in this workspace, allocated once).
+        self.attend_ws = None
+        if split_attend:
+            nbytes = hga.hga_attend_split_workspace(self.plan, 1)
+            self.attend_ws = torch.empty((nbytes + 3) // 4, dtype=f32, device=device)
         # The history's summaries were appended as its chunks closed; build
         # them once here from a transient device copy of the history keys.
         k_dev = self.k_hist.to(device)
@@ -223,6 +230,11 @@ class DecodePipeline:
                           self.k_routed, self.v_routed, src_on_host=True, stream=stream)
 
     def attend(self, stream=None):
+        if self.attend_ws is not None:
+            hga.hga_attend_split(self.plan, self.q, self.c, self.k_res, self.v_res,
+                                 self.k_routed, self.v_routed, self.group_idx, self.out,
+                                 self.attend_ws, self.lse, res_slot=self.res_slot, stream=stream)
+            return
         hga.hga_attend(self.plan, self.q, self.c, self.k_res, self.v_res, self.k_routed,
                        self.v_routed, self.group_idx, self.out, self.lse,
                        res_slot=self.res_slot, stream=stream)

@@ -325,6 +325,83 @@ def test_gather_attend_equals_separate_calls(hga, key):
     _gather_attend_both_ways(hga, pipe.plan, w, q_blk, c0, pipe.k, pipe.v, gi_blk)
 
 
+SPLIT_CASES = {k: SMALL[k] for k in ("qwen_4k_ragged", "qwen_g8", "qwen_g32", "gqa3_d64",
+                                     "mha_d128", "f32_d128_gqa")}
+
+
+@pytest.mark.parametrize("key", list(SPLIT_CASES))
+def test_attend_split_matches_oracle(hga, key):
+    """hga_attend_split computes the same softmax as hga_attend with its
+    partial sums (and the bf16 rounding of its weights, taken against each
+    split's own reference point) in another order: its outputs meet the
+    oracle bar on single query chunks (the first ones have padded routing, so
+    some splits see only masked rows), on a multi-chunk block and with planted
+    invalid group ids; where it runs as one split (fp32, one head per KV
+    head, a workspace too small for two, none) it is hga_attend bit for bit."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SPLIT_CASES[key]
+    _say(f"[attend-split] {key}")
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp, gather_mode="separate")
+    pipe.step()
+    plan, C, r = pipe.plan, w.chunk, w.gqa_ratio
+    q64, k64, v64 = (f64(inp[x], w.dtype) for x in "qkv")
+    nbytes = hga.hga_attend_split_workspace(plan, 3)
+    ws = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+
+    def run(c0, n, gi, split, workspace=ws):
+        q = pipe.q[:, :, c0 * C:(c0 + n) * C].contiguous()
+        kr = pipe.k_routed[:, :, c0:c0 + n].contiguous()
+        vr = pipe.v_routed[:, :, c0:c0 + n].contiguous()
+        out = torch.full_like(q, float("nan"))
+        lse = torch.full(q.shape[:3], float("nan"), device="cuda")
+        if split:
+            hga.hga_attend_split(plan, q, c0, pipe.k, pipe.v, kr, vr, gi, out, workspace, lse)
+        else:
+            hga.hga_attend(plan, q, c0, pipe.k, pipe.v, kr, vr, gi, out, lse)
+        torch.cuda.synchronize()
+        return out, lse
+
+    def check(c0, n, gi_np):
+        gi = torch.from_numpy(np.ascontiguousarray(gi_np[:, :, c0:c0 + n])).cuda()
+        out, lse = run(c0, n, gi, True)
+        units = [(b, j, c) for b in range(w.batch) for j in range(w.n_kv_heads)
+                 for c in range(c0, c0 + n)]
+        # the calls treat an id outside [0, c * C / G) as an absent slot (the
+        # routing never produces one); the oracle is given -1 there
+        lim = (np.arange(w.n_chunks) * (C // w.group))[None, None, :, None]
+        gi_ref = np.where((gi_np >= 0) & (gi_np < lim), gi_np, -1)
+        o_ref, l_ref = O.attend(q64, k64, v64, gi_ref, list(range(w.n_chunks)), C, w.group,
+                                w.keep_first, w.keep_last, w.force_prev, units=units)
+        ts = slice(c0 * C, (c0 + n) * C)
+        eo = np.max(np.abs(tensor_to_f64(out) - o_ref[:, :, ts]))
+        el = np.max(np.abs(tensor_to_f64(lse) - l_ref[:, :, ts]))
+        po, pl = run(c0, n, gi, False)
+        gap = float((po.float() - out.float()).abs().max())
+        _say(f"  chunks {c0}..{c0 + n - 1}: out {eo:.3g} lse {el:.3g} (vs hga_attend {gap:.3g})")
+        assert eo <= OUT_TOL[w.dtype] and el <= LSE_TOL[w.dtype]
+        return out, lse, po, pl
+
+    gi_np = pipe.group_idx.cpu().numpy()
+    for c in sorted({0, 1, 2, 3, w.n_chunks // 2, w.n_chunks - 1}):
+        out, lse, po, pl = check(c, 1, gi_np)
+        if not (w.dtype == "bf16" and r >= 2):
+            assert torch.equal(_bits(out), _bits(po)) and torch.equal(lse, pl)
+    check(w.n_chunks // 3, 3, gi_np)
+    planted = gi_np.copy()
+    c = w.n_chunks - 1
+    planted[0, 0, c, 0] = -1
+    planted[0, w.n_kv_heads - 1, c, w.topk_groups - 1] = 10 ** 6
+    check(c, 1, planted)
+    # a workspace below two splits' worth (one split of one chunk is
+    # nbytes / 48 bytes), or none: hga_attend itself
+    gi = pipe.group_idx[:, :, c:c + 1].contiguous()
+    po, pl = run(c, 1, gi, False)
+    for small in (ws[: nbytes // 96 - 1], None):
+        out, lse = run(c, 1, gi, True, workspace=small)
+        assert torch.equal(_bits(out), _bits(po)) and torch.equal(lse, pl)
+
+
 def test_gather_attend_full_size(hga):
     """The fused call equals the two calls at the full prefill sizes."""
     from paper_2606_30709_amd.pipeline import PrefillPipeline
