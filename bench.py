@@ -296,7 +296,8 @@ def blockwise_bench(w, inp, args):
     import torch
 
     from paper_2606_30709_amd.pipeline import BlockPrefillPipeline
-    pipe = BlockPrefillPipeline(w, inp)
+    split = not args.block_exact
+    pipe = BlockPrefillPipeline(w, inp, split_attend=split)
     for _ in range(args.warmup):
         pipe.step()
     torch.cuda.synchronize()
@@ -317,7 +318,8 @@ def blockwise_bench(w, inp, args):
                                 f"{w.dtype}, {w.n_chunks} blocks of {w.chunk} tokens"),
                    "seed": inp["seed"]},
         "us_per_block": round(dt * 1e6 / w.n_chunks, 2),
-        "launches_per_block": 3,
+        "attention": "split (hga_gather_attend_split)" if split else "hga_gather_attend",
+        "launches_per_block": 4 if split else 3,
     }
     print(json.dumps(res), flush=True)
 
@@ -343,6 +345,9 @@ def main():
                     help="fused: hga_gather_attend (the attention stages the routed rows and "
                          "writes the routed buffers); separate: hga_gather_kv + hga_attend "
                          "(identical results)")
+    ap.add_argument("--block-exact", action="store_true",
+                    help="with --blockwise: the single-workgroup attention whose outputs are "
+                         "bit-identical to the bulk prefill's (default: the split attention)")
     ap.add_argument("--blockwise", action="store_true",
                     help="time the block-sequential prefill (hga_prefill_blocks) instead")
     ap.add_argument("--probe-traffic", action="store_true",

@@ -306,6 +306,37 @@ hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_c
  * NULL or invalid plan or n_q_chunks < 0. */
 int64_t hga_attend_split_workspace(const hga_plan* plan, int32_t n_q_chunks);
 
+/* hga_gather_kv followed by hga_attend_split, as one pass, for any layout
+ * (Sec. 4.3 gather, Sec. 3.4 attention): the workgroups of a unit's routed
+ * tiles copy the routed groups' rows straight from k_src/v_src (rows
+ * g*group .. g*group+group-1 of group g, zeros for a padded or future id)
+ * while those of its visible tiles already compute, and the staged rows are
+ * written to k_routed/v_routed.  With the history in pinned host memory
+ * (src_on_host = 1: a decode block) the copies over the host link overlap
+ * the attention of the resident chunks instead of preceding it.
+ * k_routed, v_routed, out and lse receive exactly what
+ *   hga_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_src, v_src,
+ *                 src_tokens, src_on_host, k_routed, v_routed, stream);
+ *   hga_attend_split(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+ *                    res_tokens, res_slot, k_routed, v_routed, group_idx,
+ *                    out, lse, workspace, workspace_bytes, stream);
+ * writes (the same split count: it depends only on the plan, the chunk
+ * range and workspace_bytes).
+ *   k_src, v_src  [batch, n_kv_heads, src_tokens, head_dim] plan dtype;
+ *                 src_tokens >= (q_chunk0 + n_q_chunks - 1) * chunk (the
+ *                 causal past of the last query chunk), else HGA_EINVAL
+ *   src_on_host   0: device memory; 1: pinned, mapped host memory
+ *                 (hipHostMalloc), read through its device mapping
+ * Other arguments as hga_gather_kv and hga_attend_split; k_routed/v_routed
+ * must not overlap any input. */
+hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                                   int32_t n_q_chunks, const void* k_res, const void* v_res,
+                                   int64_t res_tokens, const int32_t* res_slot,
+                                   const void* k_src, const void* v_src, int64_t src_tokens,
+                                   int32_t src_on_host, const int32_t* group_idx, void* k_routed,
+                                   void* v_routed, void* out, float* lse, void* workspace,
+                                   int64_t workspace_bytes, void* stream);
+
 /* hga_gather_kv followed by hga_attend, for the prefill layout (resident
  * K/V indexed by token, no res_slot), as one pass: the attention copies each
  * routed group's rows straight from k_res/v_res (Sec. 4.3 gather, Sec. 3.4
@@ -347,12 +378,21 @@ hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_
  *                rows of chunks < c are read, the rows of chunk c written
  *   qbar, chunk_idx, group_idx, k_routed, v_routed, out, lse  the outputs of
  *                the three calls for one query chunk ([.., 1, ..] shapes)
+ *   workspace, workspace_bytes  NULL and 0: the attention is hga_gather_attend
+ *                as above (outputs bit-identical to the bulk prefill's);
+ *                otherwise it is hga_gather_attend_split with this workspace
+ *                (k_src = k_res, device memory): the block's few units spread
+ *                over more workgroups, out and lse equal to the bulk prefill's
+ *                up to the split's summation order (routing, summaries and the
+ *                routed buffers still bit-identical).  Owned by the caller;
+ *                hga_attend_split_workspace(plan, 1) bytes give the most splits.
  * Errors: those of the three calls. */
 hga_status hga_block_step(const hga_plan* plan, const void* q_block, int32_t c,
                           const void* k_res, const void* v_res, int64_t res_tokens,
                           float* chunk_sum, float* group_sum, int32_t table_chunks, float* qbar,
                           int32_t* chunk_idx, int32_t* group_idx, void* k_routed, void* v_routed,
-                          void* out, float* lse, void* stream);
+                          void* out, float* lse, void* workspace, int64_t workspace_bytes,
+                          void* stream);
 
 /* A block-sequential prefill of blocks 0 .. n_blocks-1: hga_block_step for
  * c = 0, 1, ... in order, all enqueued on `stream`.  Block c reads and
@@ -368,13 +408,14 @@ hga_status hga_block_step(const hga_plan* plan, const void* q_block, int32_t c,
  * blocks close.  Every block's outputs equal what the bulk prefill
  * (hga_build_summaries, then hga_route and hga_gather_attend over all chunks)
  * writes for the same query chunk.  Arguments are checked before the first
- * launch; an error returned by a later launch leaves the earlier blocks done. */
+ * launch; an error returned by a later launch leaves the earlier blocks done.
+ * workspace / workspace_bytes as for hga_block_step. */
 hga_status hga_prefill_blocks(const hga_plan* plan, const void* q_blocks, int32_t n_blocks,
                               const void* k_res, const void* v_res, int64_t res_tokens,
                               float* chunk_sum, float* group_sum, int32_t table_chunks,
                               float* qbar, int32_t* chunk_idx, int32_t* group_idx,
                               void* k_routed, void* v_routed, void* out, float* lse,
-                              void* stream);
+                              void* workspace, int64_t workspace_bytes, void* stream);
 
 /* Static description of a status code (never NULL). */
 const char* hga_status_string(int32_t status);

@@ -434,21 +434,25 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
 // workgroups per unit the first writes K and the second V), so the call also
 // produces the gather step's output.  Otherwise the routed rows are
 // read from k_routed / v_routed.
+// With kGather the routed rows come from k_src / v_src (src_tokens rows per
+// head: the resident K/V itself for the prefill layout, or the history in
+// pinned host memory, read through its device mapping, for a decode block).
 // kSplit: the unit's key tiles are divided among split_div.d workgroups
 // (split s takes tiles [ceil(s T / S), ceil((s+1) T / S)) of the T tiles, so
 // split 0 holds the current chunk); each writes its unnormalised partial
 // result to `partial_ws` instead of the output, and
 // attend_combine_kernel merges them.
 template <int D, int KS, int NS, int NW, bool kGather, bool kSplit = false>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 2))) void attend_mfma_kernel(
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64 && !kSplit ? 4 : 2))) void attend_mfma_kernel(
     const bf16_t* __restrict__ q_rot, int q_chunk0, int n_q_chunks,
     const bf16_t* __restrict__ k_res, const bf16_t* __restrict__ v_res, int64_t res_tokens,
     const int32_t* __restrict__ res_slot, bf16_t* __restrict__ k_routed,
     bf16_t* __restrict__ v_routed, const int32_t* __restrict__ group_idx,
     bf16_t* __restrict__ out, float* __restrict__ lse, int r, FastDiv kv_div, int group_shift,
     int keep_first, int window, int topk_groups, FastDiv wg_div, FastDiv chunk_div,
-    int n_blocks, float* __restrict__ partial_ws, FastDiv split_div) {
-    static_assert(!kSplit || (KS == 1 && !kGather), "split form: one wave per query tile, no gather");
+    int n_blocks, float* __restrict__ partial_ws, FastDiv split_div,
+    const bf16_t* __restrict__ k_src, const bf16_t* __restrict__ v_src, int64_t src_tokens) {
+    static_assert(!kSplit || KS == 1, "split form: one wavefront per query tile");
     using Lay = Layout<D, NS>;
     constexpr uint32_t kRowBytes = Lay::kRowBytes, kTileBytes = Lay::kTileBytes,
                        kStageBytes = Lay::kStageBytes;
@@ -505,6 +509,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
                                     static_cast<uint32_t>(res_chunks * kTileBytes));
     const u32x4 rv_res = rsrc_words(v_res + static_cast<int64_t>(bh) * res_tokens * D,
                                     static_cast<uint32_t>(res_chunks * kTileBytes));
+    const u32x4 rk_src = rsrc_words(k_src + static_cast<int64_t>(bh) * src_tokens * D,
+                                    static_cast<uint32_t>(src_tokens * kRowBytes));
+    const u32x4 rv_src = rsrc_words(v_src + static_cast<int64_t>(bh) * src_tokens * D,
+                                    static_cast<uint32_t>(src_tokens * kRowBytes));
     const u32x4 rk_rt = rsrc_words(k_routed + unit * routed_rows * D, routed_rows * kRowBytes);
     const u32x4 rv_rt = rsrc_words(v_routed + unit * routed_rows * D, routed_rows * kRowBytes);
 
@@ -607,10 +615,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
             }
 #pragma unroll
             for (int u = 0; u < KI; ++u)
-                copy16_to_lds(rk_res, sk_off[u], sk + (u * NW + wave) * 1024);
+                copy16_to_lds(rk_src, sk_off[u], sk + (u * NW + wave) * 1024);
 #pragma unroll
             for (int u = 0; u < KI; ++u)
-                copy16_to_lds(rv_res, sv_off[u], sk + kTileBytes + (u * NW + wave) * 1024);
+                copy16_to_lds(rv_src, sv_off[u], sk + kTileBytes + (u * NW + wave) * 1024);
             return;
         }
         const u32x4 rk = routed ? rk_rt : rk_res;
@@ -653,9 +661,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
         }
     };
     // Tiles requested up front; with kGather a routed tile needs the group
-    // ids in LDS, so one among them waits for the first barrier.
+    // ids in LDS, so those among them wait for the first barrier (all of
+    // them when a split starts among the routed tiles).
     const int n_up = min(NS, t1 - t0);
-    const int n_pre = kGather ? min(n_up, n_vis + 1) : n_up;
+    const int n_pre = kGather ? max(0, min(n_up, n_vis + 1 - t0)) : n_up;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
         if (s < n_pre) issue(t0 + s, s);
@@ -677,20 +686,28 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
         const int lt = tile - t0;  // position in this workgroup's tiles
         // this wave's copies of `tile` are done once at most `ahead` later
         // tiles' copies remain in flight (loads complete in issue order)
-        const int ahead = lt == 0 ? n_pre - 1 : min(NS - 2, t1 - 1 - tile);
-        if (NS >= 4 && ahead >= 3)
-            wait_loads<(NS >= 4 ? 3 : 0) * LPT>();
-        else if (NS >= 3 && ahead >= 2)
-            wait_loads<(NS >= 3 ? 2 : 0) * LPT>();
-        else if (ahead >= 1)
-            wait_loads<LPT>();
-        else
-            wait_loads<0>();
+        auto wait_ahead = [&](int ahead) {
+            if (NS >= 4 && ahead >= 3)
+                wait_loads<(NS >= 4 ? 3 : 0) * LPT>();
+            else if (NS >= 3 && ahead >= 2)
+                wait_loads<(NS >= 3 ? 2 : 0) * LPT>();
+            else if (ahead >= 1)
+                wait_loads<LPT>();
+            else
+                wait_loads<0>();
+        };
+        wait_ahead(lt == 0 ? n_pre - 1 : min(NS - 2, t1 - 1 - tile));
         __syncthreads();
+        const bool write = kGather && tile > n_vis && (write_k || write_v);
         if (lt == 0) {
             for (int s = n_pre; s < n_up; ++s) issue(t0 + s, s);
+            if (kGather && n_pre == 0) {  // nothing was in flight: wait for this tile now
+                wait_ahead(n_up - 1);
+                __syncthreads();
+            }
+            if (write) write_routed(tile, lt % NS);
         } else {
-            if (kGather && tile > n_vis && (write_k || write_v)) write_routed(tile, lt % NS);
+            if (write) write_routed(tile, lt % NS);
             if (tile + NS - 1 < t1) issue(tile + NS - 1, (lt + NS - 1) % NS);
         }
 
@@ -810,8 +827,15 @@ hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev
                          const bf16_t* k_res, const bf16_t* v_res, int64_t res_tokens,
                          const int32_t* res_slot, bf16_t* k_routed, bf16_t* v_routed,
                          const int32_t* group_idx, bf16_t* out, float* lse, int group_shift,
-                         int wg_per_unit, int n_items, float* part = nullptr, int n_split = 1) {
+                         int wg_per_unit, int n_items, float* part = nullptr, int n_split = 1,
+                         const bf16_t* k_src = nullptr, const bf16_t* v_src = nullptr,
+                         int64_t src_tokens = 0) {
     const hga_params& p = plan.p;
+    if (!k_src) {  // routed rows (kGather) from the resident K/V
+        k_src = k_res;
+        v_src = v_res;
+        src_tokens = res_tokens;
+    }
     constexpr uint32_t kLds = Layout<D, NS>::kBytes;
     static bool configured = false;  // per instantiation (the limit is a function attribute)
     if (!configured) {
@@ -828,7 +852,7 @@ hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev
                           group_idx, out, lse, p.n_q_heads / p.n_kv_heads, FastDiv(p.n_kv_heads),
                           group_shift, p.keep_first, recent_window(p), p.topk_groups,
                           FastDiv(wg_per_unit), FastDiv(n_q_chunks), n_items, part,
-                          FastDiv(n_split));
+                          FastDiv(n_split), k_src, v_src, src_tokens);
     return hipGetLastError();
 }
 
@@ -845,7 +869,8 @@ hipError_t launch_mfma_any(const hga_plan& plan, const void* q_rot, int q_chunk0
                            const void* k_res, const void* v_res, int64_t res_tokens,
                            const int32_t* res_slot, void* k_routed, void* v_routed,
                            const int32_t* group_idx, void* out, float* lse, hipEvent_t ev_start,
-                           hipEvent_t ev_stop, hipStream_t stream) {
+                           hipEvent_t ev_stop, hipStream_t stream, const void* k_src = nullptr,
+                           const void* v_src = nullptr, int64_t src_tokens = 0) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int nqt = 2 * r;
@@ -866,9 +891,11 @@ hipError_t launch_mfma_any(const hga_plan& plan, const void* q_rot, int q_chunk0
     bf16_t* kt = static_cast<bf16_t*>(k_routed);
     bf16_t* vt = static_cast<bf16_t*>(v_routed);
     bf16_t* o = static_cast<bf16_t*>(out);
+    const bf16_t* ks = static_cast<const bf16_t*>(k_src);
+    const bf16_t* vs = static_cast<const bf16_t*>(v_src);
 #define HGA_ARGS                                                                                 \
     plan, stream, ev_start, ev_stop, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot, kt, \
-        vt, group_idx, o, lse, group_shift, wg_per_unit, n_items
+        vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, nullptr, 1, ks, vs, src_tokens
     if (p.head_dim == 64) {
         if (one_head) return launch_mfma_t<64, 2, 2, 4, kGather>(HGA_ARGS);
         return launch_mfma_t<64, 1, 2, 4, kGather>(HGA_ARGS);
@@ -880,12 +907,16 @@ hipError_t launch_mfma_any(const hga_plan& plan, const void* q_rot, int q_chunk0
 
 // Split form (GQA configurations, r >= 2): the launch shape of
 // launch_mfma_any, each workgroup repeated for n_split key ranges, then the
-// merge.  `part` holds units x n_split x rows x (D + 2) floats.
+// merge.  `part` holds units x n_split x rows x (D + 2) floats.  kGather:
+// routed rows from k_src / v_src, written to k_routed / v_routed.
+template <bool kGather>
 hipError_t launch_split_any(const hga_plan& plan, const void* q_rot, int q_chunk0,
                             int n_q_chunks, const void* k_res, const void* v_res,
                             int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                             const void* v_routed, const int32_t* group_idx, void* out, float* lse,
-                            float* part, int n_split, hipStream_t stream) {
+                            float* part, int n_split, hipStream_t stream,
+                            const void* k_src = nullptr, const void* v_src = nullptr,
+                            int64_t src_tokens = 0) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int qt_per_wg = p.head_dim == 128 ? kD128Waves : 4;
@@ -899,15 +930,19 @@ hipError_t launch_split_any(const hga_plan& plan, const void* q_rot, int q_chunk
     bf16_t* kt = const_cast<bf16_t*>(static_cast<const bf16_t*>(k_routed));
     bf16_t* vt = const_cast<bf16_t*>(static_cast<const bf16_t*>(v_routed));
     bf16_t* o = static_cast<bf16_t*>(out);
+    const bf16_t* ks = static_cast<const bf16_t*>(k_src);
+    const bf16_t* vs = static_cast<const bf16_t*>(v_src);
     hipError_t e;
     if (p.head_dim == 64)
-        e = launch_mfma_t<64, 1, 2, 4, false, true>(
+        e = launch_mfma_t<64, 1, 2, 4, kGather, true>(
             plan, stream, nullptr, nullptr, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot,
-            kt, vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, part, n_split);
+            kt, vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, part, n_split, ks, vs,
+            src_tokens);
     else
-        e = launch_mfma_t<128, 1, kD128Stages, kD128Waves, false, true>(
+        e = launch_mfma_t<128, 1, kD128Stages, kD128Waves, kGather, true>(
             plan, stream, nullptr, nullptr, q, q_chunk0, n_q_chunks, kr, vr, res_tokens, res_slot,
-            kt, vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, part, n_split);
+            kt, vt, group_idx, o, lse, group_shift, wg_per_unit, n_items, part, n_split, ks, vs,
+            src_tokens);
     if (e != hipSuccess) return e;
     const int rows = 64 * r;
     const int64_t threads = static_cast<int64_t>(n_units) * rows * (p.head_dim / 4);
@@ -923,6 +958,13 @@ hipError_t launch_split_any(const hga_plan& plan, const void* q_rot, int q_chunk
 
 }  // namespace
 
+hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                              int n_q_chunks, const void* k_res, const void* v_res,
+                              int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                              const void* v_routed, const int32_t* group_idx, void* out,
+                              float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
+                              hipStream_t stream);
+
 int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks) {
     const hga_params& p = plan.p;
     const int64_t rows = 64 * (p.n_q_heads / p.n_kv_heads);
@@ -930,12 +972,12 @@ int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks) {
            static_cast<int64_t>(sizeof(float));
 }
 
-hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
-                               int n_q_chunks, const void* k_res, const void* v_res,
-                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
-                               const void* v_routed, const int32_t* group_idx, void* out,
-                               float* lse, void* workspace, int64_t workspace_bytes,
-                               hipStream_t stream) {
+// Splits for a launch of n_q_chunks query chunks from q_chunk0: enough
+// workgroups to give every compute unit one, at least two key tiles per
+// split, at most what the workspace holds; 1 where the split form does not
+// apply (fp32, one query head per KV head).
+static int choose_splits(const hga_plan& plan, int q_chunk0, int n_q_chunks,
+                         int64_t workspace_bytes) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     int n_split = 1;
@@ -955,21 +997,52 @@ hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_ch
         const int64_t fit = per > 0 ? workspace_bytes / per : 0;
         n_split = static_cast<int>(want < fit ? want : fit);
     }
+    return n_split;
+}
+
+hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                               int n_q_chunks, const void* k_res, const void* v_res,
+                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
+                               const void* v_routed, const int32_t* group_idx, void* out,
+                               float* lse, void* workspace, int64_t workspace_bytes,
+                               hipStream_t stream) {
+    const int n_split = choose_splits(plan, q_chunk0, n_q_chunks, workspace_bytes);
     if (n_split <= 1)
         return launch_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
                              res_slot, k_routed, v_routed, group_idx, out, lse, nullptr, nullptr,
                              stream);
-    return launch_split_any(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
-                            k_routed, v_routed, group_idx, out, lse,
-                            static_cast<float*>(workspace), n_split, stream);
+    return launch_split_any<false>(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                   res_slot, k_routed, v_routed, group_idx, out, lse,
+                                   static_cast<float*>(workspace), n_split, stream);
 }
 
-hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chunk0,
-                              int n_q_chunks, const void* k_res, const void* v_res,
-                              int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
-                              const void* v_routed, const int32_t* group_idx, void* out,
-                              float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
-                              hipStream_t stream);
+hipError_t launch_gather_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                                      int n_q_chunks, const void* k_res, const void* v_res,
+                                      int64_t res_tokens, const int32_t* res_slot,
+                                      const void* k_src, const void* v_src, int64_t src_tokens,
+                                      const int32_t* group_idx, void* k_routed, void* v_routed,
+                                      void* out, float* lse, void* workspace,
+                                      int64_t workspace_bytes, hipStream_t stream) {
+    const hga_params& p = plan.p;
+    if (p.dtype == HGA_F32) {
+        hipError_t e = launch_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_src, v_src,
+                                        src_tokens, k_routed, v_routed, stream);
+        if (e != hipSuccess) return e;
+        return launch_attend_valu(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                  res_slot, k_routed, v_routed, group_idx, out, lse, nullptr,
+                                  nullptr, stream);
+    }
+    const int n_split = choose_splits(plan, q_chunk0, n_q_chunks, workspace_bytes);
+    if (n_split <= 1)
+        return launch_mfma_any<true>(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                     res_slot, k_routed, v_routed, group_idx, out, lse, nullptr,
+                                     nullptr, stream, k_src, v_src, src_tokens);
+    return launch_split_any<true>(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
+                                  res_slot, k_routed, v_routed, group_idx, out, lse,
+                                  static_cast<float*>(workspace), n_split, stream, k_src, v_src,
+                                  src_tokens);
+}
+
 
 hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                          const void* k_res, const void* v_res, int64_t res_tokens,

@@ -129,6 +129,16 @@ hga_status check_tensor(const void* p, const char* name) {
     return HGA_OK;
 }
 
+// A caller workspace: NULL with 0 bytes, or 16-byte aligned with > 0 bytes.
+hga_status check_workspace(const void* workspace, int64_t workspace_bytes) {
+    if (workspace_bytes < 0) return fail(HGA_EINVAL, "workspace_bytes must be >= 0");
+    if (workspace_bytes > 0) {
+        if (!workspace) return fail(HGA_EINVAL, "workspace is NULL with workspace_bytes > 0");
+        if (!aligned(workspace, 16)) return fail(HGA_EALIGN, "workspace is not 16-byte aligned");
+    }
+    return HGA_OK;
+}
+
 hga_status check_index(const void* p, const char* name) {
     if (!p) return fail(HGA_EINVAL, "%s is NULL", name);
     if (!aligned(p, 4)) return fail(HGA_EALIGN, "%s is not 4-byte aligned", name);
@@ -397,6 +407,30 @@ hga_status hga_route_groups(const hga_plan* plan, const float* qbar, const int32
                     "hga_route_groups launch");
 }
 
+// Device addresses of two pinned host allocations (their device mappings).
+static hga_status map_host_sources(const void* k_src, const void* v_src, const void** ks,
+                                   const void** vs) {
+    void* dk = nullptr;
+    void* dv = nullptr;
+    hipError_t e = hipHostGetDevicePointer(&dk, const_cast<void*>(k_src), 0);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();  // the failed lookup must not surface at a later launch
+        return fail(HGA_EINVAL, "k_src is not a mapped pinned host allocation (%s)",
+                    hipGetErrorString(e));
+    }
+    e = hipHostGetDevicePointer(&dv, const_cast<void*>(v_src), 0);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(HGA_EINVAL, "v_src is not a mapped pinned host allocation (%s)",
+                    hipGetErrorString(e));
+    }
+    if (!aligned(dk, 16) || !aligned(dv, 16))
+        return fail(HGA_EALIGN, "mapped host sources are not 16-byte aligned");
+    *ks = dk;
+    *vs = dv;
+    return HGA_OK;
+}
+
 hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t q_chunk0,
                          int32_t n_q_chunks, const void* k_src, const void* v_src,
                          int64_t src_tokens, int32_t src_on_host, void* k_routed,
@@ -413,26 +447,7 @@ hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t
     HGA_TRY(check_tensor(v_routed, "v_routed"));
     const void* ks = k_src;
     const void* vs = v_src;
-    if (src_on_host) {
-        void* dk = nullptr;
-        void* dv = nullptr;
-        hipError_t e = hipHostGetDevicePointer(&dk, const_cast<void*>(k_src), 0);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();  // the failed lookup must not surface at a later launch
-            return fail(HGA_EINVAL, "k_src is not a mapped pinned host allocation (%s)",
-                        hipGetErrorString(e));
-        }
-        e = hipHostGetDevicePointer(&dv, const_cast<void*>(v_src), 0);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            return fail(HGA_EINVAL, "v_src is not a mapped pinned host allocation (%s)",
-                        hipGetErrorString(e));
-        }
-        if (!aligned(dk, 16) || !aligned(dv, 16))
-            return fail(HGA_EALIGN, "mapped host sources are not 16-byte aligned");
-        ks = dk;
-        vs = dv;
-    }
+    if (src_on_host) HGA_TRY(map_host_sources(k_src, v_src, &ks, &vs));
     clear_stale_error();
     return launched(hga::launch_gather_kv(*plan, group_idx, q_chunk0, n_q_chunks, ks, vs,
                                           src_tokens, k_routed, v_routed,
@@ -519,16 +534,54 @@ hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_c
     if (n_q_chunks == 0) return HGA_OK;
     HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
                          k_routed, v_routed, group_idx, out, lse));
-    if (workspace_bytes > 0) {
-        if (!workspace) return fail(HGA_EINVAL, "workspace is NULL with workspace_bytes > 0");
-        if (!aligned(workspace, 16)) return fail(HGA_EALIGN, "workspace is not 16-byte aligned");
-    }
+    HGA_TRY(check_workspace(workspace, workspace_bytes));
     clear_stale_error();
     return launched(hga::launch_attend_split(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
                                              res_tokens, res_slot, k_routed, v_routed, group_idx,
                                              out, lse, workspace, workspace ? workspace_bytes : 0,
                                              static_cast<hipStream_t>(stream)),
                     "hga_attend_split launch");
+}
+
+hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                                   int32_t n_q_chunks, const void* k_res, const void* v_res,
+                                   int64_t res_tokens, const int32_t* res_slot,
+                                   const void* k_src, const void* v_src, int64_t src_tokens,
+                                   int32_t src_on_host, const int32_t* group_idx, void* k_routed,
+                                   void* v_routed, void* out, float* lse, void* workspace,
+                                   int64_t workspace_bytes, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0 || src_tokens < 0 ||
+        workspace_bytes < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks, res_tokens, src_tokens and "
+                    "workspace_bytes must be >= 0");
+    if (src_on_host != 0 && src_on_host != 1) return fail(HGA_EINVAL, "src_on_host must be 0 or 1");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                         k_routed, v_routed, group_idx, out, lse));
+    const hga_params& p = plan->p;
+    const int64_t need = static_cast<int64_t>(q_chunk0 + n_q_chunks - 1) * p.chunk;
+    if (src_tokens < need)
+        return fail(HGA_EINVAL, "k_src/v_src hold %lld tokens per head; the causal past of query "
+                    "chunk %d needs %lld", static_cast<long long>(src_tokens),
+                    q_chunk0 + n_q_chunks - 1, static_cast<long long>(need));
+    const int64_t row_bytes = static_cast<int64_t>(p.head_dim) * (p.dtype == HGA_BF16 ? 2 : 4);
+    if (src_tokens * row_bytes >= kMaxSlabBytes)
+        return fail(HGA_EUNSUPPORTED, "one head's routed-row source (%lld bytes) exceeds the "
+                    "%lld-byte addressing limit", static_cast<long long>(src_tokens * row_bytes),
+                    static_cast<long long>(kMaxSlabBytes));
+    HGA_TRY(check_tensor(k_src, "k_src"));
+    HGA_TRY(check_tensor(v_src, "v_src"));
+    HGA_TRY(check_workspace(workspace, workspace_bytes));
+    const void* ks = k_src;
+    const void* vs = v_src;
+    if (src_on_host) HGA_TRY(map_host_sources(k_src, v_src, &ks, &vs));
+    clear_stale_error();
+    return launched(hga::launch_gather_attend_split(
+                        *plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                        ks, vs, src_tokens, group_idx, k_routed, v_routed, out, lse, workspace,
+                        workspace ? workspace_bytes : 0, static_cast<hipStream_t>(stream)),
+                    "hga_gather_attend_split launch");
 }
 
 hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
@@ -585,12 +638,19 @@ hipError_t launch_block_step(const hga_plan& plan, const void* q_block, int32_t 
                              const void* k_res, const void* v_res, int64_t res_tokens,
                              float* chunk_sum, float* group_sum, int32_t table_chunks,
                              float* qbar, int32_t* chunk_idx, int32_t* group_idx, void* k_routed,
-                             void* v_routed, void* out, float* lse, hipStream_t stream) {
+                             void* v_routed, void* out, float* lse, void* workspace,
+                             int64_t workspace_bytes, hipStream_t stream) {
     hipError_t e = hga::launch_route(plan, q_block, c, 1, chunk_sum, group_sum, table_chunks,
                                      qbar, chunk_idx, group_idx, stream);
     if (e != hipSuccess) return e;
-    e = hga::launch_gather_attend(plan, q_block, c, 1, k_res, v_res, res_tokens, group_idx,
-                                  k_routed, v_routed, out, lse, nullptr, nullptr, stream);
+    if (workspace)
+        e = hga::launch_gather_attend_split(plan, q_block, c, 1, k_res, v_res, res_tokens, nullptr,
+                                            k_res, v_res, res_tokens, group_idx, k_routed,
+                                            v_routed, out, lse, workspace, workspace_bytes,
+                                            stream);
+    else
+        e = hga::launch_gather_attend(plan, q_block, c, 1, k_res, v_res, res_tokens, group_idx,
+                                      k_routed, v_routed, out, lse, nullptr, nullptr, stream);
     if (e != hipSuccess) return e;
     return hga::launch_build_summaries(plan, k_res, res_tokens, 0, c, c + 1, chunk_sum,
                                        group_sum, table_chunks, stream);
@@ -602,14 +662,17 @@ hga_status hga_block_step(const hga_plan* plan, const void* q_block, int32_t c,
                           const void* k_res, const void* v_res, int64_t res_tokens,
                           float* chunk_sum, float* group_sum, int32_t table_chunks, float* qbar,
                           int32_t* chunk_idx, int32_t* group_idx, void* k_routed, void* v_routed,
-                          void* out, float* lse, void* stream) {
+                          void* out, float* lse, void* workspace, int64_t workspace_bytes,
+                          void* stream) {
     HGA_TRY(check_block_step(plan, q_block, c, k_res, v_res, res_tokens, chunk_sum, group_sum,
                              table_chunks, qbar, chunk_idx, group_idx, k_routed, v_routed, out,
                              lse));
+    HGA_TRY(check_workspace(workspace, workspace_bytes));
     clear_stale_error();
     return launched(launch_block_step(*plan, q_block, c, k_res, v_res, res_tokens, chunk_sum,
                                       group_sum, table_chunks, qbar, chunk_idx, group_idx,
                                       k_routed, v_routed, out, lse,
+                                      workspace_bytes > 0 ? workspace : nullptr, workspace_bytes,
                                       static_cast<hipStream_t>(stream)),
                     "hga_block_step launch");
 }
@@ -619,9 +682,10 @@ hga_status hga_prefill_blocks(const hga_plan* plan, const void* q_blocks, int32_
                               float* chunk_sum, float* group_sum, int32_t table_chunks,
                               float* qbar, int32_t* chunk_idx, int32_t* group_idx,
                               void* k_routed, void* v_routed, void* out, float* lse,
-                              void* stream) {
+                              void* workspace, int64_t workspace_bytes, void* stream) {
     HGA_TRY(check_plan(plan));
     if (n_blocks < 0) return fail(HGA_EINVAL, "n_blocks must be >= 0");
+    HGA_TRY(check_workspace(workspace, workspace_bytes));
     if (n_blocks == 0) return HGA_OK;
     const hga_params& p = plan->p;
     const int64_t eb = p.dtype == HGA_BF16 ? 2 : 4;
@@ -653,7 +717,9 @@ hga_status hga_prefill_blocks(const hga_plan* plan, const void* q_blocks, int32_
             *plan, at(q_blocks, c * q_bytes), c, k_res, v_res, res_tokens, chunk_sum, group_sum,
             table_chunks, qbar + c * qbar_elems, chunk_idx + c * ci_elems,
             group_idx + c * gi_elems, atw(k_routed, c * rt_bytes), atw(v_routed, c * rt_bytes),
-            atw(out, c * q_bytes), lse ? lse + c * bq : nullptr, static_cast<hipStream_t>(stream));
+            atw(out, c * q_bytes), lse ? lse + c * bq : nullptr,
+            workspace_bytes > 0 ? workspace : nullptr, workspace_bytes,
+            static_cast<hipStream_t>(stream));
         if (e != hipSuccess) return launched(e, "hga_prefill_blocks launch");
     }
     return HGA_OK;

@@ -91,6 +91,19 @@ hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_ch
                                float* lse, void* workspace, int64_t workspace_bytes,
                                hipStream_t stream);
 
+// The gather fused into the split attention: routed rows copied from
+// k_src / v_src (src_tokens rows per head, device memory or the device
+// mapping of pinned host memory) and written to k_routed / v_routed; the
+// visible and current chunks from k_res / v_res (res_slot as for
+// launch_attend).
+hipError_t launch_gather_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                                      int n_q_chunks, const void* k_res, const void* v_res,
+                                      int64_t res_tokens, const int32_t* res_slot,
+                                      const void* k_src, const void* v_src, int64_t src_tokens,
+                                      const int32_t* group_idx, void* k_routed, void* v_routed,
+                                      void* out, float* lse, void* workspace,
+                                      int64_t workspace_bytes, hipStream_t stream);
+
 // The gather of the routed rows fused into the attention (prefill layout:
 // resident K/V indexed by token, no slot map); writes k_routed / v_routed as
 // launch_gather_kv does.  start/stop as for launch_attend.

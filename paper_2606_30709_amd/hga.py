@@ -19,6 +19,7 @@ __all__ = [
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
     "hga_attend_timed", "hga_attend_split", "hga_attend_split_workspace", "hga_gather_attend",
+    "hga_gather_attend_split",
     "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error",
     "hga_version", "EXPORTED_SYMBOLS",
 ]
@@ -30,8 +31,8 @@ EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
     "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_attend_split",
-    "hga_attend_split_workspace", "hga_gather_attend", "hga_block_step", "hga_prefill_blocks",
-    "hga_status_string", "hga_last_error", "hga_version",
+    "hga_attend_split_workspace", "hga_gather_attend", "hga_gather_attend_split",
+    "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error", "hga_version",
 )
 
 
@@ -87,10 +88,12 @@ def library() -> ctypes.CDLL:
             "hga_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, i64,
                                  vp],
             "hga_gather_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp],
+            "hga_gather_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, i64, i32, vp,
+                                        vp, vp, vp, vp, vp, i64, vp],
             "hga_block_step": [vp, vp, i32, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp, vp,
-                               vp, vp],
+                               vp, vp, i64, vp],
             "hga_prefill_blocks": [vp, vp, i32, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp,
-                                   vp, vp, vp],
+                                   vp, vp, vp, i64, vp],
         }
         for name, args in sigs.items():
             fn = getattr(lib, name)
@@ -302,6 +305,20 @@ def hga_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v
         _ptr(workspace), nbytes, _stream(stream)))
 
 
+def hga_gather_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_src, v_src,
+                            group_idx, k_routed, v_routed, out, workspace, lse=None,
+                            res_slot=None, src_on_host=False, stream=None):
+    """hga_gather_kv (from k_src/v_src [B, Hkv, src_tokens, d], device or
+    pinned host) + hga_attend_split in one pass; k_routed/v_routed written."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(library().hga_gather_attend_split(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(res_slot), _ptr(k_src), _ptr(v_src), k_src.shape[2], 1 if src_on_host else 0,
+        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse),
+        _ptr(workspace), nbytes, _stream(stream)))
+
+
 def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx, k_routed,
                       v_routed, out, lse=None, start_event=None, stop_event=None, stream=None):
     """hga_gather_kv + hga_attend in one pass (prefill layout: k_res/v_res
@@ -316,23 +333,33 @@ def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx,
         stop_event.cuda_event if stop_event is not None else None, _stream(stream)))
 
 
+def _ws(workspace):
+    return (_ptr(workspace),
+            workspace.numel() * workspace.element_size() if workspace is not None else 0)
+
+
 def hga_block_step(plan: Plan, q_block, c: int, k_res, v_res, chunk_sum, group_sum, qbar,
-                   chunk_idx, group_idx, k_routed, v_routed, out, lse=None, stream=None):
+                   chunk_idx, group_idx, k_routed, v_routed, out, lse=None, workspace=None,
+                   stream=None):
     """One block of a block-sequential prefill: route query chunk c, gather +
     attend it, append chunk c's summaries.  q_block/out [B, Hq, C, d];
     k_res/v_res [B, Hkv, res_tokens, d]; the per-chunk outputs have a
-    query-chunk dimension of 1."""
+    query-chunk dimension of 1.  workspace: None (bit-identical to the bulk
+    prefill) or a device tensor for the split attention."""
     _check(library().hga_block_step(
         plan.handle, _ptr(q_block), c, _ptr(k_res), _ptr(v_res), k_res.shape[2],
         _ptr(chunk_sum), _ptr(group_sum), chunk_sum.shape[2], _ptr(qbar), _ptr(chunk_idx),
-        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse), _stream(stream)))
+        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse), *_ws(workspace),
+        _stream(stream)))
 
 
 def hga_prefill_blocks(plan: Plan, q_blocks, k_res, v_res, chunk_sum, group_sum, qbar,
-                       chunk_idx, group_idx, k_routed, v_routed, out, lse=None, stream=None):
+                       chunk_idx, group_idx, k_routed, v_routed, out, lse=None, workspace=None,
+                       stream=None):
     """hga_block_step for blocks 0 .. n_blocks-1 in order; block-major
-    buffers (first dimension n_blocks)."""
+    buffers (first dimension n_blocks); workspace as for hga_block_step."""
     _check(library().hga_prefill_blocks(
         plan.handle, _ptr(q_blocks), q_blocks.shape[0], _ptr(k_res), _ptr(v_res), k_res.shape[2],
         _ptr(chunk_sum), _ptr(group_sum), chunk_sum.shape[2], _ptr(qbar), _ptr(chunk_idx),
-        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse), _stream(stream)))
+        _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse), *_ws(workspace),
+        _stream(stream)))

@@ -8,7 +8,9 @@ summarises every chunk, routes every query chunk, gathers the routed groups
 RAM-backed cold tier, Sec. 4.3); the device holds the summary tables, the
 always-visible first and recent chunks and the current 64-token block.  One
 step routes the block, gathers only its routed groups over the host link,
-attends, and appends the block's summaries (the store's "append").
+attends (``hga_attend_split``; or both in one call,
+``hga_gather_attend_split``, with ``fused_gather=True``), and appends the
+block's summaries (the store's "append").
 
 Prefill routing has three equivalent forms (bit-identical summaries, query
 means and indices), chosen by ``route_mode``: "fused" (``hga_build_summaries``
@@ -122,9 +124,13 @@ class BlockPrefillPipeline:
     appended to the tables (``hga_prefill_blocks``: one native loop of
     ``hga_block_step``).  Queries, outputs and the per-block routing results
     are block-major ([n_blocks, ...]); K/V are the whole prompt's,
-    token-indexed, as in the bulk prefill."""
+    token-indexed, as in the bulk prefill.  ``split_attend``: the blocks'
+    attention in its split form (a workspace spreads each block's few units
+    over more workgroups); without it every output is bit-identical to the
+    bulk prefill's."""
 
-    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None):
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
+                 split_attend: bool = False):
         assert not w.decode_block
         self.w = w
         self.plan = plan or hga.Plan.for_workload(w)
@@ -146,21 +152,31 @@ class BlockPrefillPipeline:
         self.v_routed = torch.empty_like(self.k_routed)
         self.out = torch.empty_like(self.q_blocks)
         self.lse = torch.empty(nc, B, Hq, C, dtype=f32, device=device)
+        self.attend_ws = None
+        if split_attend:
+            nbytes = hga.hga_attend_split_workspace(self.plan, 1)
+            self.attend_ws = torch.empty((nbytes + 3) // 4, dtype=f32, device=device)
 
     def step(self, stream=None):
         hga.hga_prefill_blocks(self.plan, self.q_blocks, self.k, self.v, self.chunk_sum,
                                self.group_sum, self.qbar, self.chunk_idx, self.group_idx,
-                               self.k_routed, self.v_routed, self.out, self.lse, stream=stream)
+                               self.k_routed, self.v_routed, self.out, self.lse,
+                               workspace=self.attend_ws, stream=stream)
 
 
 class DecodePipeline:
     """One query block (the last chunk of the workload) after a host-resident history."""
 
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 fused_route: bool = True, split_attend: bool = True):
+                 fused_route: bool = True, split_attend: bool = True, fused_gather: bool = False):
         assert w.decode_block
         self.w = w
         self.fused_route = fused_route
+        # fused_gather: the host gather inside the split attention
+        # (hga_gather_attend_split), else hga_gather_kv then the attention.
+        # The separate gather is the faster one here: each unit's two query
+        # workgroups would both pull its routed rows over the host link.
+        self.fused_gather = fused_gather and split_attend
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
         f32, i32 = torch.float32, torch.int32
@@ -246,8 +262,19 @@ class DecodePipeline:
         hga.hga_build_summaries(self.plan, self.k_res, self.c, self.c + 1, self.chunk_sum,
                                 self.group_sum, k_chunk0=self.c - self.cur_slot, stream=stream)
 
+    def gather_attend(self, stream=None):
+        """The routed groups copied from pinned host memory by the split
+        attention's own workgroups while the others attend the resident chunks."""
+        hga.hga_gather_attend_split(self.plan, self.q, self.c, self.k_res, self.v_res,
+                                    self.k_hist, self.v_hist, self.group_idx, self.k_routed,
+                                    self.v_routed, self.out, self.attend_ws, self.lse,
+                                    res_slot=self.res_slot, src_on_host=True, stream=stream)
+
     def step(self, stream=None):
         self.route(stream)
-        self.gather(stream)
-        self.attend(stream)
+        if self.fused_gather:
+            self.gather_attend(stream)
+        else:
+            self.gather(stream)
+            self.attend(stream)
         self.append(stream)

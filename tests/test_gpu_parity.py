@@ -422,18 +422,21 @@ BLOCK_CASES = {k: SMALL[k] for k in ("tiny", "smalllm_2k", "qwen_4k_ragged", "qw
                                       "gqa3_d64", "qwen_chunks_4k")}
 
 
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("key", list(BLOCK_CASES))
-def test_block_sequential_prefill_equals_bulk(hga, key):
+def test_block_sequential_prefill_equals_bulk(hga, key, split):
     """Prefill as a sequence of 64-token blocks (route against the chunks
     closed so far, attend, append) writes, block by block, exactly what the
-    bulk prefill writes for the same query chunk: prefill = decode."""
+    bulk prefill writes for the same query chunk: prefill = decode.  With the
+    split attention (a workspace) the summaries, routing and routed buffers
+    are still identical and the outputs meet the oracle bar."""
     from paper_2606_30709_amd.pipeline import BlockPrefillPipeline, PrefillPipeline
     w = BLOCK_CASES[key]
-    _say(f"[block-prefill] {key}")
+    _say(f"[block-prefill] {key} split={split}")
     inp = W.generate(w)
     bulk = PrefillPipeline(w, inp)
     bulk.step()
-    blk = BlockPrefillPipeline(w, inp)
+    blk = BlockPrefillPipeline(w, inp, split_attend=split)
     for t in (blk.out, blk.lse, blk.qbar):
         t.fill_(float("nan"))
     blk.chunk_idx.fill_(-7)
@@ -451,9 +454,23 @@ def test_block_sequential_prefill_equals_bulk(hga, key):
     assert same(blk.k_routed[:, :, :, 0].permute(1, 2, 0, 3, 4), bulk.k_routed)
     assert same(blk.v_routed[:, :, :, 0].permute(1, 2, 0, 3, 4), bulk.v_routed)
     out_bulk = bulk.out.reshape(B, Hq, nc, C, d).permute(2, 0, 1, 3, 4)
-    assert same(blk.out, out_bulk)
     lse_bulk = bulk.lse.reshape(B, Hq, nc, C).permute(2, 0, 1, 3)
-    assert same(blk.lse, lse_bulk)
+    if not split:
+        assert same(blk.out, out_bulk)
+        assert same(blk.lse, lse_bulk)
+        return
+    assert not torch.isnan(blk.out).any() and not torch.isnan(blk.lse).any()
+    chunks = sorted({0, 1, nc // 2, nc - 1})
+    q64, k64, v64 = (f64(inp[x], w.dtype) for x in "qkv")
+    units = [(b, j, c) for b in range(B) for j in range(w.n_kv_heads) for c in chunks]
+    o_ref, l_ref = O.attend(q64, k64, v64, bulk.group_idx.cpu().numpy(), list(range(nc)), C,
+                            w.group, w.keep_first, w.keep_last, w.force_prev, units=units)
+    g_out = tensor_to_f64(blk.out)
+    g_lse = tensor_to_f64(blk.lse)
+    eo = max(np.max(np.abs(g_out[c] - o_ref[:, :, c * C:(c + 1) * C])) for c in chunks)
+    el = max(np.max(np.abs(g_lse[c] - l_ref[:, :, c * C:(c + 1) * C])) for c in chunks)
+    _say(f"  split blocks {chunks}: out {eo:.3g} lse {el:.3g}")
+    assert eo <= OUT_TOL[w.dtype] and el <= LSE_TOL[w.dtype]
 
 
 def _split_route_check(hga, plan, k, k_chunk0, n_chunks, table_chunks, q, q_chunk0, w):
@@ -607,6 +624,41 @@ def _decode_check(hga, w):
     return pipe
 
 
+def test_decode_fused_gather_equals_separate(hga):
+    """The host gather inside the split attention (hga_gather_attend_split)
+    writes exactly what hga_gather_kv from host memory + hga_attend_split
+    write: routed buffers, output and LSE, bit for bit; also with padded and
+    future group ids planted."""
+    from paper_2606_30709_amd.pipeline import DecodePipeline
+    for w in (W.preset("decode64k"), W_("decode64k", seq_len=8192 + 64,
+                                        needle_depths=(12, 64, 115))):
+        _say(f"[decode fused gather] N{w.seq_len}")
+        inp = W.generate(w)
+        fused = DecodePipeline(w, inp, fused_gather=True)
+        sep = DecodePipeline(w, inp, plan=fused.plan)
+        assert fused.fused_gather and not sep.fused_gather
+        for pipe in (fused, sep):
+            pipe.route()
+        torch.cuda.synchronize()
+        assert torch.equal(fused.group_idx, sep.group_idx)
+        for planted in (False, True):
+            if planted:
+                for pipe in (fused, sep):
+                    pipe.group_idx[0, 0, 0, 0] = -1
+                    pipe.group_idx[0, w.n_kv_heads - 1, 0, w.topk_groups - 1] = 10 ** 6
+            for pipe in (fused, sep):
+                for t in (pipe.k_routed, pipe.v_routed, pipe.out, pipe.lse):
+                    t.fill_(float("nan"))
+            fused.gather_attend()
+            sep.gather()
+            sep.attend()
+            torch.cuda.synchronize()
+            for name in ("k_routed", "v_routed", "out", "lse"):
+                a, b = getattr(fused, name), getattr(sep, name)
+                assert torch.equal(_bits(a), _bits(b)), name
+            assert not torch.isnan(fused.out).any()
+
+
 def test_decode_block_parity_reduced(hga):
     w = W_("decode64k", seq_len=8192 + 64, needle_depths=(12, 64, 115))
     _decode_check(hga, w)
@@ -681,6 +733,17 @@ def test_argument_errors_launch_nothing(hga):
                            1024, 1, kr.data_ptr(), kr.data_ptr(), None)
     assert st == -1
     assert "pinned" in hga.hga_last_error()
+    # the fused gather's source must cover the causal past of the last query chunk
+    st = lib.hga_gather_attend_split(plan.handle, q.data_ptr(), 0, 16, k.data_ptr(),
+                                     k.data_ptr(), 1024, None, k.data_ptr(), k.data_ptr(), 900, 0,
+                                     gi.data_ptr(), kr.data_ptr(), kr.data_ptr(), q.data_ptr(),
+                                     None, None, 0, None)
+    assert st == -1 and "causal past" in hga.hga_last_error()
+    st = lib.hga_gather_attend_split(plan.handle, q.data_ptr(), 0, 16, k.data_ptr(),
+                                     k.data_ptr(), 1024, None, host.data_ptr(), host.data_ptr(),
+                                     1024, 1, gi.data_ptr(), kr.data_ptr(), kr.data_ptr(),
+                                     q.data_ptr(), None, None, 0, None)
+    assert st == -1 and "pinned" in hga.hga_last_error()
     # empty ranges are no-ops
     hga.hga_build_summaries(plan, k, 3, 3, cs, gs)
     torch.cuda.synchronize()
