@@ -289,6 +289,59 @@ def decode_bench(w, inp, args):
     print(json.dumps(res), flush=True)
 
 
+def decode_sequence_bench(w, inp, args):
+    """Consecutive 64-token decode blocks (the last w.decode_blocks chunks):
+    per block route, gather of the routed groups (through the warm LRU cache
+    unless --no-cache, else straight from pinned host memory), split
+    attention, append.  One step = the whole sequence of blocks, starting
+    from an empty cache (a fresh sequence); the uncached rate is measured
+    in the same run for comparison."""
+    import torch
+
+    from paper_2606_30709_amd.pipeline import DecodeSequencePipeline
+    slots = args.cache_slots or 8 * w.topk_groups
+
+    def run(cache_slots):
+        pipe = DecodeSequencePipeline(w, inp, cache_slots=cache_slots)
+        for _ in range(args.warmup):
+            pipe.reset_cache()
+            pipe.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            pipe.reset_cache()
+            pipe.step()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        routed = int((pipe.group_idx >= 0).sum().item())
+        return dt, pipe.pcie_bytes(), routed
+
+    dt, pcie, routed = run(None if args.no_cache else slots)
+    res = {
+        "metric": "routed-attn decode tokens/s (64-token blocks in sequence)",
+        "value": round(w.chunk * w.batch * w.decode_blocks / dt, 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(dt * 1e3, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": (f"{w.key}: {w.decode_blocks} consecutive decode blocks "
+                                f"B{w.batch} H{w.n_q_heads}/{w.n_kv_heads} d{w.head_dim} from "
+                                f"position {w.q_chunk0 * w.chunk} {w.dtype} F{w.keep_first} "
+                                f"L{w.keep_last} Kc{w.topk_chunks} Kg{w.topk_groups}, history "
+                                f"in pinned host memory"),
+                   "seed": inp["seed"],
+                   "warm_cache_slots_per_head": None if args.no_cache else slots},
+        "us_per_block": round(dt * 1e6 / w.decode_blocks, 2),
+        "pcie_bytes_per_block": pcie // w.decode_blocks,
+        "routed_groups_fetched_from_host": round(
+            pcie / (2 * w.group * w.head_dim * w.elem_bytes) / max(routed, 1), 4),
+    }
+    if not args.no_cache:
+        dt0, pcie0, _ = run(None)
+        res["uncached"] = {"us_per_block": round(dt0 * 1e6 / w.decode_blocks, 2),
+                           "pcie_bytes_per_block": pcie0 // w.decode_blocks}
+    print(json.dumps(res), flush=True)
+
+
 def blockwise_bench(w, inp, args):
     """The prompt as a sequence of 64-token blocks (hga_prefill_blocks: per
     block, routing against the chunks closed so far, gather + attention,
@@ -345,6 +398,11 @@ def main():
                     help="fused: hga_gather_attend (the attention stages the routed rows and "
                          "writes the routed buffers); separate: hga_gather_kv + hga_attend "
                          "(identical results)")
+    ap.add_argument("--no-cache", action="store_true",
+                    help="decode sequence: gather every block's routed groups from host memory")
+    ap.add_argument("--cache-slots", type=int, default=0,
+                    help="decode sequence: warm-cache slots per (batch, KV head) "
+                         "(default 8 x topk_groups)")
     ap.add_argument("--block-exact", action="store_true",
                     help="with --blockwise: the single-workgroup attention whose outputs are "
                          "bit-identical to the bulk prefill's (default: the split attention)")
@@ -367,6 +425,9 @@ def main():
     w = W.preset(args.workload)
     torch.cuda.set_device(0)
     inp = W.generate(w)
+    if w.decode_block and w.decode_blocks > 1:
+        decode_sequence_bench(w, inp, args)
+        return
     if w.decode_block:
         decode_bench(w, inp, args)
         return

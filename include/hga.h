@@ -276,6 +276,50 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
                             const void* v_routed, const int32_t* group_idx, void* out, float* lse,
                             void* start_event, void* stop_event, void* stream);
 
+/* hga_gather_kv for one query chunk c through a warm cache in device memory
+ * (Sec. 4.3: the "warm" tier, a bounded LRU cache of recently routed token
+ * K/V; here the cached unit is the routed group, the unit the gather moves).
+ * Each (batch, KV head) owns a partition of n_slots slots; a routed group
+ * whose slot still holds it is copied from the cache (a hit), every other
+ * valid group from k_src/v_src into the least recently used slot and the
+ * routed buffer (a miss).  k_routed/v_routed receive exactly what
+ * hga_gather_kv(plan, group_idx, c, 1, k_src, v_src, src_tokens,
+ * src_on_host, k_routed, v_routed, stream) writes.
+ * Replacement: the victims are the slots with the oldest last-use tick
+ * (never-used slots first, ties to the lowest slot), taken in ascending slot
+ * order by the misses in routed order; hits and misses get `tick`.
+ *   group_idx   device int32 [batch, n_kv_heads, 1, topk_groups]; ids outside
+ *               [0, c*chunk/group) or past src_tokens are absent (zero rows);
+ *               a repeated id gets its first occurrence's rows
+ *   k_src,v_src [batch, n_kv_heads, src_tokens, head_dim], device memory
+ *               (src_on_host = 0) or pinned mapped host memory (1);
+ *               src_tokens >= c * chunk
+ *   cache_k, cache_v  device [batch, n_kv_heads, n_slots, group, head_dim]
+ *   n_slots     in [topk_groups, 8192] (so that a call never evicts a group
+ *               it uses)
+ *   slot_group  device int32 [batch, n_kv_heads, n_slots]: group held, -1 empty
+ *   slot_used   device int32 [batch, n_kv_heads, n_slots]: tick of last use
+ *   group_slot  device int32 [batch, n_kv_heads, src_tokens / group]: slot
+ *               holding the group or -1
+ *               (a new cache: every entry of the three maps -1)
+ *   entry_slot  device int32 [batch, n_kv_heads, topk_groups]: the call's
+ *               copy plan (written, then read by its second kernel; no
+ *               contents are needed before or kept after a call)
+ *   tick        >= 0 and greater than every tick of an earlier call on the
+ *               same maps (e.g. the block's position in the sequence)
+ *   n_fetched   device int32 [batch, n_kv_heads] or NULL: groups read from
+ *               k_src/v_src by this call (the misses)
+ * The caller owns every buffer; calls on the same maps must be ordered (the
+ * same stream).  HGA_EINVAL for an n_slots outside the range or a source
+ * shorter than the causal past. */
+hga_status hga_gather_kv_cached(const hga_plan* plan, const int32_t* group_idx, int32_t c,
+                                const void* k_src, const void* v_src, int64_t src_tokens,
+                                int32_t src_on_host, void* cache_k, void* cache_v,
+                                int32_t n_slots, int32_t* slot_group, int32_t* slot_used,
+                                int32_t* group_slot, int32_t* entry_slot, int32_t tick,
+                                void* k_routed, void* v_routed, int32_t* n_fetched,
+                                void* stream);
+
 /* hga_attend for launches with few units (a decode block, one block of a
  * block-sequential prefill), Sec. 3.4: each unit's key tiles (current chunk,
  * visible chunks, routed rows) are divided among up to 16 workgroups, each

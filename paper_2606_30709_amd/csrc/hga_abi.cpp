@@ -129,6 +129,9 @@ hga_status check_tensor(const void* p, const char* name) {
     return HGA_OK;
 }
 
+// Most slots a warm-cache partition may have (its LRU keys live in LDS).
+constexpr int32_t kMaxCacheSlots = 8192;
+
 // A caller workspace: NULL with 0 bytes, or 16-byte aligned with > 0 bytes.
 hga_status check_workspace(const void* workspace, int64_t workspace_bytes) {
     if (workspace_bytes < 0) return fail(HGA_EINVAL, "workspace_bytes must be >= 0");
@@ -453,6 +456,53 @@ hga_status hga_gather_kv(const hga_plan* plan, const int32_t* group_idx, int32_t
                                           src_tokens, k_routed, v_routed,
                                           static_cast<hipStream_t>(stream)),
                     "hga_gather_kv launch");
+}
+
+hga_status hga_gather_kv_cached(const hga_plan* plan, const int32_t* group_idx, int32_t c,
+                                const void* k_src, const void* v_src, int64_t src_tokens,
+                                int32_t src_on_host, void* cache_k, void* cache_v,
+                                int32_t n_slots, int32_t* slot_group, int32_t* slot_used,
+                                int32_t* group_slot, int32_t* entry_slot, int32_t tick,
+                                void* k_routed, void* v_routed, int32_t* n_fetched,
+                                void* stream) {
+    HGA_TRY(check_plan(plan));
+    const hga_params& p = plan->p;
+    if (c < 0 || src_tokens < 0 || tick < 0)
+        return fail(HGA_EINVAL, "c, src_tokens and tick must be >= 0");
+    if (src_on_host != 0 && src_on_host != 1) return fail(HGA_EINVAL, "src_on_host must be 0 or 1");
+    if (n_slots < p.topk_groups || n_slots > kMaxCacheSlots)
+        return fail(HGA_EINVAL, "n_slots must be in [topk_groups = %d, %d], got %d",
+                    p.topk_groups, kMaxCacheSlots, n_slots);
+    const int64_t need = static_cast<int64_t>(c) * p.chunk;
+    if (src_tokens < need)
+        return fail(HGA_EINVAL, "k_src/v_src hold %lld tokens per head; the causal past of query "
+                    "chunk %d needs %lld", static_cast<long long>(src_tokens), c,
+                    static_cast<long long>(need));
+    if (hga::gather_cached_lds_bytes(*plan, n_slots) > static_cast<size_t>(plan->max_lds))
+        return fail(HGA_EUNSUPPORTED, "cache bookkeeping for %d slots exceeds the LDS limit",
+                    n_slots);
+    HGA_TRY(check_index(group_idx, "group_idx"));
+    HGA_TRY(check_tensor(k_src, "k_src"));
+    HGA_TRY(check_tensor(v_src, "v_src"));
+    HGA_TRY(check_tensor(cache_k, "cache_k"));
+    HGA_TRY(check_tensor(cache_v, "cache_v"));
+    HGA_TRY(check_index(slot_group, "slot_group"));
+    HGA_TRY(check_index(slot_used, "slot_used"));
+    HGA_TRY(check_index(group_slot, "group_slot"));
+    HGA_TRY(check_index(entry_slot, "entry_slot"));
+    HGA_TRY(check_tensor(k_routed, "k_routed"));
+    HGA_TRY(check_tensor(v_routed, "v_routed"));
+    if (n_fetched && !aligned(n_fetched, 4)) return fail(HGA_EALIGN, "n_fetched is not 4-byte aligned");
+    const void* ks = k_src;
+    const void* vs = v_src;
+    if (src_on_host) HGA_TRY(map_host_sources(k_src, v_src, &ks, &vs));
+    clear_stale_error();
+    return launched(hga::launch_gather_kv_cached(*plan, group_idx, c, ks, vs, src_tokens, cache_k,
+                                                 cache_v, n_slots, slot_group, slot_used,
+                                                 group_slot, src_tokens / p.group, tick,
+                                                 entry_slot, k_routed, v_routed, n_fetched,
+                                                 static_cast<hipStream_t>(stream)),
+                    "hga_gather_kv_cached launch");
 }
 
 namespace {

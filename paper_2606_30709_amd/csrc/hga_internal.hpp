@@ -71,6 +71,16 @@ hipError_t launch_gather_kv(const hga_plan& plan, const int32_t* group_idx, int 
                             int64_t src_tokens, void* k_routed, void* v_routed,
                             hipStream_t stream);
 
+// Gather of one query chunk's routed groups through a warm LRU cache of
+// groups in device memory (one workgroup per (batch, KV head)).
+size_t gather_cached_lds_bytes(const hga_plan& plan, int n_slots);
+hipError_t launch_gather_kv_cached(const hga_plan& plan, const int32_t* group_idx, int c,
+                                   const void* k_src, const void* v_src, int64_t src_tokens,
+                                   void* cache_k, void* cache_v, int n_slots, int32_t* slot_group,
+                                   int32_t* slot_used, int32_t* group_slot, int64_t n_groups,
+                                   int tick, int32_t* entry_slot, void* k_routed, void* v_routed,
+                                   int32_t* n_fetched, hipStream_t stream);
+
 // start/stop (may be null) are recorded by the attention kernel's dispatch.
 hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, int n_q_chunks,
                          const void* k_res, const void* v_res, int64_t res_tokens,

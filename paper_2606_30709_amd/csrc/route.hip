@@ -320,8 +320,9 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
 // Top-k by a whole workgroup of kThreads threads, for keys whose ids ascend
 // with their position: writes the k ids with the largest keys to sel[0 .. k)
 // in ascending order (0 < k <= n); sel is complete when it returns.  Every
-// thread must call it.  Short lists (and lists longer than the workgroup)
-// go to wave 0's wave_select_topk.  Otherwise thread t holds key t and:
+// thread must call it.  Short lists (and lists longer than kMaxPer keys per
+// thread) go to wave 0's wave_select_topk.  Otherwise thread t holds keys
+// t, t + kThreads, ... and:
 // 1. each wave finds T_w, the k-th largest score word among its own keys
 //    (bit-by-bit bisection on ballot counts; 0 if it holds fewer than k);
 //    the k-th largest word of all keys is at least L = max_w T_w, so every
@@ -332,47 +333,74 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
 // The result is the exact top k with wave_select_topk's tie rule.
 template <int kThreads>
 struct WgSelect {
+    static constexpr int kMaxPer = 4;
     uint32_t wave_t[kThreads / 64];
-    int wave_cnt[kThreads / 64];
-    uint64_t surv[kThreads];
+    int wave_cnt[kMaxPer][kThreads / 64];
+    uint64_t surv[kMaxPer * kThreads];
 };
 
 template <int kThreads>
 __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int* sel, int* scr,
                                                WgSelect<kThreads>* S) {
     constexpr int NW = kThreads / 64;
+    constexpr int kMaxPer = WgSelect<kThreads>::kMaxPer;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if (n <= 256 || n > kThreads) {
+    if (n <= 256 || n > kMaxPer * kThreads) {
         if (wave == 0) wave_select_topk(keys, n, k, sel, scr, true);
         __syncthreads();
         return;
     }
-    const uint64_t key = tid < n ? keys[tid] : 0;
-    const uint32_t hi = static_cast<uint32_t>(key >> 32);
-    const bool valid = tid < n;
+    const int per = (n + kThreads - 1) / kThreads;  // keys per thread, 1 .. kMaxPer
+    uint64_t key[kMaxPer];
+    uint32_t hi[kMaxPer];
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+        const int x = tid + i * kThreads;
+        key[i] = i < per && x < n ? keys[x] : 0;
+        hi[i] = static_cast<uint32_t>(key[i] >> 32);  // 0 for no key: never >= a candidate
+    }
     uint32_t t_w = 0;
     for (int bit = 31; bit >= 0; --bit) {
         const uint32_t cand = t_w | (1u << bit);
-        if (__popcll(__ballot(valid && hi >= cand)) >= k) t_w = cand;
+        int cnt = 0;
+#pragma unroll
+        for (int i = 0; i < kMaxPer; ++i)
+            if (i < per) cnt += __popcll(__ballot(hi[i] >= cand));
+        if (cnt >= k) t_w = cand;
     }
     if (lane == 0) S->wave_t[wave] = t_w;
     __syncthreads();
     uint32_t bound = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) bound = S->wave_t[w] > bound ? S->wave_t[w] : bound;
-    const bool keep = valid && hi >= bound;
-    const uint64_t km = __ballot(keep);
-    if (lane == 0) S->wave_cnt[wave] = __popcll(km);
-    __syncthreads();
-    int pos = __popcll(km & ((uint64_t(1) << lane) - 1)), n_keep = 0;
+    // word 0 marks an absent key (a score's word is never 0: that pattern
+    // is a NaN), so it never passes, whatever the bound
+    uint64_t km[kMaxPer];
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-        const int cw = S->wave_cnt[w];
-        n_keep += cw;
-        if (w < wave) pos += cw;
+    for (int i = 0; i < kMaxPer; ++i) {
+        km[i] = i < per ? __ballot(hi[i] != 0 && hi[i] >= bound) : 0;
+        if (lane == 0 && i < per) S->wave_cnt[i][wave] = __popcll(km[i]);
     }
-    if (keep) S->surv[pos] = key;
+    __syncthreads();
+    // position order: pass i, then wave, then lane
+    int base = 0, n_keep = 0;
+    for (int i = 0; i < per; ++i)
+        for (int w = 0; w < NW; ++w) {
+            const int cw = S->wave_cnt[i][w];
+            n_keep += cw;
+        }
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+        if (i >= per) break;
+        int pos = base + __popcll(km[i] & ((uint64_t(1) << lane) - 1));
+        for (int w = 0; w < NW; ++w) {
+            const int cw = S->wave_cnt[i][w];
+            if (w < wave) pos += cw;
+            base += cw;
+        }
+        if (hi[i] != 0 && hi[i] >= bound) S->surv[pos] = key[i];
+    }
     __syncthreads();
     if (wave == 0) wave_select_topk(S->surv, n_keep, k, sel, scr, true);
     __syncthreads();
@@ -645,7 +673,7 @@ inline WideGeom route_wide_geom(const hga_plan& plan, int n_max, bool groups, bo
     const size_t part = qbar_in ? 0 : sizeof(float) * 8 * p.head_dim;  // wg_mean_rows partials
     const size_t tab = sizeof(float) * kWideRows * (p.head_dim + 4);
     size_t big = rows + part > tab ? rows + part : tab;
-    if (big < sizeof(WgSelect<1024>)) big = sizeof(WgSelect<1024>);
+    if (big < sizeof(WgSelect<1024>)) big = sizeof(WgSelect<1024>);  // the selection, after scoring
     WideGeom g;
     g.big_off = wave_lds_bytes(p.head_dim, groups ? p.topk_chunks : 0, ntop, nk);
     g.total = g.big_off + align16(big);

@@ -15,11 +15,11 @@ import os
 import torch
 
 __all__ = [
-    "HgaError", "HgaParams", "Plan", "library", "library_path", "F32", "BF16",
+    "HgaError", "HgaParams", "Plan", "WarmCache", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
     "hga_attend_timed", "hga_attend_split", "hga_attend_split_workspace", "hga_gather_attend",
-    "hga_gather_attend_split",
+    "hga_gather_attend_split", "hga_gather_kv_cached",
     "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error",
     "hga_version", "EXPORTED_SYMBOLS",
 ]
@@ -32,7 +32,8 @@ EXPORTED_SYMBOLS = (
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
     "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_attend_split",
     "hga_attend_split_workspace", "hga_gather_attend", "hga_gather_attend_split",
-    "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error", "hga_version",
+    "hga_gather_kv_cached", "hga_block_step", "hga_prefill_blocks", "hga_status_string",
+    "hga_last_error", "hga_version",
 )
 
 
@@ -83,6 +84,8 @@ def library() -> ctypes.CDLL:
                                          vp, vp],
             "hga_route_qbar": [vp, vp, i32, i32, vp, vp, i32, vp, vp, vp],
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
+            "hga_gather_kv_cached": [vp, vp, i32, vp, vp, i64, i32, vp, vp, i32, vp, vp, vp, vp,
+                                     i32, vp, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, i64,
@@ -259,6 +262,40 @@ def hga_gather_kv(plan: Plan, group_idx, q_chunk0: int, k_src, v_src, k_routed, 
         plan.handle, _ptr(group_idx), q_chunk0, group_idx.shape[2], _ptr(k_src), _ptr(v_src),
         k_src.shape[2], int(bool(src_on_host)), _ptr(k_routed), _ptr(v_routed),
         _stream(stream)))
+
+
+class WarmCache:
+    """Device buffers of a warm LRU cache of routed groups (one partition of
+    n_slots slots per (batch, KV head)) for hga_gather_kv_cached; every map
+    entry starts at -1 (empty)."""
+
+    def __init__(self, plan: Plan, n_slots: int, src_tokens: int, device="cuda"):
+        p = plan.params
+        bh = (p.batch, p.n_kv_heads)
+        dt = _TORCH_DTYPE[p.dtype]
+        self.n_slots = n_slots
+        self.k = torch.zeros(*bh, n_slots, p.group, p.head_dim, dtype=dt, device=device)
+        self.v = torch.zeros_like(self.k)
+        i32 = torch.int32
+        self.slot_group = torch.full((*bh, n_slots), -1, dtype=i32, device=device)
+        self.slot_used = torch.full((*bh, n_slots), -1, dtype=i32, device=device)
+        self.group_slot = torch.full((*bh, src_tokens // p.group), -1, dtype=i32, device=device)
+        self.entry_slot = torch.empty((*bh, p.topk_groups), dtype=i32, device=device)
+        self.tick = 0
+
+
+def hga_gather_kv_cached(plan: Plan, group_idx, c: int, k_src, v_src, cache: WarmCache,
+                         k_routed, v_routed, n_fetched=None, src_on_host: bool = False,
+                         stream=None):
+    """hga_gather_kv for query chunk c (group_idx [B, Hkv, 1, K_g]) through
+    `cache`; the call's tick is cache.tick, which is then advanced."""
+    _check(library().hga_gather_kv_cached(
+        plan.handle, _ptr(group_idx), c, _ptr(k_src), _ptr(v_src), k_src.shape[2],
+        int(bool(src_on_host)), _ptr(cache.k), _ptr(cache.v), cache.n_slots,
+        _ptr(cache.slot_group), _ptr(cache.slot_used), _ptr(cache.group_slot),
+        _ptr(cache.entry_slot), cache.tick,
+        _ptr(k_routed), _ptr(v_routed), _ptr(n_fetched), _stream(stream)))
+    cache.tick += 1
 
 
 def hga_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v_routed, group_idx,

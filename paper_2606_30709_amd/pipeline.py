@@ -169,7 +169,7 @@ class DecodePipeline:
 
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
                  fused_route: bool = True, split_attend: bool = True, fused_gather: bool = False):
-        assert w.decode_block
+        assert w.decode_block and w.decode_blocks == 1
         self.w = w
         self.fused_route = fused_route
         # fused_gather: the host gather inside the split attention
@@ -278,3 +278,107 @@ class DecodePipeline:
             self.gather(stream)
             self.attend(stream)
         self.append(stream)
+
+
+class DecodeSequencePipeline:
+    """Consecutive 64-token decode blocks (the last ``w.decode_blocks`` chunks)
+    after a host-resident history, each routed, gathered, attended and then
+    appended before the next one, as a serving loop does.
+
+    The history K/V of the whole sequence lives in pinned host memory (only
+    chunks before the current block are ever read).  The device holds the
+    sink chunks and, compactly, every block's recent window and current
+    chunk (``res_slot`` maps chunk -> slot), the summary tables (built for
+    the history once, then appended block by block) and, with
+    ``cache_slots``, a warm LRU cache of routed groups (``hga.WarmCache``):
+    a routed group still in the cache is copied from device memory, only the
+    others cross the host link.  Without a cache every block's routed groups
+    come from host memory (``hga_gather_kv``)."""
+
+    def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
+                 cache_slots: int | None = None):
+        assert w.decode_block
+        self.w = w
+        self.plan = plan or hga.Plan.for_workload(w)
+        B, Hq, Hkv, d, C, G = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.chunk, w.group
+        f32, i32 = torch.float32, torch.int32
+        self.c0, self.n_blocks = w.q_chunk0, w.decode_blocks
+        c_end = self.c0 + self.n_blocks
+        k_all = to_device(inputs["k"], w.dtype, "cpu")
+        v_all = to_device(inputs["v"], w.dtype, "cpu")
+        self.k_hist = k_all.contiguous().pin_memory()      # cold tier: every token
+        self.v_hist = v_all.contiguous().pin_memory()
+        window = max(w.keep_last, 1 if w.force_prev else 0)
+        hot = sorted(set(range(min(w.keep_first, self.c0))) |
+                     set(range(max(0, self.c0 - window), c_end)))
+        slot = np.full(c_end, -1, dtype=np.int32)
+        for s, cc in enumerate(hot):
+            slot[cc] = s
+        self.slot_of = slot
+        self.res_slot = torch.from_numpy(slot).to(device)
+        idx = torch.tensor([t for cc in hot for t in range(cc * C, (cc + 1) * C)])
+        self.k_res = k_all[:, :, idx].contiguous().to(device)
+        self.v_res = v_all[:, :, idx].contiguous().to(device)
+        dt = self.k_res.dtype
+        q = to_device(inputs["q"], w.dtype, "cpu")           # [B, Hq, n_blocks*C, d]
+        self.q_blocks = q.reshape(B, Hq, self.n_blocks, C, d).permute(2, 0, 1, 3, 4) \
+            .contiguous().to(device)                          # [n_blocks, B, Hq, C, d]
+        self.chunk_sum = torch.zeros(B, Hkv, c_end, d, dtype=f32, device=device)
+        self.group_sum = torch.zeros(B, Hkv, c_end * (C // G), d, dtype=f32, device=device)
+        self.qbar = torch.empty(B, Hkv, 1, d, dtype=f32, device=device)
+        self.chunk_idx = torch.empty(B, Hkv, 1, w.topk_chunks, dtype=i32, device=device)
+        self.group_idx = torch.empty(self.n_blocks, B, Hkv, 1, w.topk_groups, dtype=i32,
+                                     device=device)
+        self.k_routed = torch.empty(B, Hkv, 1, w.topk_groups * G, d, dtype=dt, device=device)
+        self.v_routed = torch.empty_like(self.k_routed)
+        self.out = torch.empty_like(self.q_blocks)
+        self.lse = torch.empty(self.n_blocks, B, Hq, C, dtype=f32, device=device)
+        self.n_fetched = torch.zeros(self.n_blocks, B, Hkv, dtype=i32, device=device)
+        nbytes = hga.hga_attend_split_workspace(self.plan, 1)
+        self.attend_ws = torch.empty((nbytes + 3) // 4, dtype=f32, device=device)
+        self.cache = (hga.WarmCache(self.plan, cache_slots, self.k_hist.shape[2], device)
+                      if cache_slots else None)
+        # the history's summaries, built once from a transient device copy
+        k_dev = self.k_hist[:, :, :self.c0 * C].to(device)
+        hga.hga_build_summaries(self.plan, k_dev, 0, self.c0, self.chunk_sum, self.group_sum)
+        torch.cuda.synchronize()
+        del k_dev
+
+    def block(self, b: int, stream=None):
+        """Route, gather, attend and append block b (query chunk c0 + b)."""
+        c = self.c0 + b
+        q = self.q_blocks[b]
+        gi = self.group_idx[b]
+        hga.hga_route(self.plan, q, c, self.chunk_sum, self.group_sum, self.qbar,
+                      self.chunk_idx, gi, stream=stream)
+        if self.cache is not None:
+            hga.hga_gather_kv_cached(self.plan, gi, c, self.k_hist, self.v_hist, self.cache,
+                                     self.k_routed, self.v_routed, self.n_fetched[b],
+                                     src_on_host=True, stream=stream)
+        else:
+            hga.hga_gather_kv(self.plan, gi, c, self.k_hist, self.v_hist, self.k_routed,
+                              self.v_routed, src_on_host=True, stream=stream)
+        hga.hga_attend_split(self.plan, q, c, self.k_res, self.v_res, self.k_routed,
+                             self.v_routed, gi, self.out[b], self.attend_ws, self.lse[b],
+                             res_slot=self.res_slot, stream=stream)
+        # chunk c closes: its summaries from the resident copy (slot slot_of[c])
+        hga.hga_build_summaries(self.plan, self.k_res, c, c + 1, self.chunk_sum, self.group_sum,
+                                k_chunk0=c - int(self.slot_of[c]), stream=stream)
+
+    def reset_cache(self):
+        """Empty the warm cache (a new sequence); its tick keeps counting."""
+        if self.cache is not None:
+            for t in (self.cache.slot_group, self.cache.slot_used, self.cache.group_slot):
+                t.fill_(-1)
+
+    def step(self, stream=None):
+        for b in range(self.n_blocks):
+            self.block(b, stream)
+
+    def pcie_bytes(self) -> int:
+        """Bytes that crossed the host link for the blocks' routed groups."""
+        w = self.w
+        row = w.head_dim * w.elem_bytes
+        if self.cache is not None:
+            return int(self.n_fetched.sum().item()) * 2 * w.group * row
+        return int((self.group_idx >= 0).sum().item()) * 2 * w.group * row

@@ -63,7 +63,8 @@ class Workload:
     needle_count: int = 0
     needle_shift: float = 0.0
     needle_depths: tuple = ()  # chunk ids for needle_mode == "depths"
-    decode_block: bool = False  # True: queries are only the last chunk
+    decode_block: bool = False  # True: queries are only the last chunk(s)
+    decode_blocks: int = 1      # with decode_block: the last this many chunks are query blocks
     seed: int = 0
 
     @property
@@ -73,7 +74,7 @@ class Workload:
     @property
     def q_chunk0(self) -> int:
         """Absolute id of the first query chunk."""
-        return self.n_chunks - 1 if self.decode_block else 0
+        return self.n_chunks - self.decode_blocks if self.decode_block else 0
 
     @property
     def n_q_chunks(self) -> int:
@@ -124,6 +125,15 @@ PRESETS = {
         keep_first=2, keep_last=8, topk_chunks=20, topk_groups=32,
         needle_mode="depths", needle_depths=(102, 512, 921), needle_shift=2.0,
         decode_block=True, seed=1005),
+    # sixteen consecutive decode blocks after the same 64K history: the
+    # blocks share the needle directions (as consecutive tokens of one
+    # context share what they look up), so their routing overlaps
+    "decode64k_seq": Workload(
+        key="decode64k_seq", number=7, batch=1, n_q_heads=32, n_kv_heads=4,
+        head_dim=128, seq_len=65536 + 16 * 64, dtype="bf16", rope_base=1e6,
+        keep_first=2, keep_last=8, topk_chunks=20, topk_groups=32,
+        needle_mode="depths", needle_depths=(102, 512, 921), needle_shift=2.0,
+        decode_block=True, decode_blocks=16, seed=1007),
 }
 
 

@@ -659,6 +659,126 @@ def test_decode_fused_gather_equals_separate(hga):
             assert not torch.isnan(fused.out).any()
 
 
+class _LruModel:
+    """The warm cache's replacement rule in plain Python: per (batch, KV
+    head), hits keep their slot; misses take the slots not used in this call
+    with the oldest last use (never-used first, then the lowest slot), in
+    ascending slot order, in routed order; a repeated id is served once."""
+
+    def __init__(self, n_units, n_slots):
+        self.n_slots = n_slots
+        self.sg = [[-1] * n_slots for _ in range(n_units)]
+        self.su = [[-1] * n_slots for _ in range(n_units)]
+        self.gs = [dict() for _ in range(n_units)]
+
+    def call(self, unit, ids, lim, tick):
+        sg, su, gs = self.sg[unit], self.su[unit], self.gs[unit]
+        seen, hits, misses = set(), set(), []
+        for g in ids:
+            if not (0 <= g < lim) or g in seen:
+                continue
+            seen.add(g)
+            v = gs.get(g, -1)
+            if v >= 0 and sg[v] == g:
+                hits.add(v)
+            else:
+                misses.append(g)
+        for v in hits:
+            su[v] = tick
+        cand = sorted((su[v], v) for v in range(self.n_slots) if v not in hits)
+        victims = sorted(v for _, v in cand[:len(misses)])
+        for g, v in zip(misses, victims):
+            old = sg[v]
+            if old >= 0 and gs.get(old) == v:
+                del gs[old]
+            sg[v], gs[g], su[v] = g, v, tick
+        return len(misses)
+
+
+@pytest.mark.parametrize("slots_per_topk", [1, 4])
+def test_warm_cache_gather(hga, slots_per_topk):
+    """Consecutive decode blocks through the warm LRU cache of routed groups:
+    every block's routed buffers and outputs equal those of the uncached host
+    gather bit for bit, the per-head count of groups fetched from host memory
+    and the final slot maps follow the LRU model, every occupied slot holds
+    its group's rows, and the last block meets the oracle bar.  Run twice
+    over the sequence (the second pass starts warm)."""
+    from paper_2606_30709_amd.pipeline import DecodeSequencePipeline
+    w = W_("decode64k_seq", seq_len=8192 + 16 * 64, needle_depths=(12, 64, 115))
+    n_slots = slots_per_topk * w.topk_groups
+    _say(f"[warm cache] {n_slots} slots, {w.decode_blocks} blocks")
+    inp = W.generate(w)
+    cached = DecodeSequencePipeline(w, inp, cache_slots=n_slots)
+    plain = DecodeSequencePipeline(w, inp, plan=cached.plan)
+    B, Hkv, C, G = w.batch, w.n_kv_heads, w.chunk, w.group
+    model = _LruModel(B * Hkv, n_slots)
+    src_tokens = cached.k_hist.shape[2]
+    fetched_total = 0
+    for rep in range(2):
+        for b in range(w.decode_blocks):
+            tick = cached.cache.tick
+            cached.block(b)
+            plain.block(b)
+            torch.cuda.synchronize()
+            assert torch.equal(cached.group_idx[b], plain.group_idx[b])
+            for name in ("k_routed", "v_routed"):
+                assert torch.equal(_bits(getattr(cached, name)), _bits(getattr(plain, name))), name
+            assert torch.equal(_bits(cached.out[b]), _bits(plain.out[b]))
+            assert torch.equal(cached.lse[b], plain.lse[b])
+            c = cached.c0 + b
+            lim = min(c * (C // G), src_tokens // G)
+            gi = cached.group_idx[b].cpu().numpy()
+            got = cached.n_fetched[b].cpu().numpy()
+            for bb in range(B):
+                for j in range(Hkv):
+                    exp = model.call(bb * Hkv + j, [int(x) for x in gi[bb, j, 0]], lim, tick)
+                    assert got[bb, j] == exp, (rep, b, bb, j, got[bb, j], exp)
+                    fetched_total += exp
+        _say(f"  pass {rep}: {int(cached.n_fetched.sum())} of "
+             f"{int((cached.group_idx >= 0).sum())} routed groups fetched from host")
+    sg = cached.cache.slot_group.cpu().numpy().reshape(B * Hkv, n_slots)
+    assert sg.tolist() == model.sg
+    kh = cached.k_hist
+    ck = cached.cache.k.cpu()
+    for bb in range(B):
+        for j in range(Hkv):
+            for v in range(n_slots):
+                g = int(sg[bb * Hkv + j, v])
+                if g >= 0:
+                    assert torch.equal(_bits(ck[bb, j, v]), _bits(kh[bb, j, g * G:(g + 1) * G]))
+    # the last block against the oracle
+    b = w.decode_blocks - 1
+    c = cached.c0 + b
+    q64, k64, v64 = (f64(inp[x], w.dtype) for x in "qkv")
+    gi_all = cached.group_idx[:, :, :, 0].permute(1, 2, 0, 3).cpu().numpy()   # [B, Hkv, nb, K]
+    units = [(bb, j, b) for bb in range(B) for j in range(Hkv)]
+    o_ref, l_ref = O.attend(q64, k64, v64, gi_all, list(range(cached.c0, cached.c0 + w.decode_blocks)),
+                            C, G, w.keep_first, w.keep_last, w.force_prev, units=units)
+    eo = np.max(np.abs(tensor_to_f64(cached.out[b]) - o_ref[:, :, b * C:(b + 1) * C]))
+    el = np.max(np.abs(tensor_to_f64(cached.lse[b]) - l_ref[:, :, b * C:(b + 1) * C]))
+    _say(f"  block {c}: out {eo:.3g} lse {el:.3g}")
+    assert eo <= OUT_TOL[w.dtype] and el <= LSE_TOL[w.dtype]
+    # planted repeats and invalid ids in one call
+    gi = cached.group_idx[b].clone()
+    gi[0, 0, 0, 1] = gi[0, 0, 0, 0]
+    gi[0, 1, 0, 2] = -1
+    gi[0, 2, 0, 3] = 10 ** 6
+    kr, vr = torch.empty_like(cached.k_routed), torch.empty_like(cached.v_routed)
+    tick = cached.cache.tick
+    hga.hga_gather_kv_cached(cached.plan, gi, c, cached.k_hist, cached.v_hist, cached.cache,
+                             kr, vr, cached.n_fetched[0], src_on_host=True)
+    kp, vp = torch.empty_like(kr), torch.empty_like(vr)
+    hga.hga_gather_kv(cached.plan, gi, c, cached.k_hist, cached.v_hist, kp, vp, src_on_host=True)
+    torch.cuda.synchronize()
+    assert torch.equal(_bits(kr), _bits(kp)) and torch.equal(_bits(vr), _bits(vp))
+    got = cached.n_fetched[0].cpu().numpy()
+    lim = min(c * (C // G), src_tokens // G)
+    gnp = gi.cpu().numpy()
+    for bb in range(B):
+        for j in range(Hkv):
+            assert got[bb, j] == model.call(bb * Hkv + j, [int(x) for x in gnp[bb, j, 0]], lim, tick)
+
+
 def test_decode_block_parity_reduced(hga):
     w = W_("decode64k", seq_len=8192 + 64, needle_depths=(12, 64, 115))
     _decode_check(hga, w)
