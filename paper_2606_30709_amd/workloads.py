@@ -125,6 +125,14 @@ PRESETS = {
         keep_first=2, keep_last=8, topk_chunks=20, topk_groups=32,
         needle_mode="depths", needle_depths=(102, 512, 921), needle_shift=2.0,
         decode_block=True, seed=1005),
+    # a context beyond 64K: 2037 routable middle chunks per unit (needles at
+    # 10/50/90% depth, as in decode64k)
+    "decode128k": Workload(
+        key="decode128k", number=8, batch=1, n_q_heads=32, n_kv_heads=4,
+        head_dim=128, seq_len=131072 + 64, dtype="bf16", rope_base=1e6,
+        keep_first=2, keep_last=8, topk_chunks=20, topk_groups=32,
+        needle_mode="depths", needle_depths=(204, 1024, 1843), needle_shift=2.0,
+        decode_block=True, seed=1008),
     # sixteen consecutive decode blocks after the same 64K history: the
     # blocks share the needle directions (as consecutive tokens of one
     # context share what they look up), so their routing overlaps

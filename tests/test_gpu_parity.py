@@ -784,6 +784,13 @@ def test_decode_block_parity_reduced(hga):
     _decode_check(hga, w)
 
 
+def test_decode_block_parity_128k(hga):
+    """A context beyond 64K: 2037 routable chunks per unit (the wide route's
+    selection with two candidates per thread), history of 131,072 tokens in
+    pinned host memory."""
+    _decode_check(hga, W.preset("decode128k"))
+
+
 def test_decode_block_parity_full(hga):
     pipe = _decode_check(hga, W.preset("decode64k"))
     # host-sourced gather equals a device-sourced gather of the same history

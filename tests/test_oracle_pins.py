@@ -314,7 +314,8 @@ def test_fetched_tokens_closed_form_and_budget(key):
     budget = {"tiny": 0.25, "smalllm": 0.03125, "train12k": 0.03125, "qwen32k": 0.03125,
               "qwen32k_chunks": (2 + 8 + 16 + 1) * 64 / 32768,
               "decode64k": 1216 / 65600,
-              "decode64k_seq": 1216 / (65536 + 16 * 64)}[key]
+              "decode64k_seq": 1216 / (65536 + 16 * 64),
+              "decode128k": 1216 / (131072 + 64)}[key]
     assert frac == pytest.approx(budget, rel=1e-12)
 
 
