@@ -331,6 +331,58 @@ def attend(q_rot: np.ndarray, k_rot: np.ndarray, v: np.ndarray, group_idx: np.nd
     return out, lse
 
 
+def attend_backward(q_rot: np.ndarray, k_rot: np.ndarray, v: np.ndarray, dout: np.ndarray,
+                    group_idx: np.ndarray, q_chunk_ids, chunk: int, group: int,
+                    keep_first: int, keep_last: int, force_prev: int, units=None):
+    """Gradients of the exact-token attention of ``attend`` (Sec. 3.4,
+    Eq. (1)) with respect to its inputs, for the output gradient ``dout``
+    [B, Hq, nq*chunk, d].  Routing is not differentiated (the selected sets
+    are fixed); the routed rows are the resident rows they were gathered
+    from, so their gradients land on those token rows.
+
+    For query row i of a unit with working set X (visible chunks, opened
+    groups, current-chunk tokens u <= t) and logits s_ix = q_i.k_x / sqrt(d),
+    p_ix = softmax_x(s_ix), o_i = sum_x p_ix v_x, the chain rule gives
+        dv_x += sum_i p_ix dout_i,
+        dp_ix = dout_i . v_x,   D_i = sum_x p_ix dp_ix = dout_i . o_i,
+        ds_ix = p_ix (dp_ix - D_i),
+        dq_i = sum_x ds_ix k_x / sqrt(d),   dk_x += sum_i ds_ix q_i / sqrt(d).
+    Returns (dq like q_rot, dk and dv like k_rot), float64; rows of query
+    units not listed in ``units`` get no contribution (dq stays zero there).
+    """
+    B, Hq, T, d = q_rot.shape
+    Hkv = k_rot.shape[1]
+    r = Hq // Hkv
+    dq = np.zeros((B, Hq, T, d))
+    dk = np.zeros(k_rot.shape)
+    dv = np.zeros(v.shape)
+    scale = 1.0 / math.sqrt(d)
+    if units is None:
+        units = [(b, j, i) for b in range(B) for j in range(Hkv) for i in range(len(q_chunk_ids))]
+    causal = np.tril(np.ones((chunk, chunk), dtype=bool))
+    for (b, j, i) in units:
+        c = int(q_chunk_ids[i])
+        hist = working_set(c, group_idx[b, j, i], chunk, group, keep_first, keep_last, force_prev)
+        cur = np.arange(c * chunk, (c + 1) * chunk)
+        idx = np.concatenate([hist, cur])
+        keys = np.asarray(k_rot[b, j, idx], dtype=np.float64)          # [X, d]
+        vals = np.asarray(v[b, j, idx], dtype=np.float64)
+        rows = slice(i * chunk, (i + 1) * chunk)
+        qs = np.asarray(q_rot[b, j * r:(j + 1) * r, rows], dtype=np.float64)   # [r, C, d]
+        go = np.asarray(dout[b, j * r:(j + 1) * r, rows], dtype=np.float64)
+        logits = (qs @ keys.T) * scale                                  # [r, C, X]
+        logits[:, :, hist.size:][:, ~causal] = -np.inf
+        p = np.exp(logits - logits.max(axis=-1, keepdims=True))
+        p /= p.sum(axis=-1, keepdims=True)
+        dp = go @ vals.T                                                # [r, C, X]
+        big_d = (p * dp).sum(axis=-1, keepdims=True)
+        ds = p * (dp - big_d)
+        dq[b, j * r:(j + 1) * r, rows] = (ds @ keys) * scale
+        np.add.at(dk[b, j], idx, np.einsum("hcx,hcd->xd", ds, qs) * scale)
+        np.add.at(dv[b, j], idx, np.einsum("hcx,hcd->xd", p, go))
+    return dq, dk, dv
+
+
 def fetched_tokens(c: int, n_groups: int, chunk: int, group: int, keep_first: int,
                    keep_last: int, force_prev: int) -> int:
     """Size of the closed-history working set of chunk c with n_groups opened

@@ -79,6 +79,83 @@ def test_full_coverage_is_dense_causal_attention(B, Hq, Hkv, N, d, base, F, L):
     assert np.max(np.abs(res["lse"] - ref_lse)) < 1e-12
 
 
+def _sdpa_dense_grads(q, k, v, dout):
+    """Gradients of dense causal attention by torch autograd of its own SDPA
+    in float64 on CPU (K/V repeated over the r query heads of a KV head; the
+    repeat's backward sums them back)."""
+    r = q.shape[1] // k.shape[1]
+    qt = torch.from_numpy(q).requires_grad_(True)
+    kt = torch.from_numpy(k).requires_grad_(True)
+    vt = torch.from_numpy(v).requires_grad_(True)
+    out = torch.nn.functional.scaled_dot_product_attention(
+        qt, kt.repeat_interleave(r, dim=1), vt.repeat_interleave(r, dim=1), is_causal=True)
+    out.backward(torch.from_numpy(dout))
+    return qt.grad.numpy(), kt.grad.numpy(), vt.grad.numpy()
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,N,d,base,F,L", [
+    (1, 2, 2, 512, 64, 1e4, 1, 0),      # MHA, d64
+    (1, 8, 1, 512, 128, 1e6, 1, 2),     # GQA 8:1, d128
+])
+def test_backward_full_coverage_is_dense_gradient(B, Hq, Hkv, N, d, base, F, L):
+    """With every chunk and group routed, the attention backward must give
+    the gradients of dense causal attention (torch autograd of SDPA)."""
+    rng = np.random.default_rng(11)
+    q, k, v = _rand_qkv(rng, B, Hq, Hkv, N, d, base)
+    dout = rng.standard_normal(q.shape)
+    C, G = 64, 16
+    nc = N // C
+    res = O.hga_forward(q, k, v, chunk=C, group=G, keep_first=F, keep_last=L, force_prev=1,
+                        topk_chunks=nc, topk_groups=nc * C // G, rope_base=base)
+    dq, dk, dv = O.attend_backward(q, k, v, dout, res["group_idx"], list(range(nc)), C, G, F, L,
+                                   1)
+    rq, rk, rv = _sdpa_dense_grads(q, k, v, dout)
+    assert np.max(np.abs(dq - rq)) < 1e-11
+    assert np.max(np.abs(dk - rk)) < 1e-11
+    assert np.max(np.abs(dv - rv)) < 1e-11
+
+
+def test_backward_matches_finite_differences():
+    """Routed backward against central differences of the oracle's own
+    forward (loss = sum of dout * out) on a tiny case whose routing drops
+    chunks and groups: a dropped term, a wrong sign or a transposed operand
+    anywhere in the chain rule moves some entry by far more than 1e-6."""
+    rng = np.random.default_rng(5)
+    B, Hq, Hkv, N, d, base = 1, 4, 2, 320, 8, 1e4
+    C, G, F, L, Kc, Kg = 32, 8, 1, 1, 2, 3
+    q, k, v = _rand_qkv(rng, B, Hq, Hkv, N, d, base)
+    dout = rng.standard_normal(q.shape)
+    nc = N // C
+    res = O.hga_forward(q, k, v, chunk=C, group=G, keep_first=F, keep_last=L, force_prev=1,
+                        topk_chunks=Kc, topk_groups=Kg, rope_base=base)
+    gi = res["group_idx"]
+    assert (gi[0, 0, nc - 1] >= 0).sum() == Kg       # a real budget: groups are dropped
+    ids = list(range(nc))
+
+    def loss(q_, k_, v_):
+        out, _ = O.attend(q_, k_, v_, gi, ids, C, G, F, L, 1)
+        return float(np.sum(out * dout))
+
+    dq, dk, dv = O.attend_backward(q, k, v, dout, gi, ids, C, G, F, L, 1)
+    h = 1e-6
+    for name, x, g in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        flat = x.reshape(-1)
+        picks = rng.choice(flat.size, size=40, replace=False)
+        # also the rows of a routed group and of the sink chunk
+        if name != "q":
+            g0 = int(gi[0, 0, nc - 1, 0])
+            picks = np.concatenate([picks, [(g0 * G) * d + 3, 5 * d + 1]])
+        for e in picks:
+            old = flat[e]
+            flat[e] = old + h
+            lp = loss(q, k, v)
+            flat[e] = old - h
+            lm = loss(q, k, v)
+            flat[e] = old
+            num = (lp - lm) / (2 * h)
+            assert abs(num - g.reshape(-1)[e]) < 1e-6 * max(1.0, abs(num)), (name, e)
+
+
 def test_attention_matches_scalar_loops_of_eq1():
     """Tiny case against Eq. (1) written as scalar Python loops, with a
     routing budget that actually drops chunks: the loops visit exactly the
