@@ -350,6 +350,35 @@ hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_c
  * NULL or invalid plan or n_q_chunks < 0. */
 int64_t hga_attend_split_workspace(const hga_plan* plan, int32_t n_q_chunks);
 
+/* Backward of hga_attend (Sec. 3.4, Eq. (1)) for the prefill layout and the
+ * bf16 plan dtype: the gradients of the attention outputs with respect to
+ * the rotated queries and the resident keys and values, the routing held
+ * fixed (it is not differentiable).  For query row i of query chunk c and
+ * key x of its working set (visible chunks, the routed groups of group_idx
+ * valid as in hga_attend, the current chunk's tokens u <= t), with
+ * p = exp(q_i.k_x/sqrt(d) - lse_i), D_i = dout_i . out_i,
+ * ds = p (dout_i . v_x - D_i):
+ *   dq_i = sum_x ds k_x / sqrt(d)                  (written)
+ *   dk_x += sum_i ds q_i / sqrt(d), dv_x += sum_i p dout_i   (accumulated)
+ * A routed row is resident token g*group + o, so its gradients land there.
+ *   q_rot, out, dout  [batch, n_q_heads, n_q_chunks*chunk, head_dim] bf16:
+ *               out and lse are hga_attend's results for these inputs
+ *   k_res,v_res [batch, n_kv_heads, res_tokens, head_dim] bf16, token-indexed
+ *               ((q_chunk0 + n_q_chunks) * chunk <= res_tokens)
+ *   group_idx   as for hga_attend
+ *   lse         fp32 [batch, n_q_heads, n_q_chunks*chunk] (required)
+ *   dq          fp32 like q_rot, written
+ *   dk, dv      fp32 [batch, n_kv_heads, res_tokens, head_dim], ADDED INTO
+ *               (zero them for a plain gradient; the sums over query units
+ *               are fp32 atomic adds, so their order, and the last bits, may
+ *               vary from call to call)
+ * HGA_EUNSUPPORTED for an fp32 plan; other errors as hga_attend. */
+hga_status hga_attend_backward(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                               int32_t n_q_chunks, const void* k_res, const void* v_res,
+                               int64_t res_tokens, const int32_t* group_idx, const void* out,
+                               const float* lse, const void* dout, float* dq, float* dk,
+                               float* dv, void* stream);
+
 /* hga_gather_kv followed by hga_attend_split, as one pass, for any layout
  * (Sec. 4.3 gather, Sec. 3.4 attention): the workgroups of a unit's routed
  * tiles copy the routed groups' rows straight from k_src/v_src (rows

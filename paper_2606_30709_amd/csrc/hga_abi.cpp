@@ -634,6 +634,33 @@ hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int3
                     "hga_gather_attend_split launch");
 }
 
+hga_status hga_attend_backward(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                               int32_t n_q_chunks, const void* k_res, const void* v_res,
+                               int64_t res_tokens, const int32_t* group_idx, const void* out,
+                               const float* lse, const void* dout, float* dq, float* dk,
+                               float* dv, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
+    if (plan->p.dtype != HGA_BF16)
+        return fail(HGA_EUNSUPPORTED, "the attention backward is built for bf16 plans");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, nullptr,
+                         k_res, v_res, group_idx, out, lse));
+    if (!lse) return fail(HGA_EINVAL, "lse (the forward's log-sum-exp) is required");
+    HGA_TRY(check_tensor(dout, "dout"));
+    HGA_TRY(check_tensor(dq, "dq"));
+    HGA_TRY(check_tensor(dk, "dk"));
+    HGA_TRY(check_tensor(dv, "dv"));
+    if (hga::attend_backward_lds_bytes(*plan) > static_cast<size_t>(plan->max_lds))
+        return fail(HGA_EUNSUPPORTED, "the backward's LDS tiles exceed the device limit");
+    clear_stale_error();
+    return launched(hga::launch_attend_backward(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+                                                res_tokens, group_idx, out, lse, dout, dq, dk, dv,
+                                                static_cast<hipStream_t>(stream)),
+                    "hga_attend_backward launch");
+}
+
 hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                              int32_t n_q_chunks, const void* k_res, const void* v_res,
                              int64_t res_tokens, const int32_t* group_idx, void* k_routed,

@@ -101,6 +101,15 @@ hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_ch
                                float* lse, void* workspace, int64_t workspace_bytes,
                                hipStream_t stream);
 
+// Backward of the attention (bf16): dq written, dk and dv (fp32, resident
+// layout) accumulated into.
+size_t attend_backward_lds_bytes(const hga_plan& plan);
+hipError_t launch_attend_backward(const hga_plan& plan, const void* q_rot, int q_chunk0,
+                                  int n_q_chunks, const void* k_res, const void* v_res,
+                                  int64_t res_tokens, const int32_t* group_idx, const void* out,
+                                  const float* lse, const void* dout, float* dq, float* dk,
+                                  float* dv, hipStream_t stream);
+
 // The gather fused into the split attention: routed rows copied from
 // k_src / v_src (src_tokens rows per head, device memory or the device
 // mapping of pinned host memory) and written to k_routed / v_routed; the

@@ -19,7 +19,7 @@ __all__ = [
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
     "hga_attend_timed", "hga_attend_split", "hga_attend_split_workspace", "hga_gather_attend",
-    "hga_gather_attend_split", "hga_gather_kv_cached",
+    "hga_gather_attend_split", "hga_gather_kv_cached", "hga_attend_backward",
     "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error",
     "hga_version", "EXPORTED_SYMBOLS",
 ]
@@ -32,7 +32,8 @@ EXPORTED_SYMBOLS = (
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
     "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_attend_split",
     "hga_attend_split_workspace", "hga_gather_attend", "hga_gather_attend_split",
-    "hga_gather_kv_cached", "hga_block_step", "hga_prefill_blocks", "hga_status_string",
+    "hga_gather_kv_cached", "hga_attend_backward", "hga_block_step", "hga_prefill_blocks",
+    "hga_status_string",
     "hga_last_error", "hga_version",
 )
 
@@ -91,6 +92,8 @@ def library() -> ctypes.CDLL:
             "hga_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, i64,
                                  vp],
             "hga_gather_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp],
+            "hga_attend_backward": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp,
+                                    vp],
             "hga_gather_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, i64, i32, vp,
                                         vp, vp, vp, vp, vp, i64, vp],
             "hga_block_step": [vp, vp, i32, vp, vp, i64, vp, vp, i32, vp, vp, vp, vp, vp, vp,
@@ -354,6 +357,17 @@ def hga_gather_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_sr
         _ptr(res_slot), _ptr(k_src), _ptr(v_src), k_src.shape[2], 1 if src_on_host else 0,
         _ptr(group_idx), _ptr(k_routed), _ptr(v_routed), _ptr(out), _ptr(lse),
         _ptr(workspace), nbytes, _stream(stream)))
+
+
+def hga_attend_backward(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx, out, lse,
+                        dout, dq, dk, dv, stream=None):
+    """Gradients of hga_attend (bf16, prefill layout): dq [B, Hq, nq*C, d]
+    fp32 written; dk, dv [B, Hkv, res_tokens, d] fp32 added into."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_attend_backward(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(group_idx), _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+        _stream(stream)))
 
 
 def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx, k_routed,

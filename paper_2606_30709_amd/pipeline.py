@@ -108,6 +108,17 @@ class PrefillPipeline:
                               self.k_routed, self.v_routed, self.out, self.lse,
                               start_event=start_event, stop_event=stop_event, stream=stream)
 
+    def backward(self, dout, stream=None):
+        """Gradients of the attention of the last ``step`` for output gradient
+        ``dout`` (like ``out``): returns (dq, dk, dv), fp32, dk and dv in
+        the resident K/V layout (routing held fixed)."""
+        dq = torch.empty(self.q.shape, dtype=torch.float32, device=self.q.device)
+        dk = torch.zeros(self.k.shape, dtype=torch.float32, device=self.k.device)
+        dv = torch.zeros_like(dk)
+        hga.hga_attend_backward(self.plan, self.q, 0, self.k, self.v, self.group_idx, self.out,
+                                self.lse, dout, dq, dk, dv, stream=stream)
+        return dq, dk, dv
+
     def step(self, stream=None):
         self.summaries(stream)
         self.route(stream)

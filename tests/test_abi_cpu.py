@@ -94,6 +94,8 @@ def test_calls_reject_null_plan():
                                        None, None, None, None, None, None, 0, None) == -1
     assert lib.hga_gather_kv_cached(None, None, 0, None, None, 0, 0, None, None, 0, None, None,
                                     None, None, 0, None, None, None, None) == -1
+    assert lib.hga_attend_backward(None, None, 0, 0, None, None, 0, None, None, None, None, None,
+                                   None, None, None) == -1
     assert lib.hga_gather_attend(None, None, 0, 0, None, None, 0, None, None, None, None, None,
                                  None, None, None) == -1
     assert lib.hga_block_step(None, None, 0, None, None, 0, None, None, 0, None, None, None,

@@ -17,7 +17,7 @@ torch = pytest.importorskip("torch")
 from oracle import hga_oracle as O  # noqa: E402
 from paper_2606_30709_amd import workloads as W  # noqa: E402
 
-from parity_util import (LSE_TOL, OUT_TOL, SelectionReport, check_selection, f64,  # noqa: E402
+from parity_util import (BWD_TOL, LSE_TOL, OUT_TOL, SelectionReport, check_selection, f64,  # noqa: E402
                          score_bounds, summary_bound, tensor_to_f64)
 
 pytestmark = pytest.mark.gpu
@@ -327,6 +327,42 @@ def test_gather_attend_equals_separate_calls(hga, key):
 
 SPLIT_CASES = {k: SMALL[k] for k in ("qwen_4k_ragged", "qwen_g8", "qwen_g32", "gqa3_d64",
                                      "mha_d128", "f32_d128_gqa")}
+
+
+BWD_CASES = {k: SMALL[k] for k in ("smalllm_2k", "gqa3_d64", "qwen_4k_ragged", "qwen_g8",
+                                   "qwen_g32", "mha_d128", "qwen_chunks_4k")}
+
+
+@pytest.mark.parametrize("key", list(BWD_CASES))
+def test_attend_backward_matches_oracle(hga, key):
+    """hga_attend_backward against the oracle's chain rule (float64, on the
+    GPU's routing and with a seeded output gradient): dq, dk, dv within the
+    bar derived from the bf16 rounding of the weights and of dS."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = BWD_CASES[key]
+    _say(f"[backward] {key}")
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    pipe.step()
+    rng = np.random.default_rng(77)
+    dout_f = rng.standard_normal(pipe.q.shape).astype(np.float32)
+    dout = torch.from_numpy(dout_f).to(torch.bfloat16).cuda()
+    dq, dk, dv = pipe.backward(dout)
+    torch.cuda.synchronize()
+    q64, k64, v64 = (f64(inp[x], w.dtype) for x in "qkv")
+    go = dout.float().cpu().numpy().astype(np.float64)
+    rq, rk, rv = O.attend_backward(
+        q64, k64, v64, go, pipe.group_idx.cpu().numpy(), list(range(w.n_chunks)), w.chunk,
+        w.group, w.keep_first, w.keep_last, w.force_prev)
+    for name, g, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        g = g.cpu().numpy().astype(np.float64)
+        assert np.isfinite(g).all(), name
+        err = np.max(np.abs(g - ref))
+        scale = np.max(np.abs(ref))
+        rel = np.linalg.norm(g - ref) / np.linalg.norm(ref)
+        _say(f"  {name}: max-abs {err:.3g} of max {scale:.3g} ({err / scale:.3g}), "
+             f"normwise {rel:.3g}")
+        assert err <= BWD_TOL * scale and rel <= BWD_TOL / 4, name
 
 
 @pytest.mark.parametrize("key", list(SPLIT_CASES))
