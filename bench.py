@@ -87,6 +87,12 @@ def algorithmic_bytes(w, n_valid_rows: int) -> dict:
     }
 
 
+def _prefill_label(w) -> str:
+    return (f"B{w.batch} H{w.n_q_heads}/{w.n_kv_heads} d{w.head_dim} N{w.seq_len} {w.dtype} "
+            f"C{w.chunk} G{w.group} F{w.keep_first} L{w.keep_last} Kc{w.topk_chunks} "
+            f"Kg{w.topk_groups}")
+
+
 def attention_flops(w, group_idx: np.ndarray) -> float:
     """Exact-attention FLOPs of a step: 4*d per (query, key) pair (QK^T and PV)."""
     C, G, d, r = w.chunk, w.group, w.head_dim, w.gqa_ratio
@@ -342,6 +348,62 @@ def decode_sequence_bench(w, inp, args):
     print(json.dumps(res), flush=True)
 
 
+def backward_bench(w, inp, args):
+    """The attention backward (hga_attend_backward) of a prefill preset: after
+    one forward step, each timed step zeroes dk, dv and computes dq, dk, dv
+    for a fixed output gradient.  Roofline: 10*d FLOP per (query, key) pair
+    (S recomputed, dP, dQ, dK, dV) against the bf16 matrix-core peak."""
+    import torch
+
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    pipe = PrefillPipeline(w, inp)
+    pipe.step()
+    torch.cuda.synchronize()
+    gen = np.random.default_rng(w.seed + 99)
+    dout = torch.from_numpy(gen.standard_normal(pipe.q.shape).astype(np.float32)).to(
+        torch.bfloat16).cuda()
+    for _ in range(args.warmup):
+        pipe.backward(dout)
+    torch.cuda.synchronize()
+    K = args.steps
+    t0 = time.perf_counter()
+    for _ in range(K):
+        pipe.backward(dout)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / K
+    # the kernel alone, between events (allocation and zeroing outside)
+    from paper_2606_30709_amd import hga
+    dq = torch.empty(pipe.q.shape, dtype=torch.float32, device="cuda")
+    dk = torch.zeros(pipe.k.shape, dtype=torch.float32, device="cuda")
+    dv = torch.zeros_like(dk)
+    times = []
+    for _ in range(max(5, K // 4)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        hga.hga_attend_backward(pipe.plan, pipe.q, 0, pipe.k, pipe.v, pipe.group_idx, pipe.out,
+                                pipe.lse, dout, dq, dk, dv)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e-3)
+    ksec = float(np.median(times))
+    flops = 2.5 * attention_flops(w, pipe.group_idx.cpu().numpy())
+    res = {
+        "metric": "routed-attn backward tokens/s per layer",
+        "value": round(w.batch * w.seq_len / dt, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(dt * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.key}: attention backward " + _prefill_label(w),
+                   "seed": inp["seed"]},
+        "kernel_us": round(ksec * 1e6, 2),
+        "roofline": {"bound": "mfma", "achieved": round(flops / ksec / 1e12, 2),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(flops / ksec / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "alg_flops_per_launch": flops, "traffic": None},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def blockwise_bench(w, inp, args):
     """The prompt as a sequence of 64-token blocks (hga_prefill_blocks: per
     block, routing against the chunks closed so far, gather + attention,
@@ -403,6 +465,8 @@ def main():
     ap.add_argument("--cache-slots", type=int, default=0,
                     help="decode sequence: warm-cache slots per (batch, KV head) "
                          "(default 8 x topk_groups)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the attention backward (hga_attend_backward) of the workload")
     ap.add_argument("--block-exact", action="store_true",
                     help="with --blockwise: the single-workgroup attention whose outputs are "
                          "bit-identical to the bulk prefill's (default: the split attention)")
@@ -433,6 +497,9 @@ def main():
         return
     if args.blockwise:
         blockwise_bench(w, inp, args)
+        return
+    if args.backward:
+        backward_bench(w, inp, args)
         return
     if args.probe_traffic:
         probe_traffic(w, inp, args.gather)
@@ -596,9 +663,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": {
-            "workload": (f"{w.key}: prefill B{w.batch} H{w.n_q_heads}/{w.n_kv_heads} "
-                         f"d{w.head_dim} N{w.seq_len} {w.dtype} C{w.chunk} G{w.group} "
-                         f"F{w.keep_first} L{w.keep_last} Kc{w.topk_chunks} Kg{w.topk_groups}"),
+            "workload": f"{w.key}: prefill " + _prefill_label(w),
             "batch": w.batch, "seq_len": w.seq_len, "tokens_per_step": tokens,
             "seed": inp["seed"],
         },

@@ -11,18 +11,24 @@
 // key/value gradients land on those rows.
 //
 // Work item: (unit, part): a workgroup of NW wavefronts takes NW query tiles
-// of 32 rows of the unit's r*64 (as the forward packs them).  Every matrix
-// product reads its operands as 16-byte rows of row-major LDS tiles (A as
-// [m][k], B as B^T [n][k]): per 64-key tile the workgroup stages K and V
-// row-major and K transposed; per 32-key sub-tile each wavefront
-//   S^T = K.Q^T and dP^T = V.dO^T   (Q and dO fragments in registers),
+// of 32 rows of the unit's r*64 (as the forward packs them).  Per 64-key tile
+// the workgroup stages K and V row-major and K transposed in LDS; per 32-key
+// sub-tile each wavefront computes, for its own 32 queries,
+//   S^T = K.Q^T and dP^T = V.dO^T   (B operands: the wave's Q, dO rows in LDS),
 //   P^T, dS^T elementwise           (each lane owns one query column),
-//   dS, dS^T, P^T to its LDS scratch (bf16),
-//   dQ += dS.K                      (registers, over all tiles),
-//   dK += dS^T.Q, dV += P^T.dO      (fragments of Q^T, dO^T in registers),
-// and adds its dK, dV rows into the workgroup's fp32 LDS accumulators.  After
-// the tile the accumulators are added into the global fp32 dk, dv with
-// hardware atomics (other units share visible chunks and routed groups).
+//   dQ += dS.K                      (A = the lane's own dS values, in registers),
+// and writes dS^T and P^T to its LDS scratch.  The key gradients of the
+// sub-tile sum over every query of the workgroup, so after one barrier the
+// 2*D/32 blocks (dK or dV, 32 dimensions) are split among the wavefronts:
+// each contracts the scratch of all wavefronts against Q^T / dO^T fragments
+// it gathered into registers once, and adds its blocks into the global fp32
+// dk, dv with hardware atomics (other units share visible chunks and routed
+// groups).  No two wavefronts accumulate into the same LDS words.
+//
+// A product's contraction index may be permuted as long as both operands use
+// the same permutation: dQ's A operand is the lane's own dS^T column (keys in
+// the order of the accumulator layout) and its B operand reads K^T in that
+// same key order.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -33,6 +39,7 @@ namespace hga {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int KT = 64;    // keys per tile (= chunk)
@@ -41,21 +48,23 @@ constexpr int SCR = 40;   // row stride (bf16) of the 32 x 32 scratch tiles
 template <int D, int NW>
 struct BwdLayout {
     static constexpr int KS = D + 8;        // row stride (bf16) of K, V, Q, dO tiles
-    static constexpr int TS = KT + 8;       // row stride (bf16) of the K^T tile
-    static constexpr int AS = D + 4;        // row stride (fp32) of the dK, dV accumulators
+    static constexpr int TS = KT + 4;       // row stride (bf16) of the K^T tile
     static constexpr int kK = 0;
     static constexpr int kV = kK + KT * KS * 2;
     static constexpr int kKT = kV + KT * KS * 2;
     static constexpr int kQ = kKT + D * TS * 2;                  // NW x (Q, dO) rows
-    static constexpr int kScr = kQ + NW * 2 * 32 * KS * 2;       // NW x 3 scratch tiles
-    static constexpr int kAcc = kScr + NW * 3 * 32 * SCR * 2;    // dK then dV, 32 rows, fp32
-    static constexpr int kTok = kAcc + 2 * 32 * AS * 4;          // tile row -> token
-    static constexpr int kGid = kTok + KT * 4;
+    static constexpr int kScr = kQ + NW * 2 * 32 * KS * 2;       // NW x 2 buffers x (dS^T, P^T)
+    static constexpr int kTok = kScr + NW * 4 * 32 * SCR * 2;    // 2 x (tile row -> token)
+    static constexpr int kGid = kTok + 2 * KT * 4;
     static constexpr int kBytes = kGid + kMaxTopK * 4;
 };
 
 __device__ __forceinline__ bf16x8_t frag(const bf16_t* p) {
     return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const vec16*>(p));
+}
+
+__device__ __forceinline__ bf16x4_t frag4(const bf16_t* p) {
+    return *reinterpret_cast<const bf16x4_t*>(p);
 }
 
 __device__ __forceinline__ float add_halves(float x) {
@@ -64,9 +73,10 @@ __device__ __forceinline__ float add_halves(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+// Workgroup barrier that orders LDS only: waits for this wave's LDS
+// operations, not for its global atomics (which nothing here reads back).
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int D, int NW>
@@ -81,13 +91,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     constexpr int NKS = D / 16;   // 16-wide k-steps over d
     constexpr int NDT = D / 32;   // 32-wide blocks of d
     constexpr int VPR = D / 8;    // 16-byte vectors per row
+    constexpr int IPW = 2 * NDT / NW;  // key-gradient blocks per wave
+    static_assert(IPW >= 1 && IPW * NW == 2 * NDT, "blocks must split evenly");
     extern __shared__ __align__(16) unsigned char smem[];
     bf16_t* sK = reinterpret_cast<bf16_t*>(smem + Lay::kK);
     bf16_t* sV = reinterpret_cast<bf16_t*>(smem + Lay::kV);
     bf16_t* sKT = reinterpret_cast<bf16_t*>(smem + Lay::kKT);
-    float* sdK = reinterpret_cast<float*>(smem + Lay::kAcc);
-    float* sdV = sdK + 32 * Lay::AS;
-    int* s_tok = reinterpret_cast<int*>(smem + Lay::kTok);
+    bf16_t* sQall = reinterpret_cast<bf16_t*>(smem + Lay::kQ);
+    bf16_t* scr_all = reinterpret_cast<bf16_t*>(smem + Lay::kScr);
+    int* s_tok_all = reinterpret_cast<int*>(smem + Lay::kTok);
     int* s_gid = reinterpret_cast<int*>(smem + Lay::kGid);
 
     const int item = blockIdx.x;
@@ -103,6 +115,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     const int nqt = 2 * r;
     const int qtile = part * NW + wave;
     const bool qactive = qtile < nqt;
+    // query tiles of this workgroup that hold queries (a prefix of its waves)
+    const int nqa = min(NW, nqt - part * NW);
     const int routed_rows = topk_groups * group;
     const int64_t qtok = static_cast<int64_t>(n_q_chunks) * KT;
     const int n_q_heads = r * n_kv;
@@ -121,12 +135,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
         s_gid[s] = group_idx[static_cast<int64_t>(unit) * topk_groups + s];
 
     // The wave's 32 rows of Q and dO stay in LDS, row-major: the B fragments
-    // of S^T = K.Q^T and dP^T = V.dO^T are 16-byte row reads.  The B
-    // fragments of Q^T and dO^T ([n = d][k = query], for dK and dV) are
-    // column reads, done once into registers.
-    bf16_t* sQ = reinterpret_cast<bf16_t*>(smem + Lay::kQ) + wave * 2 * 32 * Lay::KS;
+    // of S^T = K.Q^T and dP^T = V.dO^T are 16-byte row reads.
+    bf16_t* sQ = sQall + wave * 2 * 32 * Lay::KS;
     bf16_t* sG = sQ + 32 * Lay::KS;
-    bf16x8_t qt[NDT][2], gt[NDT][2];
     float dsum = 0.f, lse2 = 0.f;
     if (qactive) {
         const bf16_t* qp = q_rot + my_row * D;
@@ -147,21 +158,29 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
         dsum = add_halves(acc);
         lse2 = lse[my_row] * 1.4426950408889634f;
     }
-    wave_lds_sync();
-    if (qactive) {
-        // Q^T fragment (nb, ks): lane holds Q[ks*16 + half*8 + e][nb*32 + col]
+    lds_barrier();
+
+    // Key-gradient block u of this wave: kind (0: dK from dS^T and Q, 1: dV
+    // from P^T and dO) and 32-dimension block nb.  With NW even the kind is
+    // the wave's parity.  xt[u][q][ks]: B fragment of X^T over query tile q
+    // (the workgroup's q-th), k-step ks: lane holds X[ks*16 + half*8 + e][nb*32 + col].
+    const int kind = wave & 1;
+    bf16x8_t xt[IPW][NW][2];
 #pragma unroll
-        for (int nb = 0; nb < NDT; ++nb)
+    for (int u = 0; u < IPW; ++u) {
+        const int nb = (wave + NW * u) >> 1;
+#pragma unroll
+        for (int q = 0; q < NW; ++q) {
+            const bf16_t* src = sQall + (q * 2 + kind) * 32 * Lay::KS + nb * 32 + col;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int m = ks * 16 + half * 8 + e, dd = nb * 32 + col;
-                    qt[nb][ks][e] = __builtin_bit_cast(__bf16, sQ[m * Lay::KS + dd]);
-                    gt[nb][ks][e] = __builtin_bit_cast(__bf16, sG[m * Lay::KS + dd]);
-                }
+                for (int e = 0; e < 8; ++e)
+                    xt[u][q][ks][e] = q < nqa ? __builtin_bit_cast(
+                                                    __bf16, src[(ks * 16 + half * 8 + e) * Lay::KS])
+                                              : static_cast<__bf16>(0.f);
+        }
     }
-    for (int x = tid; x < 2 * 32 * Lay::AS; x += NW * 64) sdK[x] = 0.f;
 
     f32x16_t dqacc[NDT];
 #pragma unroll
@@ -175,21 +194,26 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     const int n_tiles = 1 + n_vis + n_rt;
     const bf16_t* kbase = k_res + static_cast<int64_t>(bh) * res_tokens * D;
     const bf16_t* vbase = v_res + static_cast<int64_t>(bh) * res_tokens * D;
-    float* dkbase = dk + static_cast<int64_t>(bh) * res_tokens * D;
-    float* dvbase = dv + static_cast<int64_t>(bh) * res_tokens * D;
+    float* gbase = (kind ? dv : dk) + static_cast<int64_t>(bh) * res_tokens * D;
+    const float gscale = kind ? 1.f : inv_sqrt_d;
     const int lim = c * gpc;  // routed groups must lie in the causal past
 
-    bf16_t* scr = reinterpret_cast<bf16_t*>(smem + Lay::kScr) + wave * 3 * 32 * SCR;
-    bf16_t* s_ds = scr;                 // dS   [query][key]
-    bf16_t* s_dst = scr + 32 * SCR;     // dS^T [key][query]
-    bf16_t* s_pt = scr + 2 * 32 * SCR;  // P^T  [key][query]
+    // scratch of wave w, buffer x: dS^T then P^T, each [key][query]
+    auto scratch = [&](int w, int x) { return scr_all + (w * 2 + x) * 2 * 32 * SCR; };
 
     for (int tile = 0; tile < n_tiles; ++tile) {
-        __syncthreads();  // the previous tile's reads and flushes are done
-        // stage K, V row-major and K transposed; the token of each tile row
-        // (-1: a routed row to skip, staged as zeros)
-        for (int x = tid; x < KT * VPR; x += NW * 64) {
-            const int row = x / VPR, cv = x % VPR;
+        // Stage K, V row-major and K transposed; the token of each tile row
+        // (-1: a routed row to skip, staged as zeros) goes to the token table
+        // of the tile's parity.  Every wave has passed the previous tile's
+        // last barrier, after which only the token table of that tile's
+        // parity and the scratch are read.  Thread (row, part) issues all its
+        // vectors of the row at once; consecutive threads take consecutive
+        // rows, so the transposed writes are consecutive too.
+        int* s_tok = s_tok_all + (tile & 1) * KT;
+        {
+            constexpr int TPR = NW * 64 / KT;  // threads per row
+            constexpr int VPT = VPR / TPR;     // vectors per thread
+            const int row = tid % KT, pv = tid / KT;
             int tok;
             if (tile <= n_vis) {
                 tok = (tile == 0 ? c : vis.chunk(tile - 1)) * KT + row;
@@ -198,19 +222,29 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
                 const int g = rr < routed_rows ? s_gid[rr >> group_shift] : -1;
                 tok = g >= 0 && g < lim ? g * group + (rr & (group - 1)) : -1;
             }
-            if (cv == 0) s_tok[row] = tok;
-            vec16 kx{{0u, 0u, 0u, 0u}}, vx{{0u, 0u, 0u, 0u}};
-            if (tok >= 0) {
-                kx = load16(kbase + static_cast<int64_t>(tok) * D + cv * 8);
-                vx = load16(vbase + static_cast<int64_t>(tok) * D + cv * 8);
-            }
-            *reinterpret_cast<vec16*>(sK + row * Lay::KS + cv * 8) = kx;
-            *reinterpret_cast<vec16*>(sV + row * Lay::KS + cv * 8) = vx;
-            const bf16_t* ke = reinterpret_cast<const bf16_t*>(&kx);
+            if (pv == 0) s_tok[row] = tok;
+            vec16 kx[VPT], vx[VPT];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) sKT[(cv * 8 + e) * Lay::TS + row] = ke[e];
+            for (int u = 0; u < VPT; ++u) {
+                const int cv = pv * VPT + u;
+                kx[u] = vec16{{0u, 0u, 0u, 0u}};
+                vx[u] = kx[u];
+                if (tok >= 0) {
+                    kx[u] = load16(kbase + static_cast<int64_t>(tok) * D + cv * 8);
+                    vx[u] = load16(vbase + static_cast<int64_t>(tok) * D + cv * 8);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < VPT; ++u) {
+                const int cv = pv * VPT + u;
+                *reinterpret_cast<vec16*>(sK + row * Lay::KS + cv * 8) = kx[u];
+                *reinterpret_cast<vec16*>(sV + row * Lay::KS + cv * 8) = vx[u];
+                const bf16_t* ke = reinterpret_cast<const bf16_t*>(&kx[u]);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) sKT[(cv * 8 + e) * Lay::TS + row] = ke[e];
+            }
         }
-        __syncthreads();
+        lds_barrier();
         const bool current = tile == 0;
         for (int st = 0; st < 2; ++st) {
             if (qactive) {
@@ -230,7 +264,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
                     pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         frag(sV + krow * Lay::KS + off), frag(sG + col * Lay::KS + off), pacc, 0, 0, 0);
                 }
-                // P^T, dS^T: lane (half, col) holds keys st*32 + kl, kl below
+                // P^T, dS^T: lane (half, col) holds keys st*32 + kl, kl below;
+                // element e of fragment kap is e' = kap*8 + e of the accumulator
+                bf16_t* s_dst = scratch(wave, st);
+                bf16_t* s_pt = s_dst + 32 * SCR;
+                bf16x8_t dsf[2];
 #pragma unroll
                 for (int e = 0; e < 16; ++e) {
                     const int kl = (e >> 2) * 8 + half * 4 + (e & 3);
@@ -238,64 +276,52 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
                     const bool ok = s_tok[key] >= 0 && (!current || key <= t);
                     const float p = ok ? __builtin_amdgcn_exp2f(sacc[e] * scale2 - lse2) : 0.f;
                     const float ds = p * (pacc[e] - dsum);
-                    const bf16_t pb = __builtin_bit_cast(bf16_t, static_cast<__bf16>(p));
-                    const bf16_t db = __builtin_bit_cast(bf16_t, static_cast<__bf16>(ds));
-                    s_ds[col * SCR + kl] = db;
-                    s_dst[kl * SCR + col] = db;
-                    s_pt[kl * SCR + col] = pb;
+                    const __bf16 db = static_cast<__bf16>(ds);
+                    dsf[e >> 3][e & 7] = db;
+                    s_dst[kl * SCR + col] = __builtin_bit_cast(bf16_t, db);
+                    s_pt[kl * SCR + col] = __builtin_bit_cast(bf16_t, static_cast<__bf16>(p));
                 }
-                wave_lds_sync();
-                // dQ += dS.K: A = dS [query][key], B^T = K^T [d][key]
+                // dQ += dS.K: k-slot half*8 + e of fragment kap is key
+                // st*32 + kap*16 + (e/4)*8 + half*4 + e%4, so the B operand
+                // is two 4-key runs of the K^T row of dimension nb*32 + col.
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const bf16x8_t af = frag(s_ds + col * SCR + ks * 16 + half * 8);
+                for (int kap = 0; kap < 2; ++kap)
 #pragma unroll
-                    for (int nb = 0; nb < NDT; ++nb)
-                        dqacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            af, frag(sKT + (nb * 32 + col) * Lay::TS + st * 32 + ks * 16 + half * 8),
-                            dqacc[nb], 0, 0, 0);
-                }
-                // dK, dV of the sub-tile's keys: A = dS^T / P^T [key][query],
-                // B^T = Q^T / dO^T [d][query]; added into the LDS accumulators
-#pragma unroll
-                for (int nb = 0; nb < NDT; ++nb) {
-                    f32x16_t kacc, vacc;
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        kacc[e] = 0.f;
-                        vacc[e] = 0.f;
+                    for (int nb = 0; nb < NDT; ++nb) {
+                        const bf16_t* kp = sKT + (nb * 32 + col) * Lay::TS + st * 32 + kap * 16 + half * 4;
+                        const bf16x4_t lo = frag4(kp), hi = frag4(kp + 8);
+                        const bf16x8_t bf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                        dqacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dsf[kap], bf, dqacc[nb], 0, 0, 0);
                     }
-#pragma unroll
-                    for (int ks = 0; ks < 2; ++ks) {
-                        kacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            frag(s_dst + col * SCR + ks * 16 + half * 8), qt[nb][ks], kacc, 0, 0, 0);
-                        vacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            frag(s_pt + col * SCR + ks * 16 + half * 8), gt[nb][ks], vacc, 0, 0, 0);
-                    }
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int a = ((e >> 2) * 8 + half * 4 + (e & 3)) * Lay::AS + nb * 32 + col;
-                        atomicAdd(sdK + a, kacc[e]);
-                        atomicAdd(sdV + a, vacc[e]);
-                    }
-                    __builtin_amdgcn_sched_barrier(0);  // one block's accumulators live at a time
-                }
-                wave_lds_sync();  // scratch reads done before the next sub-tile writes it
             }
-            __syncthreads();
-            // add the sub-tile's dK, dV into the resident rows; clear
-            for (int x = tid; x < 32 * D; x += NW * 64) {
-                const int row = x / D, dd = x % D;
-                const int tok = s_tok[st * 32 + row];
-                const int a = row * Lay::AS + dd;
-                if (tok >= 0) {
-                    unsafeAtomicAdd(dkbase + static_cast<int64_t>(tok) * D + dd, sdK[a] * inv_sqrt_d);
-                    unsafeAtomicAdd(dvbase + static_cast<int64_t>(tok) * D + dd, sdV[a]);
+            lds_barrier();  // every wave's dS^T, P^T of sub-tile st are in LDS
+            // This wave's key-gradient blocks over the workgroup's queries:
+            // A = dS^T or P^T [key][query] of query tile q, B = xt.
+#pragma unroll
+            for (int u = 0; u < IPW; ++u) {
+                const int nb = (wave + NW * u) >> 1;
+                f32x16_t acc;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll
+                for (int q = 0; q < NW; ++q) {
+                    if (q < nqa) {
+                        const bf16_t* a = scratch(q, st) + kind * 32 * SCR + col * SCR + half * 8;
+#pragma unroll
+                        for (int ks = 0; ks < 2; ++ks)
+                            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag(a + ks * 16), xt[u][q][ks],
+                                                                          acc, 0, 0, 0);
+                    }
                 }
-                sdK[a] = 0.f;
-                sdV[a] = 0.f;
+                // acc[e]: key st*32 + (e/4)*8 + half*4 + e%4, dimension nb*32 + col
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    const int tok = s_tok[st * 32 + (e >> 2) * 8 + half * 4 + (e & 3)];
+                    if (tok >= 0)
+                        unsafeAtomicAdd(gbase + static_cast<int64_t>(tok) * D + nb * 32 + col,
+                                        acc[e] * gscale);
+                }
             }
-            __syncthreads();
         }
     }
 
