@@ -367,7 +367,10 @@ int64_t hga_attend_split_workspace(const hga_plan* plan, int32_t n_q_chunks);
  *               ((q_chunk0 + n_q_chunks) * chunk <= res_tokens)
  *   group_idx   as for hga_attend
  *   lse         fp32 [batch, n_q_heads, n_q_chunks*chunk] (required)
- *   dq          fp32 like q_rot, written
+ *   dq          fp32 like q_rot, written (with GQA groups beyond one
+ *               workgroup's query rows the call first keeps D_i in dq's
+ *               leading floats, then overwrites all of dq); must not
+ *               overlap any other argument
  *   dk, dv      fp32 [batch, n_kv_heads, res_tokens, head_dim], ADDED INTO
  *               (zero them for a plain gradient; the sums over query units
  *               are fp32 atomic adds, so their order, and the last bits, may

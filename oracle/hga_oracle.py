@@ -109,24 +109,28 @@ def summaries(k_rot: np.ndarray, span: int, base: float, n_hf: int) -> np.ndarra
 
 
 def summaries_literal(k_rot: np.ndarray, span: int, base: float, n_hf: int,
-                      first_position: int = 0) -> np.ndarray:
+                      first_position: int = 0, wrap: int = 0) -> np.ndarray:
     """The paper's two-part rule taken literally (Sec. 3.2).
 
-    Keys are un-rotated to raw space with their absolute positions
-    (first_position + t).  High-frequency pairs: rotate per token (that is,
-    keep k_rot) and average.  Low-frequency pairs: average the raw keys, then
-    rotate the average at the span's middle position start + (span - 1)/2.
+    Keys are un-rotated to raw space with their RoPE positions
+    (first_position + t, taken modulo ``wrap`` when it is set: the variant of
+    Sec. 5 on long-context positional encoding).  High-frequency pairs:
+    rotate per token (that is, keep k_rot) and average.  Low-frequency pairs:
+    average the raw keys, then rotate the average at the span's middle
+    position, the mean of its tokens' positions.
     """
     B, H, N, d = k_rot.shape
     half = d // 2
     n = N // span
     theta = rope_inv_freq(d, base)
     pos = first_position + np.arange(n * span, dtype=np.float64)
+    if wrap:
+        pos = np.mod(pos, wrap)
     k = np.asarray(k_rot[:, :, :n * span, :], dtype=np.float64)
     raw = rotate_pairs(k, -pos[:, None] * theta[None, :])
     rot_mean = k.reshape(B, H, n, span, d).mean(axis=3)
     raw_mean = raw.reshape(B, H, n, span, d).mean(axis=3)
-    middle = first_position + np.arange(n, dtype=np.float64) * span + (span - 1) / 2.0
+    middle = pos.reshape(n, span).mean(axis=1)
     low = rotate_pairs(raw_mean, middle[:, None] * theta[None, :])
     out = low.copy()
     out[..., :n_hf] = rot_mean[..., :n_hf]

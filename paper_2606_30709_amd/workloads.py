@@ -65,6 +65,8 @@ class Workload:
     needle_depths: tuple = ()  # chunk ids for needle_mode == "depths"
     decode_block: bool = False  # True: queries are only the last chunk(s)
     decode_blocks: int = 1      # with decode_block: the last this many chunks are query blocks
+    rope_wrap: int = 0          # > 0: RoPE positions taken modulo this (Sec. 5, positional
+                                # encoding: p mod 65536); a multiple of chunk
     seed: int = 0
 
     @property
@@ -201,6 +203,17 @@ def _unit(rng: np.random.Generator, shape) -> np.ndarray:
     return u / np.linalg.norm(u, axis=-1, keepdims=True)
 
 
+def _positions(w: Workload, pos: np.ndarray) -> np.ndarray:
+    """RoPE positions of tokens at absolute positions ``pos``: wrapped modulo
+    ``w.rope_wrap`` when set.  The wrap is a multiple of the chunk, so every
+    chunk and group still holds consecutive positions."""
+    if w.rope_wrap <= 0:
+        return pos
+    if w.rope_wrap % w.chunk:
+        raise ValueError("rope_wrap must be a multiple of the chunk")
+    return pos % w.rope_wrap
+
+
 def generate(w: Workload, seed: int | None = None, position_offset: int = 0,
              unrounded: bool = False) -> dict:
     """Draw the inputs of workload ``w``.
@@ -225,9 +238,9 @@ def generate(w: Workload, seed: int | None = None, position_offset: int = 0,
     k_raw = rng.standard_normal((B, Hkv, N, d)) * w.prescale
     v = rng.standard_normal((B, Hkv, N, d))
 
-    q = _rotary(q_raw, np.arange(q0_tok, N) + position_offset, w.rope_base)
+    q = _rotary(q_raw, _positions(w, np.arange(q0_tok, N) + position_offset), w.rope_base)
     del q_raw
-    k = _rotary(k_raw, np.arange(N) + position_offset, w.rope_base)
+    k = _rotary(k_raw, _positions(w, np.arange(N) + position_offset), w.rope_base)
     del k_raw
 
     needles = []

@@ -827,6 +827,14 @@ def test_decode_block_parity_128k(hga):
     _decode_check(hga, W.preset("decode128k"))
 
 
+def test_decode_block_parity_128k_wrapped_positions(hga):
+    """The same 128K context with RoPE positions taken modulo 65536 (Sec. 5,
+    long-context positional encoding): the keys past 64K repeat the first
+    positions' rotations; routing and attention are unchanged code and still
+    match the oracle on these inputs."""
+    _decode_check(hga, W_("decode128k", rope_wrap=65536))
+
+
 def test_decode_block_parity_full(hga):
     pipe = _decode_check(hga, W.preset("decode64k"))
     # host-sourced gather equals a device-sourced gather of the same history

@@ -222,6 +222,54 @@ def test_summary_phase_form_equals_literal_rule(d, base, pos0):
 
 
 @pytest.mark.parametrize("d,base", [(64, 1e4), (128, 1e6)])
+def test_summary_phase_form_with_wrapped_positions(d, base):
+    """Sec. 5 (long-context positional encoding): RoPE positions taken modulo
+    65536.  The phase form never sees absolute positions, only offsets within
+    a span, so it is exact as long as every span holds consecutive positions:
+    with the wrap at 65536, a multiple of every span, it equals the literal
+    rule evaluated on the wrapped positions across the wrap; with a wrap that
+    splits a span (65536 - 8) the low-frequency pairs of that span differ."""
+    rng = np.random.default_rng(12)
+    N, start = 512, 65536 - 256
+    half = d // 2
+    theta = base ** (-2.0 * np.arange(half) / d)
+    raw = rng.standard_normal((2, 3, N, d))
+
+    def rotated(wrap):
+        pos = np.mod(start + np.arange(N), wrap)
+        z = (raw[..., :half] + 1j * raw[..., half:]) * np.exp(1j * pos[:, None] * theta)
+        return np.concatenate([z.real, z.imag], -1)
+
+    for span in (64, 16):
+        nhf = O.high_freq_pairs(span, d, base)
+        k_rot = rotated(65536)
+        a = O.summaries(k_rot, span, base, nhf)
+        b = O.summaries_literal(k_rot, span, base, nhf, first_position=start, wrap=65536)
+        assert np.max(np.abs(a - b)) < 1e-9
+        k_bad = rotated(65536 - 8)
+        a = O.summaries(k_bad, span, base, nhf)
+        b = O.summaries_literal(k_bad, span, base, nhf, first_position=start, wrap=65536 - 8)
+        split = (256 - 8) // span  # the span that holds the wrap
+        assert np.max(np.abs(a[:, :, split, nhf:half] - b[:, :, split, nhf:half])) > 1e-3
+        others = [x for x in range(N // span) if x != split]
+        assert np.max(np.abs(a[:, :, others] - b[:, :, others])) < 1e-9
+
+
+def test_workload_rope_wrap_positions():
+    """The generator's wrapped positions: a sequence starting at 65536 with
+    the wrap draws exactly the keys and queries of the same sequence at
+    position 0 without it; a wrap that is not a multiple of the chunk is
+    refused."""
+    import dataclasses
+    w = dataclasses.replace(W.preset("tiny"), dtype="f32")
+    a = W.generate(w)
+    b = W.generate(dataclasses.replace(w, rope_wrap=65536), position_offset=65536)
+    assert np.array_equal(a["q"], b["q"]) and np.array_equal(a["k"], b["k"])
+    with pytest.raises(ValueError):
+        W.generate(dataclasses.replace(w, rope_wrap=65536 + 16))
+
+
+@pytest.mark.parametrize("d,base", [(64, 1e4), (128, 1e6)])
 @pytest.mark.parametrize("span,start", [(64, 0), (64, 640), (16, 48), (16, 4096)])
 def test_summary_of_constant_raw_key_closed_form(d, base, span, start):
     """A span whose raw key is the same vector w at every token.  Closed form:
