@@ -61,6 +61,12 @@ SMALL = {
                    topk_groups=9),
     "gqa3_d64": W_("smalllm", batch=1, seq_len=2048, n_q_heads=6, n_kv_heads=2, topk_chunks=4,
                    topk_groups=7, keep_first=2, keep_last=1),
+    # two query heads per KV head: the backward's fused form with four
+    # wavefronts (d64) and its split form with a four-wavefront dQ (d128)
+    "gqa2_d64": W_("smalllm", batch=1, seq_len=2048, n_q_heads=4, n_kv_heads=2, topk_chunks=4,
+                   topk_groups=6),
+    "gqa2_d128": W_("qwen32k", seq_len=2048, n_q_heads=4, n_kv_heads=2, topk_chunks=5,
+                    topk_groups=9, keep_last=1),
     "tiny_noforce": W_("tiny", force_prev=0),
     "f32_d128_gqa": W_("tiny", seq_len=1024, n_q_heads=4, n_kv_heads=2, head_dim=128,
                        rope_base=1e6, topk_chunks=3, topk_groups=5, keep_last=2),
@@ -329,7 +335,8 @@ SPLIT_CASES = {k: SMALL[k] for k in ("qwen_4k_ragged", "qwen_g8", "qwen_g32", "g
                                      "mha_d128", "f32_d128_gqa")}
 
 
-BWD_CASES = {k: SMALL[k] for k in ("smalllm_2k", "gqa3_d64", "qwen_4k_ragged", "qwen_g8",
+BWD_CASES = {k: SMALL[k] for k in ("smalllm_2k", "gqa2_d64", "gqa2_d128", "gqa3_d64",
+                                   "qwen_4k_ragged", "qwen_g8",
                                    "qwen_g32", "mha_d128", "qwen_chunks_4k")}
 
 
