@@ -267,7 +267,7 @@ def decode_bench(w, inp, args):
     import torch
 
     from paper_2606_30709_amd.pipeline import DecodePipeline
-    pipe = DecodePipeline(w, inp)
+    pipe = DecodePipeline(w, inp, qbar_first=not args.route_from_q)
     for _ in range(args.warmup):
         pipe.step()
     torch.cuda.synchronize()
@@ -308,7 +308,8 @@ def decode_sequence_bench(w, inp, args):
     slots = args.cache_slots or 8 * w.topk_groups
 
     def run(cache_slots):
-        pipe = DecodeSequencePipeline(w, inp, cache_slots=cache_slots)
+        pipe = DecodeSequencePipeline(w, inp, cache_slots=cache_slots,
+                                      qbar_first=not args.route_from_q)
         for _ in range(args.warmup):
             pipe.reset_cache()
             pipe.step()
@@ -460,6 +461,10 @@ def main():
                     help="fused: hga_gather_attend (the attention stages the routed rows and "
                          "writes the routed buffers); separate: hga_gather_kv + hga_attend "
                          "(identical results)")
+    ap.add_argument("--route-from-q", action="store_true",
+                    help="decode: hga_route forms q_bar from the query rows and the block's "
+                         "summaries follow it (default: hga_build_summaries_qbar first, then "
+                         "hga_route_qbar)")
     ap.add_argument("--no-cache", action="store_true",
                     help="decode sequence: gather every block's routed groups from host memory")
     ap.add_argument("--cache-slots", type=int, default=0,

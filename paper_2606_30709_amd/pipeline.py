@@ -179,10 +179,17 @@ class DecodePipeline:
     """One query block (the last chunk of the workload) after a host-resident history."""
 
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 fused_route: bool = True, split_attend: bool = True, fused_gather: bool = False):
+                 fused_route: bool = True, split_attend: bool = True, fused_gather: bool = False,
+                 qbar_first: bool = True):
         assert w.decode_block and w.decode_blocks == 1
         self.w = w
         self.fused_route = fused_route
+        # qbar_first: the block's summaries and its q_bar in one launch
+        # (hga_build_summaries_qbar) before routing from q_bar
+        # (hga_route_qbar), so the routing launch does not wait on the query
+        # rows; the block's own chunk is never among its routing candidates.
+        # Otherwise hga_route forms q_bar and the summaries follow the block.
+        self.qbar_first = qbar_first and fused_route
         # fused_gather: the host gather inside the split attention
         # (hga_gather_attend_split), else hga_gather_kv then the attention.
         # The separate gather is the faster one here: each unit's two query
@@ -281,14 +288,26 @@ class DecodePipeline:
                                     self.v_routed, self.out, self.attend_ws, self.lse,
                                     res_slot=self.res_slot, src_on_host=True, stream=stream)
 
+    def append_qbar(self, stream=None):
+        """The block's chunk summaries (as ``append``) and its q_bar, one launch."""
+        hga.hga_build_summaries_qbar(self.plan, self.k_res, self.c - self.cur_slot, self.c,
+                                     self.c + 1, self.chunk_sum, self.group_sum, self.q, self.c,
+                                     self.qbar, stream=stream)
+
     def step(self, stream=None):
-        self.route(stream)
+        if self.qbar_first:
+            self.append_qbar(stream)
+            hga.hga_route_qbar(self.plan, self.qbar, self.c, self.chunk_sum, self.group_sum,
+                               self.chunk_idx, self.group_idx, stream=stream)
+        else:
+            self.route(stream)
         if self.fused_gather:
             self.gather_attend(stream)
         else:
             self.gather(stream)
             self.attend(stream)
-        self.append(stream)
+        if not self.qbar_first:
+            self.append(stream)
 
 
 class DecodeSequencePipeline:
@@ -307,9 +326,10 @@ class DecodeSequencePipeline:
     come from host memory (``hga_gather_kv``)."""
 
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 cache_slots: int | None = None):
+                 cache_slots: int | None = None, qbar_first: bool = True):
         assert w.decode_block
         self.w = w
+        self.qbar_first = qbar_first  # as DecodePipeline's
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hq, Hkv, d, C, G = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.chunk, w.group
         f32, i32 = torch.float32, torch.int32
@@ -360,8 +380,16 @@ class DecodeSequencePipeline:
         c = self.c0 + b
         q = self.q_blocks[b]
         gi = self.group_idx[b]
-        hga.hga_route(self.plan, q, c, self.chunk_sum, self.group_sum, self.qbar,
-                      self.chunk_idx, gi, stream=stream)
+        k_chunk0 = c - int(self.slot_of[c])  # chunk c sits at resident slot slot_of[c]
+        if self.qbar_first:
+            hga.hga_build_summaries_qbar(self.plan, self.k_res, k_chunk0, c, c + 1,
+                                         self.chunk_sum, self.group_sum, q, c, self.qbar,
+                                         stream=stream)
+            hga.hga_route_qbar(self.plan, self.qbar, c, self.chunk_sum, self.group_sum,
+                               self.chunk_idx, gi, stream=stream)
+        else:
+            hga.hga_route(self.plan, q, c, self.chunk_sum, self.group_sum, self.qbar,
+                          self.chunk_idx, gi, stream=stream)
         if self.cache is not None:
             hga.hga_gather_kv_cached(self.plan, gi, c, self.k_hist, self.v_hist, self.cache,
                                      self.k_routed, self.v_routed, self.n_fetched[b],
@@ -372,9 +400,10 @@ class DecodeSequencePipeline:
         hga.hga_attend_split(self.plan, q, c, self.k_res, self.v_res, self.k_routed,
                              self.v_routed, gi, self.out[b], self.attend_ws, self.lse[b],
                              res_slot=self.res_slot, stream=stream)
-        # chunk c closes: its summaries from the resident copy (slot slot_of[c])
-        hga.hga_build_summaries(self.plan, self.k_res, c, c + 1, self.chunk_sum, self.group_sum,
-                                k_chunk0=c - int(self.slot_of[c]), stream=stream)
+        if not self.qbar_first:
+            # chunk c closes: its summaries from the resident copy
+            hga.hga_build_summaries(self.plan, self.k_res, c, c + 1, self.chunk_sum,
+                                    self.group_sum, k_chunk0=k_chunk0, stream=stream)
 
     def reset_cache(self):
         """Empty the warm cache (a new sequence); its tick keeps counting."""
