@@ -481,7 +481,7 @@ def main():
                     help="run attention and a known-size copy for rocprofv3 --pmc, then exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for "
+        print(f"bench.py runs on one GPU: the library has no multi-GPU path (asked for "
               f"--gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
 
