@@ -372,6 +372,45 @@ def test_attend_backward_matches_oracle(hga, key):
         assert err <= BWD_TOL * scale and rel <= BWD_TOL / 4, name
 
 
+@pytest.mark.parametrize("key", ["smalllm_2k", "gqa3_d64", "qwen_4k_ragged"])
+def test_attend_backward_query_block_offset(hga, key):
+    """hga_attend_backward on the last two query chunks alone (q_chunk0 > 0,
+    as for a block's gradient): dq of those rows, and dk, dv holding only
+    their contributions, against the oracle on the same chunk ids; both
+    backward forms (fused for smalllm_2k, split for the GQA cases)."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SMALL[key]
+    _say(f"[backward-offset] {key}")
+    inp = W.generate(w)
+    pipe = PrefillPipeline(w, inp)
+    pipe.step()
+    C, q0 = w.chunk, w.n_chunks - 2
+    rows = slice(q0 * C, w.n_chunks * C)
+    q = pipe.q[:, :, rows].contiguous()
+    out = pipe.out[:, :, rows].contiguous()
+    lse = pipe.lse[:, :, rows].contiguous()
+    gi = pipe.group_idx[:, :, q0:].contiguous()
+    rng = np.random.default_rng(78)
+    dout = torch.from_numpy(rng.standard_normal(q.shape).astype(np.float32)).to(torch.bfloat16).cuda()
+    dq = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    dk = torch.zeros(pipe.k.shape, dtype=torch.float32, device="cuda")
+    dv = torch.zeros_like(dk)
+    hga.hga_attend_backward(pipe.plan, q, q0, pipe.k, pipe.v, gi, out, lse, dout, dq, dk, dv)
+    torch.cuda.synchronize()
+    q64, k64, v64 = (f64(inp[x], w.dtype) for x in "qkv")
+    rq, rk, rv = O.attend_backward(
+        q64[:, :, rows], k64, v64, dout.float().cpu().numpy().astype(np.float64),
+        gi.cpu().numpy(), [q0, q0 + 1], C, w.group, w.keep_first, w.keep_last, w.force_prev)
+    for name, g, ref in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
+        g = g.cpu().numpy().astype(np.float64)
+        assert np.isfinite(g).all(), name
+        err = np.max(np.abs(g - ref))
+        scale = np.max(np.abs(ref))
+        rel = np.linalg.norm(g - ref) / np.linalg.norm(ref)
+        _say(f"  {name}: max-abs {err:.3g} of max {scale:.3g}, normwise {rel:.3g}")
+        assert err <= BWD_TOL * scale and rel <= BWD_TOL / 4, name
+
+
 @pytest.mark.parametrize("key", list(SPLIT_CASES))
 def test_attend_split_matches_oracle(hga, key):
     """hga_attend_split computes the same softmax as hga_attend with its
