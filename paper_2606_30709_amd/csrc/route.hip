@@ -334,8 +334,11 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
 template <int kThreads>
 struct WgSelect {
     static constexpr int kMaxPer = 4;
+    static constexpr int kTopW = 4;  // largest words each wave contributes to the bound
     uint32_t wave_t[kThreads / 64];
     int wave_cnt[kMaxPer][kThreads / 64];
+    uint32_t cand[kTopW * (kThreads / 64)];
+    uint32_t bound;
     uint64_t surv[kMaxPer * kThreads];
 };
 
@@ -360,20 +363,63 @@ __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int
         key[i] = i < per && x < n ? keys[x] : 0;
         hi[i] = static_cast<uint32_t>(key[i] >> 32);  // 0 for no key: never >= a candidate
     }
-    uint32_t t_w = 0;
-    for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t cand = t_w | (1u << bit);
-        int cnt = 0;
-#pragma unroll
-        for (int i = 0; i < kMaxPer; ++i)
-            if (i < per) cnt += __popcll(__ballot(hi[i] >= cand));
-        if (cnt >= k) t_w = cand;
-    }
-    if (lane == 0) S->wave_t[wave] = t_w;
-    __syncthreads();
+    // A lower bound on the k-th largest score word.  With k <= kTopW * NW:
+    // each wave hands over its kTopW largest words (one key removed per
+    // round), and the k-th largest of those kTopW * NW words, each of a
+    // different key, is found by wave 0.  Otherwise: the largest per-wave
+    // k-th largest word.  Either way at least k keys reach the bound, so the
+    // exact selection below sees every key of the result.
+    constexpr int kTopW = WgSelect<kThreads>::kTopW;
     uint32_t bound = 0;
+    if (k <= kTopW * NW) {
+        uint32_t used = 0;  // this thread's keys already handed over
 #pragma unroll
-    for (int w = 0; w < NW; ++w) bound = S->wave_t[w] > bound ? S->wave_t[w] : bound;
+        for (int rr = 0; rr < kTopW; ++rr) {
+            uint32_t my = 0;
+            int mi = -1;
+#pragma unroll
+            for (int i = 0; i < kMaxPer; ++i)
+                if (i < per && !((used >> i) & 1u) && (mi < 0 || hi[i] > my)) {
+                    my = hi[i];
+                    mi = i;
+                }
+            uint32_t m = my;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), off));
+                m = o > m ? o : m;
+            }
+            const uint64_t holders = __ballot(mi >= 0 && my == m);
+            if (lane == static_cast<int>(__builtin_ctzll(holders))) used |= 1u << mi;
+            if (lane == 0) S->cand[rr * NW + wave] = m;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            const uint32_t v = lane < kTopW * NW ? S->cand[lane] : 0u;
+            uint32_t t = 0;
+            for (int bit = 31; bit >= 0; --bit) {
+                const uint32_t c = t | (1u << bit);
+                if (__popcll(__ballot(lane < kTopW * NW && v >= c)) >= k) t = c;
+            }
+            if (lane == 0) S->bound = t;
+        }
+        __syncthreads();
+        bound = S->bound;
+    } else {
+        uint32_t t_w = 0;
+        for (int bit = 31; bit >= 0; --bit) {
+            const uint32_t cand = t_w | (1u << bit);
+            int cnt = 0;
+#pragma unroll
+            for (int i = 0; i < kMaxPer; ++i)
+                if (i < per) cnt += __popcll(__ballot(hi[i] >= cand));
+            if (cnt >= k) t_w = cand;
+        }
+        if (lane == 0) S->wave_t[wave] = t_w;
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < NW; ++w) bound = S->wave_t[w] > bound ? S->wave_t[w] : bound;
+    }
     // word 0 marks an absent key (a score's word is never 0: that pattern
     // is a NaN), so it never passes, whatever the bound
     uint64_t km[kMaxPer];
