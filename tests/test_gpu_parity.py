@@ -966,6 +966,40 @@ def test_argument_errors_launch_nothing(hga):
     torch.cuda.synchronize()
 
 
+def test_backward_argument_errors(hga):
+    """hga_attend_backward refuses, before any launch: an fp32 plan
+    (unsupported), a missing lse, and resident K/V that do not cover the
+    query chunks; the outputs stay untouched."""
+    lib = hga.library()
+    dev = "cuda"
+    plan32 = hga.Plan.for_workload(SMALL["tiny"])
+    q = torch.zeros(1, 1, 1024, 64, device=dev)
+    k = torch.zeros(1, 1, 1024, 64, device=dev)
+    gi = torch.zeros(1, 1, 16, 4, dtype=torch.int32, device=dev)
+    lse = torch.zeros(1, 1, 1024, device=dev)
+    st = lib.hga_attend_backward(plan32.handle, q.data_ptr(), 0, 16, k.data_ptr(), k.data_ptr(),
+                                 1024, gi.data_ptr(), q.data_ptr(), lse.data_ptr(), q.data_ptr(),
+                                 q.data_ptr(), q.data_ptr(), q.data_ptr(), None)
+    assert st == -2 and "bf16" in hga.hga_last_error()
+    w = SMALL["smalllm_2k"]
+    plan = hga.Plan.for_workload(w)
+    B, Hq, Hkv, d, N = w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.seq_len
+    qb = torch.zeros(B, Hq, N, d, dtype=torch.bfloat16, device=dev)
+    kb = torch.zeros(B, Hkv, N, d, dtype=torch.bfloat16, device=dev)
+    gib = torch.zeros(B, Hkv, w.n_chunks, w.topk_groups, dtype=torch.int32, device=dev)
+    lseb = torch.zeros(B, Hq, N, device=dev)
+    dq = torch.full((B, Hq, N, d), 7.0, device=dev)
+    dk = torch.full((B, Hkv, N, d), 7.0, device=dev)
+    args = lambda lse_ptr, res: (plan.handle, qb.data_ptr(), 0, w.n_chunks, kb.data_ptr(),
+                                 kb.data_ptr(), res, gib.data_ptr(), qb.data_ptr(), lse_ptr,
+                                 qb.data_ptr(), dq.data_ptr(), dk.data_ptr(), dk.data_ptr(), None)
+    assert lib.hga_attend_backward(*args(None, N)) == -1
+    assert "lse" in hga.hga_last_error()
+    assert lib.hga_attend_backward(*args(lseb.data_ptr(), N - 64)) == -1
+    torch.cuda.synchronize()
+    assert bool((dq == 7.0).all()) and bool((dk == 7.0).all())
+
+
 def test_gather_and_attend_handle_invalid_slots(hga):
     """-1 and out-of-range group ids give zero rows in the gather and are
     skipped by attention; an invalid resident slot poisons its rows."""
