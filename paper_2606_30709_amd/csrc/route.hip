@@ -339,6 +339,8 @@ struct WgSelect {
     int wave_cnt[kMaxPer][kThreads / 64];
     uint32_t cand[kTopW * (kThreads / 64)];
     uint32_t bound;
+    int offset[kMaxPer * (kThreads / 64)];  // survivors before (pass, wave), position order
+    int n_keep;
     uint64_t surv[kMaxPer * kThreads];
 };
 
@@ -429,26 +431,29 @@ __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int
         if (lane == 0 && i < per) S->wave_cnt[i][wave] = __popcll(km[i]);
     }
     __syncthreads();
-    // position order: pass i, then wave, then lane
-    int base = 0, n_keep = 0;
-    for (int i = 0; i < per; ++i)
-        for (int w = 0; w < NW; ++w) {
-            const int cw = S->wave_cnt[i][w];
-            n_keep += cw;
+    // position order: pass i, then wave, then lane.  Wave 0 scans the
+    // per * NW counts (one per lane) into exclusive offsets.
+    static_assert(kMaxPer * NW <= 64, "one lane per (pass, wave)");
+    if (wave == 0) {
+        const int c0 = lane < per * NW ? S->wave_cnt[lane / NW][lane % NW] : 0;
+        int v = c0;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(v, off);
+            if (lane >= off) v += o;
         }
+        if (lane < per * NW) S->offset[lane] = v - c0;
+        if (lane == 63) S->n_keep = v;
+    }
+    __syncthreads();
 #pragma unroll
     for (int i = 0; i < kMaxPer; ++i) {
         if (i >= per) break;
-        int pos = base + __popcll(km[i] & ((uint64_t(1) << lane) - 1));
-        for (int w = 0; w < NW; ++w) {
-            const int cw = S->wave_cnt[i][w];
-            if (w < wave) pos += cw;
-            base += cw;
-        }
-        if (hi[i] != 0 && hi[i] >= bound) S->surv[pos] = key[i];
+        if (hi[i] != 0 && hi[i] >= bound)
+            S->surv[S->offset[i * NW + wave] + __popcll(km[i] & ((uint64_t(1) << lane) - 1))] = key[i];
     }
     __syncthreads();
-    if (wave == 0) wave_select_topk(S->surv, n_keep, k, sel, scr, true);
+    if (wave == 0) wave_select_topk(S->surv, S->n_keep, k, sel, scr, true);
     __syncthreads();
 }
 
