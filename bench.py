@@ -10,9 +10,11 @@ hga_gather_attend (the attention stages each routed group's rows from the
 resident K/V and writes them to the routed buffers, the gather's output).
 --route fused / separate use hga_route or the two routing calls instead,
 --gather separate uses hga_gather_kv + hga_attend (identical results).  The
-default workload is the SmallLM-shaped prefill (B4, 8/8 heads, d64, 8192
-tokens, bf16, C64 G16, first chunk hot, K_c 3, K_g 4 -> 3.125% of the
-context fetched by the last chunk).
+default workload is the largest single-GPU prefill, the Qwen3-30B-A3B
+attention-layer shape (B1, 32 query heads over 4 KV heads, d128, 32768
+tokens, bf16, RoPE base 1e6, C64 G16, first chunk and the 2 most recent
+chunks hot, K_c 30, K_g 48 -> 3.125% of the context fetched by the last
+chunk); --workload selects another preset.
 
 Prints one JSON line.  The step rate comes from the wall clock between two
 synchronizations around the timed steps.  In about ten of the timed steps,
@@ -172,39 +174,69 @@ def probe_traffic(w, inp, gather_mode: str):
                       "kernel_source_sha256": attend_source_hash()}), flush=True)
 
 
-def cpu_baseline(w, inp, max_seconds: float) -> dict:
-    """The float64 oracle, as it stands, over the (batch, KV head) units of the
-    same workload in order (wrapping around) until max_seconds of CPU work."""
+def cpu_model() -> str:
+    """The host CPU's model name (Linux /proc/cpuinfo), else the machine type."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def _spread_order(n: int) -> list:
+    """0 .. n-1 in bit-reversed order of the next power of two (any prefix is
+    spread over the whole range)."""
+    bits = max(1, (n - 1).bit_length())
+    rev = [int(format(i, f"0{bits}b")[::-1], 2) for i in range(1 << bits)]
+    return [i for i in rev if i < n]
+
+
+def cpu_baseline(w, inp, max_seconds: float, block_chunks: int = 64) -> dict:
+    """The float64 oracle, as it stands, over a bounded sample of the same
+    workload: pieces of `block_chunks` query chunks of one (batch, KV head),
+    all five stages for those query chunks (summaries of every chunk up to
+    the piece's end, routing, gather, attention), taken with the blocks in a
+    spread-out order and the units in turn, until max_seconds of CPU work.
+    A piece is worth block_chunks * chunk / n_kv_heads tokens of the layer."""
     from threadpoolctl import threadpool_info
 
     from oracle import hga_oracle as O
     from paper_2606_30709_amd import workloads as W
 
-    r = w.gqa_ratio
+    r, C = w.gqa_ratio, w.chunk
     units = [(b, j) for b in range(w.batch) for j in range(w.n_kv_heads)]
-    done = 0
+    n_blocks = (w.n_chunks + block_chunks - 1) // block_chunks
+    pieces = [(u, blk) for blk in _spread_order(n_blocks) for u in units]
+    done = chunks = 0
     t0 = time.perf_counter()
     while True:
-        b, j = units[done % len(units)]
-        q = W.storage_to_f64(inp["q"][b:b + 1, j * r:(j + 1) * r], w.dtype)
-        k = W.storage_to_f64(inp["k"][b:b + 1, j:j + 1], w.dtype)
-        v = W.storage_to_f64(inp["v"][b:b + 1, j:j + 1], w.dtype)
-        O.hga_forward(q, k, v, chunk=w.chunk, group=w.group, keep_first=w.keep_first,
+        (b, j), blk = pieces[done % len(pieces)]
+        c0 = blk * block_chunks
+        c1 = min(w.n_chunks, c0 + block_chunks)
+        q = W.storage_to_f64(inp["q"][b:b + 1, j * r:(j + 1) * r, c0 * C:c1 * C], w.dtype)
+        k = W.storage_to_f64(inp["k"][b:b + 1, j:j + 1, :c1 * C], w.dtype)
+        v = W.storage_to_f64(inp["v"][b:b + 1, j:j + 1, :c1 * C], w.dtype)
+        O.hga_forward(q, k, v, chunk=C, group=w.group, keep_first=w.keep_first,
                       keep_last=w.keep_last, force_prev=w.force_prev, topk_chunks=w.topk_chunks,
-                      topk_groups=w.topk_groups, rope_base=w.rope_base, with_gather=True)
+                      topk_groups=w.topk_groups, rope_base=w.rope_base, q_chunk0=c0,
+                      with_gather=True)
         done += 1
+        chunks += c1 - c0
         if time.perf_counter() - t0 > max_seconds:
             break
     dt = time.perf_counter() - t0
-    frac = done / len(units)           # may exceed 1: the layer is swept repeatedly
-    tokens = frac * w.batch * w.seq_len
+    tokens = chunks * C / w.n_kv_heads
     threads = 1
     for pool in threadpool_info():
         threads = max(threads, int(pool.get("num_threads", 1)))
     return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} (batch, KV head) units of {len(units)} in the layer, all "
-                      f"{w.n_chunks} chunks each, five stages, float64 NumPy, {dt:.1f} s",
-            "cpu": platform.processor() or platform.machine(), "host_cpus": os.cpu_count()}
+            "sample": f"{done} pieces of {block_chunks} query chunks of one (batch, KV head) "
+                      f"({chunks} of the layer's {w.n_chunks * len(units)} unit-chunks, blocks "
+                      f"spread over the sequence), five stages, float64 NumPy, {dt:.1f} s",
+            "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
 def measured_copy_bandwidth(nbytes: int = 1 << 30, reps: int = 10) -> float:
@@ -445,8 +477,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="smalllm",
-                    help="workload preset (default smalllm, the SmallLM-shaped prefill)")
+    ap.add_argument("--workload", default="qwen32k",
+                    help="workload preset (default qwen32k, the largest single-GPU prefill: "
+                         "the Qwen3-30B-A3B attention-layer shape)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")

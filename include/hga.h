@@ -299,9 +299,12 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
  *               it uses)
  *   slot_group  device int32 [batch, n_kv_heads, n_slots]: group held, -1 empty
  *   slot_used   device int32 [batch, n_kv_heads, n_slots]: tick of last use
- *   group_slot  device int32 [batch, n_kv_heads, src_tokens / group]: slot
- *               holding the group or -1
- *               (a new cache: every entry of the three maps -1)
+ *   group_slot  device int32 [batch, n_kv_heads, map_groups]: slot holding
+ *               the group or -1 (a new cache: every entry of the three maps -1)
+ *   map_groups  groups per (batch, KV head) partition of group_slot, fixed for
+ *               the lifetime of the maps (the partition stride), at least
+ *               src_tokens / group: a history that grows between calls keeps
+ *               its maps as long as it stays within this capacity
  *   entry_slot  device int32 [batch, n_kv_heads, topk_groups]: the call's
  *               copy plan (written, then read by its second kernel; no
  *               contents are needed before or kept after a call)
@@ -310,14 +313,14 @@ hga_status hga_attend_timed(const hga_plan* plan, const void* q_rot, int32_t q_c
  *   n_fetched   device int32 [batch, n_kv_heads] or NULL: groups read from
  *               k_src/v_src by this call (the misses)
  * The caller owns every buffer; calls on the same maps must be ordered (the
- * same stream).  HGA_EINVAL for an n_slots outside the range or a source
- * shorter than the causal past. */
+ * same stream).  HGA_EINVAL for an n_slots outside the range, a source
+ * shorter than the causal past or longer than map_groups groups. */
 hga_status hga_gather_kv_cached(const hga_plan* plan, const int32_t* group_idx, int32_t c,
                                 const void* k_src, const void* v_src, int64_t src_tokens,
                                 int32_t src_on_host, void* cache_k, void* cache_v,
                                 int32_t n_slots, int32_t* slot_group, int32_t* slot_used,
-                                int32_t* group_slot, int32_t* entry_slot, int32_t tick,
-                                void* k_routed, void* v_routed, int32_t* n_fetched,
+                                int32_t* group_slot, int64_t map_groups, int32_t* entry_slot,
+                                int32_t tick, void* k_routed, void* v_routed, int32_t* n_fetched,
                                 void* stream);
 
 /* hga_attend for launches with few units (a decode block, one block of a

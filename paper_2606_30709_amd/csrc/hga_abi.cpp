@@ -86,8 +86,9 @@ hga_status validate_params(const hga_params* p) {
     if (p->n_q_heads % p->n_kv_heads != 0)
         return fail(HGA_EINVAL, "n_q_heads (%d) must be a multiple of n_kv_heads (%d)",
                     p->n_q_heads, p->n_kv_heads);
-    if (p->n_q_heads / p->n_kv_heads > 64)
-        return fail(HGA_EUNSUPPORTED, "GQA ratio above 64 is not supported");
+    if (p->n_q_heads / p->n_kv_heads > 16)
+        return fail(HGA_EUNSUPPORTED, "GQA ratio %d above 16 is not supported",
+                    p->n_q_heads / p->n_kv_heads);
     if (static_cast<int64_t>(p->batch) * p->n_kv_heads > 65535)
         return fail(HGA_EUNSUPPORTED, "batch * n_kv_heads above 65535 is not supported");
     if (p->head_dim != 64 && p->head_dim != 128)
@@ -462,8 +463,8 @@ hga_status hga_gather_kv_cached(const hga_plan* plan, const int32_t* group_idx, 
                                 const void* k_src, const void* v_src, int64_t src_tokens,
                                 int32_t src_on_host, void* cache_k, void* cache_v,
                                 int32_t n_slots, int32_t* slot_group, int32_t* slot_used,
-                                int32_t* group_slot, int32_t* entry_slot, int32_t tick,
-                                void* k_routed, void* v_routed, int32_t* n_fetched,
+                                int32_t* group_slot, int64_t map_groups, int32_t* entry_slot,
+                                int32_t tick, void* k_routed, void* v_routed, int32_t* n_fetched,
                                 void* stream) {
     HGA_TRY(check_plan(plan));
     const hga_params& p = plan->p;
@@ -478,6 +479,10 @@ hga_status hga_gather_kv_cached(const hga_plan* plan, const int32_t* group_idx, 
         return fail(HGA_EINVAL, "k_src/v_src hold %lld tokens per head; the causal past of query "
                     "chunk %d needs %lld", static_cast<long long>(src_tokens), c,
                     static_cast<long long>(need));
+    if (map_groups < src_tokens / p.group)
+        return fail(HGA_EINVAL, "group_slot holds %lld groups per head; a %lld-token source has "
+                    "%lld", static_cast<long long>(map_groups), static_cast<long long>(src_tokens),
+                    static_cast<long long>(src_tokens / p.group));
     if (hga::gather_cached_lds_bytes(*plan, n_slots) > static_cast<size_t>(plan->max_lds))
         return fail(HGA_EUNSUPPORTED, "cache bookkeeping for %d slots exceeds the LDS limit",
                     n_slots);
@@ -499,7 +504,7 @@ hga_status hga_gather_kv_cached(const hga_plan* plan, const int32_t* group_idx, 
     clear_stale_error();
     return launched(hga::launch_gather_kv_cached(*plan, group_idx, c, ks, vs, src_tokens, cache_k,
                                                  cache_v, n_slots, slot_group, slot_used,
-                                                 group_slot, src_tokens / p.group, tick,
+                                                 group_slot, map_groups, tick,
                                                  entry_slot, k_routed, v_routed, n_fetched,
                                                  static_cast<hipStream_t>(stream)),
                     "hga_gather_kv_cached launch");

@@ -85,8 +85,8 @@ def library() -> ctypes.CDLL:
                                          vp, vp],
             "hga_route_qbar": [vp, vp, i32, i32, vp, vp, i32, vp, vp, vp],
             "hga_gather_kv": [vp, vp, i32, i32, vp, vp, i64, i32, vp, vp, vp],
-            "hga_gather_kv_cached": [vp, vp, i32, vp, vp, i64, i32, vp, vp, i32, vp, vp, vp, vp,
-                                     i32, vp, vp, vp, vp],
+            "hga_gather_kv_cached": [vp, vp, i32, vp, vp, i64, i32, vp, vp, i32, vp, vp, vp, i64,
+                                     vp, i32, vp, vp, vp, vp],
             "hga_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, i64,
@@ -282,7 +282,8 @@ class WarmCache:
         i32 = torch.int32
         self.slot_group = torch.full((*bh, n_slots), -1, dtype=i32, device=device)
         self.slot_used = torch.full((*bh, n_slots), -1, dtype=i32, device=device)
-        self.group_slot = torch.full((*bh, src_tokens // p.group), -1, dtype=i32, device=device)
+        self.map_groups = src_tokens // p.group
+        self.group_slot = torch.full((*bh, self.map_groups), -1, dtype=i32, device=device)
         self.entry_slot = torch.empty((*bh, p.topk_groups), dtype=i32, device=device)
         self.tick = 0
 
@@ -296,7 +297,7 @@ def hga_gather_kv_cached(plan: Plan, group_idx, c: int, k_src, v_src, cache: War
         plan.handle, _ptr(group_idx), c, _ptr(k_src), _ptr(v_src), k_src.shape[2],
         int(bool(src_on_host)), _ptr(cache.k), _ptr(cache.v), cache.n_slots,
         _ptr(cache.slot_group), _ptr(cache.slot_used), _ptr(cache.group_slot),
-        _ptr(cache.entry_slot), cache.tick,
+        cache.map_groups, _ptr(cache.entry_slot), cache.tick,
         _ptr(k_routed), _ptr(v_routed), _ptr(n_fetched), _stream(stream)))
     cache.tick += 1
 

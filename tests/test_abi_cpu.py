@@ -63,6 +63,7 @@ def _params(**kw):
     (dict(rope_base=float("inf")), -1),
     (dict(batch=0), -1),
     (dict(hf_pairs_chunk=2, hf_pairs_group=5), -2),
+    (dict(n_q_heads=34, n_kv_heads=2), -2),      # GQA ratio 17: above the tested 16
 ])
 def test_plan_rejects_bad_params_before_touching_a_device(bad, status):
     lib = hga.library()
@@ -93,7 +94,7 @@ def test_calls_reject_null_plan():
     assert lib.hga_gather_attend_split(None, None, 0, 0, None, None, 0, None, None, None, 0, 0,
                                        None, None, None, None, None, None, 0, None) == -1
     assert lib.hga_gather_kv_cached(None, None, 0, None, None, 0, 0, None, None, 0, None, None,
-                                    None, None, 0, None, None, None, None) == -1
+                                    None, 0, None, 0, None, None, None, None) == -1
     assert lib.hga_attend_backward(None, None, 0, 0, None, None, 0, None, None, None, None, None,
                                    None, None, None) == -1
     assert lib.hga_gather_attend(None, None, 0, 0, None, None, 0, None, None, None, None, None,

@@ -67,6 +67,16 @@ SMALL = {
                    topk_groups=6),
     "gqa2_d128": W_("qwen32k", seq_len=2048, n_q_heads=4, n_kv_heads=2, topk_chunks=5,
                     topk_groups=9, keep_last=1),
+    # four and sixteen query heads per KV head (the largest ratio the ABI accepts)
+    "gqa4_d64": W_("smalllm", batch=1, seq_len=2048, n_q_heads=8, n_kv_heads=2, topk_chunks=4,
+                   topk_groups=7),
+    "gqa4_d128": W_("qwen32k", seq_len=2048, n_q_heads=8, n_kv_heads=2, topk_chunks=5,
+                    topk_groups=9),
+    "gqa16_d64": W_("smalllm", batch=1, seq_len=2048, n_q_heads=16, n_kv_heads=1, topk_chunks=4,
+                    topk_groups=7),
+    "gqa16_d128": W_("qwen32k", seq_len=2048, n_q_heads=32, n_kv_heads=2, topk_chunks=5,
+                     topk_groups=9),
+    "f32_gqa16": W_("tiny", n_q_heads=16, n_kv_heads=1),
     "tiny_noforce": W_("tiny", force_prev=0),
     "f32_d128_gqa": W_("tiny", seq_len=1024, n_q_heads=4, n_kv_heads=2, head_dim=128,
                        rope_base=1e6, topk_chunks=3, topk_groups=5, keep_last=2),
@@ -332,10 +342,12 @@ def test_gather_attend_equals_separate_calls(hga, key):
 
 
 SPLIT_CASES = {k: SMALL[k] for k in ("qwen_4k_ragged", "qwen_g8", "qwen_g32", "gqa3_d64",
-                                     "mha_d128", "f32_d128_gqa")}
+                                     "mha_d128", "f32_d128_gqa", "gqa4_d64", "gqa16_d64",
+                                     "gqa4_d128", "gqa16_d128")}
 
 
 BWD_CASES = {k: SMALL[k] for k in ("smalllm_2k", "gqa2_d64", "gqa2_d128", "gqa3_d64",
+                                   "gqa4_d64", "gqa4_d128", "gqa16_d64", "gqa16_d128",
                                    "qwen_4k_ragged", "qwen_g8",
                                    "qwen_g32", "mha_d128", "qwen_chunks_4k")}
 

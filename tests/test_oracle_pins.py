@@ -304,6 +304,139 @@ def test_summary_all_high_frequency_is_plain_mean():
     assert np.max(np.abs(got - k.reshape(1, 2, 4, 64, 64).mean(axis=3))) < 1e-15
 
 
+# ------------------------------------------ magnitudes behind the fp32 bounds ---
+# summary_magnitudes and query_magnitudes size the rounding bounds of every
+# GPU summary / q_bar comparison and of the selection margins, so each is
+# pinned to closed forms a dropped abs, a wrong phase table or a mean over the
+# wrong axis would fail.
+
+def test_summary_magnitudes_all_high_frequency_is_mean_abs():
+    """No pair turns (every pair high-frequency): the magnitude a summary
+    element accumulates is the span mean of |k| (Sec. 3.2 rotated mean)."""
+    rng = np.random.default_rng(12)
+    k = rng.standard_normal((2, 3, 128, 64))
+    got = O.summary_magnitudes(k, 16, 1e4, 32)
+    want = np.abs(k).reshape(2, 3, 8, 16, 64).mean(axis=3)
+    assert np.max(np.abs(got - want)) < 1e-15
+
+
+@pytest.mark.parametrize("d,base", [(64, 1e4), (128, 1e6)])
+@pytest.mark.parametrize("span", [64, 16])
+def test_summary_magnitudes_of_a_constant_key_closed_form(d, base, span):
+    """Every token of every span holds the same rotated key: the unit half
+    vector e_a (ones in the first half) or e_b (ones in the second half).  A
+    low-frequency pair is turned by phi = (m - o) theta with m - o running over
+    the symmetric offsets +-1/2 .. +-(span-1)/2, a high-frequency pair not at
+    all, so the magnitudes are span means of |cos phi| and |sin phi|.  For a
+    pair whose wavelength exceeds 2*span every |phi| < pi/2, and the sums of
+    cosines and sines of an arithmetic progression give
+        mean |cos phi| = sin(span theta/2) / (span sin(theta/2))
+        mean |sin phi| = (2/span) sin^2(span theta/4) / sin(theta/2)."""
+    half = d // 2
+    theta = base ** (-2.0 * np.arange(half) / d)
+    nhf = O.high_freq_pairs(span, d, base)
+    hf = np.arange(half) < nhf
+    cos_m = np.where(hf, 1.0, np.sin(span * theta / 2) / (span * np.sin(theta / 2)))
+    sin_m = np.where(hf, 0.0, (2.0 / span) * np.sin(span * theta / 4) ** 2 / np.sin(theta / 2))
+    covered = hf | (2 * np.pi / theta > 2 * span)
+    assert covered.sum() >= half - 3
+    for first in (True, False):
+        key = np.zeros(d)
+        key[:half] = 1.0 if first else 0.0
+        key[half:] = 0.0 if first else 1.0
+        k = np.broadcast_to(key, (1, 2, 3 * span, d)).copy()
+        got = O.summary_magnitudes(k, span, base, nhf)
+        assert got.shape == (1, 2, 3, d)
+        lo, hi = got[..., :half], got[..., half:]
+        want_lo, want_hi = (cos_m, sin_m) if first else (sin_m, cos_m)
+        assert np.max(np.abs(lo[..., covered] - want_lo[covered])) < 1e-13
+        assert np.max(np.abs(hi[..., covered] - want_hi[covered])) < 1e-13
+    # the sine part of the low-frequency pairs is what a dropped abs would zero
+    assert np.all(sin_m[~hf] > 1e-6)
+
+
+def test_summary_magnitudes_bound_the_summaries():
+    """Triangle inequality: |summary| <= magnitude elementwise, with equality
+    for keys whose every term has one sign (all-high-frequency, positive)."""
+    rng = np.random.default_rng(13)
+    k = rng.standard_normal((1, 2, 256, 128))
+    for span in (64, 16):
+        nhf = O.high_freq_pairs(span, 128, 1e6)
+        s = O.summaries(k, span, 1e6, nhf)
+        m = O.summary_magnitudes(k, span, 1e6, nhf)
+        assert np.all(np.abs(s) <= m * (1 + 1e-12))
+        assert np.mean(np.abs(s) / m) < 0.5
+    kp = np.abs(k)
+    assert np.max(np.abs(O.summaries(kp, 64, 1e6, 64) - O.summary_magnitudes(kp, 64, 1e6, 64))) < 1e-14
+
+
+def test_query_magnitudes_of_a_signed_pattern():
+    """q[h, t, i] = (-1)^t (h + 1)(i + 1): the chunk's tokens cancel, so q_bar
+    is 0, while the magnitude is the mean of (h + 1) over KV head j's query
+    heads j*r .. j*r + r - 1 times (i + 1), i.e. (j*r + (r + 1)/2)(i + 1)."""
+    B, Hq, Hkv, T, d = 2, 8, 2, 128, 6
+    sign = (-1.0) ** np.arange(T)
+    q = ((np.arange(Hq) + 1.0)[:, None, None] * sign[None, :, None]
+         * (np.arange(d) + 1.0)[None, None, :])
+    q = np.broadcast_to(q[None], (B, Hq, T, d)).copy()
+    r = Hq // Hkv
+    qm = O.query_magnitudes(q, Hkv, 64)
+    assert qm.shape == (B, Hkv, T // 64, d)
+    assert np.all(O.query_means(q, Hkv, 64) == 0.0)
+    for j in range(Hkv):
+        want = (j * r + (r + 1) / 2.0) * (np.arange(d) + 1.0)
+        assert np.max(np.abs(qm[:, j] - want)) < 1e-12
+
+
+def test_rounding_bounds_dominate_an_fp32_evaluation():
+    """The bounds the GPU comparisons use (tests/parity_util.py) hold for a
+    plain fp32 evaluation of the same sums, accumulated in sequence: the
+    summaries from fp32 keys and fp32 phase factors, q_bar over r*C rows, and
+    each score as an fp32 dot product of the two."""
+    from parity_util import score_bounds, summary_bound
+    rng = np.random.default_rng(14)
+    B, Hq, Hkv, N, d, base = 1, 4, 1, 512, 128, 1e6
+    f32 = np.float32
+    k = rng.standard_normal((B, Hkv, N, d)).astype(f32).astype(np.float64)
+    q = rng.standard_normal((B, Hq, N, d)).astype(f32).astype(np.float64)
+    half = d // 2
+    for span in (64, 16):
+        nhf = O.high_freq_pairs(span, d, base)
+        phi = O.span_phases(span, d, base, nhf)
+        c32, s32 = np.cos(phi).astype(f32), np.sin(phi).astype(f32)
+        kk = k.reshape(B, Hkv, N // span, span, d).astype(f32)
+        acc = np.zeros((B, Hkv, N // span, d), f32)
+        for o in range(span):
+            a, b = kk[..., o, :half], kk[..., o, half:]
+            acc[..., :half] = acc[..., :half] + (a * c32[o] - b * s32[o])
+            acc[..., half:] = acc[..., half:] + (a * s32[o] + b * c32[o])
+        got = acc * f32(1.0 / span)
+        exact = O.summaries(k, span, base, nhf)
+        mag = O.summary_magnitudes(k, span, base, nhf)
+        err = np.abs(got.astype(np.float64) - exact)
+        assert np.all(err <= summary_bound(mag, span))
+        assert err.max() > 0
+        if span != 64:
+            continue
+        r, C = Hq // Hkv, 64
+        qq = q.reshape(B, Hkv, r, N // C, C, d).astype(f32)
+        qacc = np.zeros((B, Hkv, N // C, d), f32)
+        for h in range(r):
+            for t in range(C):
+                qacc = qacc + qq[:, :, h, :, t]
+        qb32 = qacc * f32(1.0 / (r * C))
+        qb = O.query_means(q, Hkv, C)
+        qmag = O.query_magnitudes(q, Hkv, C)
+        assert np.all(np.abs(qb32 - qb) <= summary_bound(qmag, r * C))
+        for c in range(N // C):
+            sc32 = np.zeros(N // C, f32)
+            for i in range(d):
+                sc32 = sc32 + qb32[0, 0, c, i] * got[0, 0, :, i]
+            exact_sc = exact[0, 0] @ qb[0, 0, c]
+            eps = score_bounds(qb[0, 0, c], exact[0, 0], qmag[0, 0, c], mag[0, 0], span, r * C, d)
+            assert np.all(np.abs(sc32 - exact_sc) <= eps)
+
+
 # ------------------------------------------------------------- query means ---
 
 def test_query_means_group_consecutive_heads():
