@@ -157,8 +157,8 @@ hga_status hga_build_summaries(const hga_plan* plan, const void* k_rot, int64_t 
  *   qbar       fp32 out [batch, n_kv_heads, n_q_chunks, head_dim]
  *   chunk_idx  int32 out [batch, n_kv_heads, n_q_chunks, topk_chunks]
  * Requires q_chunk0 >= 0, n_q_chunks >= 0 and q_chunk0 + n_q_chunks - 1 <=
- * table_chunks.  HGA_EUNSUPPORTED when a query chunk has more than 16384
- * middle chunks. */
+ * table_chunks.  HGA_EUNSUPPORTED when a query chunk has more than 262144
+ * (2^18) middle chunks. */
 hga_status hga_route_chunks(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                             int32_t n_q_chunks, const float* chunk_sum, int32_t table_chunks,
                             float* qbar, int32_t* chunk_idx, void* stream);

@@ -17,8 +17,9 @@ struct hga_plan {
 
 namespace hga {
 
-// Largest candidate lists the routing kernels keep in LDS.
-constexpr int kMaxChunkCandidates = 16384;
+// Most middle chunks a query chunk may have (2^18: a 16.7M-token context);
+// beyond 1024 the routing streams the table and keeps no per-candidate list.
+constexpr int kMaxChunkCandidates = 1 << 18;
 constexpr int kMaxTopK = 512;
 
 // visible-window length W = max(L, force_prev ? 1 : 0)

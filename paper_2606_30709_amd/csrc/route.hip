@@ -319,14 +319,17 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
 
 // Top-k by a whole workgroup of kThreads threads, for keys whose ids ascend
 // with their position: writes the k ids with the largest keys to sel[0 .. k)
-// in ascending order (0 < k <= n); sel is complete when it returns.  Every
-// thread must call it.  Short lists (and lists longer than kMaxPer keys per
-// thread) go to wave 0's wave_select_topk.  Otherwise thread t holds keys
-// t, t + kThreads, ... and:
-// 1. each wave finds T_w, the k-th largest score word among its own keys
-//    (bit-by-bit bisection on ballot counts; 0 if it holds fewer than k);
-//    the k-th largest word of all keys is at least L = max_w T_w, so every
-//    key of the top k has a word >= L;
+// in ascending order (0 < k <= n <= kMaxPer * kThreads); sel is complete
+// when it returns.  Every thread must call it.  Short lists (n <= 256) go to
+// wave 0's wave_select_topk.  Otherwise thread t holds keys t, t + kThreads,
+// ... in registers and:
+// 1. a lower bound L on the k-th largest score word is found, in one of two
+//    forms.  For k <= kTopW * (waves): each wave hands over its kTopW largest
+//    words (one key removed per round) and wave 0 takes the k-th largest of
+//    those words, each of a different key.  For larger k: each wave finds its
+//    own k-th largest word (bisection on ballot counts; 0 if it holds fewer
+//    than k keys) and L is the largest of them.  Either way at least k keys
+//    have a word >= L, so every key of the top k does;
 // 2. the keys with word >= L (usually a few times k) are compacted in
 //    position order, which keeps ids ascending;
 // 3. wave 0 selects the top k of those with wave_select_topk.
@@ -351,7 +354,7 @@ __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int
     constexpr int kMaxPer = WgSelect<kThreads>::kMaxPer;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    if (n <= 256 || n > kMaxPer * kThreads) {
+    if (n <= 256) {
         if (wave == 0) wave_select_topk(keys, n, k, sel, scr, true);
         __syncthreads();
         return;
@@ -669,6 +672,227 @@ __global__ __launch_bounds__(1024) void route_wide_kernel(
         for (int t = lane; t < topk_groups; t += 64) gout[t] = L.sel[t];
 }
 
+// Routing of units with more middle chunks than the other kernels hold as
+// key lists (long contexts: the exhaustive scan of the summary table the
+// paper names as its limit, Sec. 3.6 and Sec. 7), one workgroup of
+// kLongThreads per unit.  The table streams through LDS in blocks of
+// kLongRows rows (the next block in registers while the current one is
+// scored); a quad scores a row with the arithmetic of the other kernels
+// (lane qd sums the dimensions d = qd mod 4 in order, the quad adds the four
+// sums pairwise), so every score, and hence every key, is bit-identical to
+// theirs.  Only keys above the running cut are kept, in an LDS buffer of
+// kLongCap keys; when it cannot take another block, an exact selection
+// (long_select) reduces it to its k largest keys and the k-th becomes the
+// cut.  Keys are unique (score word, then the complemented id), so selecting
+// by key value is the lowest-index tie rule.  The group stage scores its
+// candidates with batch_keys into the same buffer and selects the same way.
+constexpr int kLongThreads = 512;
+constexpr int kLongRows = kLongThreads / 4;   // one table row per quad
+constexpr int kLongCap = 4096;                // >= every group list (K_c * chunk/group)
+constexpr int kLongPer = kLongCap / kLongThreads;
+static_assert(kLongCap >= kMaxTopK + kLongRows, "a reduced buffer takes a further block");
+
+struct LongCtl {
+    uint64_t cut;                           // keys above it are kept
+    int n;                                  // keys in the buffer
+    int cnt[2][kLongThreads / 64];          // per-wave counts of a bisection step
+};
+
+// The k largest of the n keys of buf (0 < k <= n <= kLongCap), left in
+// buf[0 .. k) in no particular order; returns the k-th largest key.  The
+// k-th largest key T is found bit by bit from the top (T grows by a bit
+// while at least k keys are >= it: one count per step, summed over the
+// waves through LDS), then the keys >= T, exactly k of them, are compacted.
+// Every thread must call it; the buffer is complete when it returns.
+__device__ uint64_t long_select(uint64_t* buf, int n, int k, LongCtl* ctl) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    constexpr int NW = kLongThreads / 64;
+    uint64_t key[kLongPer];
+#pragma unroll
+    for (int i = 0; i < kLongPer; ++i) {
+        const int x = tid + i * kLongThreads;
+        key[i] = x < n ? buf[x] : 0;  // 0 is below every key
+    }
+    uint64_t T = 0;
+    for (int bit = 63; bit >= 0; --bit) {
+        const uint64_t c = T | (uint64_t(1) << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int i = 0; i < kLongPer; ++i) cnt += __popcll(__ballot(key[i] >= c));
+        const int par = bit & 1;
+        if (lane == 0) ctl->cnt[par][wave] = cnt;
+        __syncthreads();
+        int tot = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) tot += ctl->cnt[par][w];
+        if (tot >= k) T = c;
+    }
+    // every thread holds its keys; the buffer is rewritten from the start
+    if (tid == 0) ctl->n = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kLongPer; ++i) {
+        const bool keep = key[i] >= T && key[i] != 0;
+        const uint64_t m = __ballot(keep);
+        int base = 0;
+        if (lane == 0 && m) base = atomicAdd(&ctl->n, __popcll(m));
+        base = __shfl(base, 0);
+        if (keep) buf[base + __popcll(m & ((uint64_t(1) << lane) - 1))] = key[i];
+    }
+    __syncthreads();
+    return T;
+}
+
+// The ids of buf[0 .. k) (k <= kLongThreads), ascending, to sel.
+__device__ __forceinline__ void long_sorted_ids(const uint64_t* buf, int k, int* sel) {
+    const int tid = threadIdx.x;
+    if (tid < k) {
+        const int id = key_index(buf[tid]);
+        int rank = 0;
+        for (int t = 0; t < k; ++t) rank += key_index(buf[t]) < id;
+        sel[rank] = id;
+    }
+    __syncthreads();
+}
+
+template <typename T, int D, bool kGroups, bool kQbarIn>
+__global__ __launch_bounds__(kLongThreads) void route_long_kernel(
+    const T* __restrict__ q_rot, int q_chunk0, int n_q_chunks, const float* __restrict__ chunk_sum,
+    const float* __restrict__ group_sum, int table_chunks, float* __restrict__ qbar,
+    int32_t* __restrict__ chunk_idx, int32_t* __restrict__ group_idx, int n_q_heads, int n_kv,
+    int keep_first, int window, int topk, int topk_groups, int gpc_shift) {
+    constexpr int F4 = D / 4;                       // float4 per table row
+    constexpr int TS = D + 4;                       // padded LDS row stride (floats)
+    constexpr int PF = kLongRows * F4 / kLongThreads;  // float4 per thread per block
+    __shared__ __align__(16) float s_q[D];
+    __shared__ __align__(16) float s_tab[kLongRows * TS];
+    __shared__ uint64_t s_buf[kLongCap];
+    __shared__ int s_sel[kMaxTopK];
+    __shared__ int s_list[kMaxTopK];
+    __shared__ LongCtl ctl;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int unit = blockIdx.x;
+    const int bh = unit / n_q_chunks, i = unit % n_q_chunks;
+    const int b = bh / n_kv, j = bh % n_kv, r = n_q_heads / n_kv;
+    const int c = q_chunk0 + i;
+    const int gpc = 1 << gpc_shift;
+
+    int n = c - window - keep_first;  // middle chunks [keep_first, keep_first + n)
+    if (n < 0) n = 0;
+    const float* table = chunk_sum + (static_cast<int64_t>(bh) * table_chunks + keep_first) * D;
+    const buf_rsrc t_rsrc = make_rsrc(table, static_cast<uint32_t>(n) * D * sizeof(float));
+    float4 pf[PF];
+    auto fetch_block = [&](int r0) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int x = tid + u * kLongThreads;
+            const uint32_t off =
+                (static_cast<uint32_t>(r0 + x / F4) * D + (x % F4) * 4) * sizeof(float);
+            pf[u] = __builtin_bit_cast(float4, buf_load16(t_rsrc, off));
+        }
+    };
+    if (n > 0) fetch_block(0);
+
+    // 1. q_bar (wave 0 forms it with the packed kernel's code, or reads it)
+    if (tid == 0) {
+        ctl.cut = 0;
+        ctl.n = 0;
+    }
+    if constexpr (kQbarIn) {
+        if (tid < D / 4)
+            *reinterpret_cast<float4*>(s_q + tid * 4) =
+                *reinterpret_cast<const float4*>(qbar + static_cast<int64_t>(unit) * D + tid * 4);
+    } else {
+        if (wave == 0) {
+            wave_query_mean<T, D>(q_rot, b, j, i, n_q_heads, r, n_q_chunks, s_q);
+            wave_sync_lds();
+            if (lane < D / 4)
+                *reinterpret_cast<float4*>(qbar + static_cast<int64_t>(unit) * D + lane * 4) =
+                    *reinterpret_cast<const float4*>(s_q + lane * 4);
+        }
+    }
+    __syncthreads();
+
+    // 2. chunk scores, a block of kLongRows rows at a time; keys above the
+    // cut are appended to the buffer, which is reduced to the top k whenever
+    // it could not take another block
+    const int k = n < topk ? n : topk;
+    const int qd = lane & 3;
+    const int rl = tid >> 2;  // this quad's row within a block
+    float qv[F4];
+#pragma unroll
+    for (int f = 0; f < F4; ++f) qv[f] = s_q[4 * f + qd];
+    for (int r0 = 0; r0 < n; r0 += kLongRows) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int x = tid + u * kLongThreads;
+            *reinterpret_cast<float4*>(s_tab + (x / F4) * TS + (x % F4) * 4) = pf[u];
+        }
+        __syncthreads();
+        if (r0 + kLongRows < n) fetch_block(r0 + kLongRows);
+        const float* row = s_tab + rl * TS + qd;
+        float a = 0.f;
+#pragma unroll
+        for (int f = 0; f < F4; ++f) a = fmaf(qv[f], row[4 * f], a);
+        a = add_quad<0xb1>(a);  // (s0 + s1), (s2 + s3)
+        a = add_quad<0x4e>(a);  // (s0 + s1) + (s2 + s3)
+        const int m = r0 + rl;
+        const uint64_t key = select_key(a, keep_first + m);
+        const bool keep = qd == 0 && m < n && key > ctl.cut;
+        const uint64_t mm = __ballot(keep);
+        int base = 0;
+        if (lane == 0 && mm) base = atomicAdd(&ctl.n, __popcll(mm));
+        base = __shfl(base, 0);
+        if (keep) s_buf[base + __popcll(mm & ((uint64_t(1) << lane) - 1))] = key;
+        __syncthreads();  // the block is scored and appended
+        const int nb = ctl.n;
+        if (nb > kLongCap - kLongRows) {
+            const uint64_t cut = long_select(s_buf, nb, k, &ctl);
+            if (tid == 0) ctl.cut = cut;
+            __syncthreads();
+        }
+    }
+
+    // 3. top-k chunks, ascending, -1 padded
+    int32_t* out = chunk_idx + static_cast<int64_t>(unit) * topk;
+    if (k > 0) {
+        const int nb = ctl.n;
+        if (nb > k) long_select(s_buf, nb, k, &ctl);
+        long_sorted_ids(s_buf, k, s_sel);
+    }
+    for (int t = tid; t < topk; t += kLongThreads) out[t] = t < k ? s_sel[t] : -1;
+    if constexpr (!kGroups) return;
+
+    // 4. group refinement of the chosen chunks (every candidate kept when
+    // the budget covers them: ascending, written without scoring)
+    const int ng = k * gpc;
+    int32_t* gout = group_idx + static_cast<int64_t>(unit) * topk_groups;
+    if (ng <= topk_groups) {
+        for (int t = tid; t < topk_groups; t += kLongThreads)
+            gout[t] = t < ng ? s_sel[t >> gpc_shift] * gpc + (t & (gpc - 1)) : -1;
+        return;
+    }
+    for (int t = tid; t < k; t += kLongThreads) s_list[t] = s_sel[t];
+    __syncthreads();
+    const float* gtab = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
+    for (int m0 = wave * 16; m0 < ng; m0 += 16 * (kLongThreads / 64)) {
+        const int rem = ng - m0;
+        batch_keys<D, 1>(
+            s_q, gtab,
+            [&](int kk) {
+                const int m = m0 + (kk < rem ? kk : rem - 1);
+                return s_list[m >> gpc_shift] * gpc + (m & (gpc - 1));
+            },
+            rem, s_buf + m0);
+    }
+    __syncthreads();
+    long_select(s_buf, ng, topk_groups, &ctl);
+    long_sorted_ids(s_buf, topk_groups, s_sel);
+    for (int t = tid; t < topk_groups; t += kLongThreads) gout[t] = s_sel[t];
+}
+
 // Up to four waves per workgroup, as many as the LDS budget allows.
 int waves_per_block(size_t wave_bytes, int max_lds) {
     int w = static_cast<int>(static_cast<size_t>(max_lds) / wave_bytes);
@@ -701,8 +925,13 @@ inline RouteGeom route_geom(const hga_plan& plan, int n_max, bool groups) {
 }
 
 // Launches with at most this many units route each unit with a whole
-// workgroup (route_wide_kernel); larger ones pack four units per workgroup.
+// workgroup (route_wide_kernel, for up to kWideMaxCandidates middle chunks:
+// four keys per thread in its selection); larger ones pack four units per
+// workgroup (route_kernel, up to kPackedMaxCandidates: sixteen keys per
+// lane).  Longer candidate lists take route_long_kernel.
 constexpr int kWideMaxUnits = 128;
+constexpr int kWideMaxCandidates = WgSelect<1024>::kMaxPer * 1024;
+constexpr int kPackedMaxCandidates = 1024;
 
 // LDS of route_wide_kernel: the WaveLds pieces (keys for the larger
 // candidate list), then one region (at the returned offset) for the staged
@@ -738,24 +967,31 @@ hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0,
     const hga_params& p = plan.p;
     const int n_max = middle_count(p, q_chunk0 + n_q_chunks - 1);
     const int units = p.batch * p.n_kv_heads * n_q_chunks;
-    if (units <= kWideMaxUnits) {
+    const int gpc = p.chunk / p.group;
+    const int gpc_shift = gpc == 8 ? 3 : (gpc == 4 ? 2 : 1);
+    if (units <= kWideMaxUnits && n_max <= kWideMaxCandidates) {
         const WideGeom wg = route_wide_geom(plan, n_max, kGroups, kQbarIn);
         if (wg.total <= static_cast<size_t>(plan.max_lds)) {
-            const int gpc = p.chunk / p.group;
             hipLaunchKernelGGL((route_wide_kernel<T, D, kGroups, kQbarIn>), dim3(units),
                                dim3(1024), wg.total, stream, static_cast<const T*>(q_rot),
                                q_chunk0, n_q_chunks, chunk_sum, group_sum, table_chunks, qbar,
                                chunk_idx, group_idx, p.n_q_heads, p.n_kv_heads, p.keep_first,
-                               recent_window(p), p.topk_chunks, p.topk_groups,
-                               gpc == 8 ? 3 : (gpc == 4 ? 2 : 1), static_cast<int>(wg.big_off));
+                               recent_window(p), p.topk_chunks, p.topk_groups, gpc_shift,
+                               static_cast<int>(wg.big_off));
             return hipGetLastError();
         }
+    }
+    if (n_max > kPackedMaxCandidates) {
+        hipLaunchKernelGGL((route_long_kernel<T, D, kGroups, kQbarIn>), dim3(units),
+                           dim3(kLongThreads), 0, stream, static_cast<const T*>(q_rot), q_chunk0,
+                           n_q_chunks, chunk_sum, group_sum, table_chunks, qbar, chunk_idx,
+                           group_idx, p.n_q_heads, p.n_kv_heads, p.keep_first, recent_window(p),
+                           p.topk_chunks, p.topk_groups, gpc_shift);
+        return hipGetLastError();
     }
     const RouteGeom g = route_geom(plan, n_max, kGroups);
     const int upb = g.units_per_block < n_q_chunks ? g.units_per_block : n_q_chunks;
     const int blocks = p.batch * p.n_kv_heads * ((n_q_chunks + upb - 1) / upb);
-    const int gpc = p.chunk / p.group;
-    const int gpc_shift = gpc == 8 ? 3 : (gpc == 4 ? 2 : 1);
     hipLaunchKernelGGL((route_kernel<T, D, kGroups, kQbarIn>), dim3(blocks), dim3(256), g.total,
                        stream,
                        static_cast<const T*>(q_rot), q_chunk0, n_q_chunks, chunk_sum, group_sum,
@@ -808,7 +1044,15 @@ hipError_t launch_groups_t(const hga_plan& plan, const float* qbar, const int32_
 }  // namespace
 
 size_t route_lds_bytes(const hga_plan& plan, int n_max, bool groups) {
-    // smallest configuration (one wavefront per block) must fit
+    // beyond the packed kernel's lists: route_long_kernel, whose LDS does not
+    // depend on the candidate count
+    if (n_max > kPackedMaxCandidates) {
+        const int d = plan.p.head_dim;
+        return sizeof(float) * d + sizeof(float) * kLongRows * (d + 4) +
+               sizeof(uint64_t) * kLongCap + 2 * sizeof(int) * kMaxTopK + sizeof(LongCtl);
+    }
+    // otherwise the smallest packed configuration (one wavefront per block)
+    // must fit
     const hga_params& p = plan.p;
     const int gpc = p.chunk / p.group;
     const int nk = groups && p.topk_chunks * gpc > n_max ? p.topk_chunks * gpc : n_max;
