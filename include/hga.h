@@ -353,6 +353,32 @@ hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_c
  * NULL or invalid plan or n_q_chunks < 0. */
 int64_t hga_attend_split_workspace(const hga_plan* plan, int32_t n_q_chunks);
 
+/* hga_attend_split without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the split partial results go to a fixed
+ * array of hga_static_scratch_bytes() (16 MiB) that the library holds on every
+ * device it runs on, from the first plan created there until the process
+ * ends.  The call allocates nothing and writes exactly what
+ *   hga_attend_split(..., workspace = that array,
+ *                    workspace_bytes = hga_static_scratch_bytes(), stream)
+ * writes (same split count, same out and lse bit for bit).
+ * Limit: where the split form applies (bf16 plan, several query heads per KV
+ * head), HGA_EUNSUPPORTED when two splits of the call's units need more than
+ * the array holds (2 * hga_attend_split_workspace(plan, n_q_chunks) / 16 bytes
+ * above hga_static_scratch_bytes(); a decode block of 32/4 heads at d128 uses
+ * 2 MiB).  Every call on one device shares that device's array: calls that
+ * overlap in time on one device (different streams, or threads) race and
+ * must be serialised by the caller.  Other arguments, layouts, requirements
+ * and errors as hga_attend_split. */
+hga_status hga_attend_split_static(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                                   int32_t n_q_chunks, const void* k_res, const void* v_res,
+                                   int64_t res_tokens, const int32_t* res_slot,
+                                   const void* k_routed, const void* v_routed,
+                                   const int32_t* group_idx, void* out, float* lse, void* stream);
+
+/* Size in bytes of the per-device array hga_attend_split_static uses. */
+int64_t hga_static_scratch_bytes(void);
+
 /* Backward of hga_attend (Sec. 3.4, Eq. (1)) for the prefill layout and the
  * bf16 plan dtype: the gradients of the attention outputs with respect to
  * the rotated queries and the resident keys and values, the routing held

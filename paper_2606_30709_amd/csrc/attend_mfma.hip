@@ -972,6 +972,10 @@ int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks) {
            static_cast<int64_t>(sizeof(float));
 }
 
+bool attend_split_applies(const hga_plan& plan) {
+    return plan.p.dtype == HGA_BF16 && plan.p.n_q_heads / plan.p.n_kv_heads >= 2;
+}
+
 // Splits for a launch of n_q_chunks query chunks from q_chunk0: enough
 // workgroups to give every compute unit one, at least two key tiles per
 // split, at most what the workspace holds; 1 where the split form does not
@@ -981,7 +985,7 @@ static int choose_splits(const hga_plan& plan, int q_chunk0, int n_q_chunks,
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     int n_split = 1;
-    if (p.dtype == HGA_BF16 && r >= 2) {
+    if (attend_split_applies(plan)) {
         // enough workgroups to give every compute unit one, at least two key
         // tiles per split, at most what the workspace holds
         const int qt_per_wg = p.head_dim == 128 ? kD128Waves : 4;

@@ -206,6 +206,10 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
     int n_cu = 0;
     e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    // the device's copy of the library's static scratch (allocation-free split
+    // attention): its address, taken once per device with the device current
+    e = hga::static_scratch_init(dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (static scratch)");
     hga_plan* pl = new (std::nothrow) hga_plan();
     if (!pl) return fail(HGA_EINVAL, "out of host memory");
     pl->p = p;
@@ -597,6 +601,37 @@ hga_status hga_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_c
                                              static_cast<hipStream_t>(stream)),
                     "hga_attend_split launch");
 }
+
+hga_status hga_attend_split_static(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
+                                   int32_t n_q_chunks, const void* k_res, const void* v_res,
+                                   int64_t res_tokens, const int32_t* res_slot,
+                                   const void* k_routed, const void* v_routed,
+                                   const int32_t* group_idx, void* out, float* lse, void* stream) {
+    HGA_TRY(check_plan(plan));
+    if (q_chunk0 < 0 || n_q_chunks < 0 || res_tokens < 0)
+        return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
+    if (n_q_chunks == 0) return HGA_OK;
+    HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
+                         k_routed, v_routed, group_idx, out, lse));
+    void* scratch = hga::static_scratch(plan->device);
+    if (!scratch) return fail(HGA_EHIP, "no static scratch address for device %d", plan->device);
+    if (hga::attend_split_applies(*plan)) {
+        const int64_t per = hga::attend_split_bytes_per_split(*plan, n_q_chunks);
+        if (2 * per > hga::kStaticScratchBytes)
+            return fail(HGA_EUNSUPPORTED, "two splits of %d query chunks need %lld bytes of "
+                        "scratch, above the static %lld bytes; use hga_attend_split with a "
+                        "workspace", n_q_chunks, static_cast<long long>(2 * per),
+                        static_cast<long long>(hga::kStaticScratchBytes));
+    }
+    clear_stale_error();
+    return launched(hga::launch_attend_split(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
+                                             res_tokens, res_slot, k_routed, v_routed, group_idx,
+                                             out, lse, scratch, hga::kStaticScratchBytes,
+                                             static_cast<hipStream_t>(stream)),
+                    "hga_attend_split_static launch");
+}
+
+int64_t hga_static_scratch_bytes(void) { return hga::kStaticScratchBytes; }
 
 hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                                    int32_t n_q_chunks, const void* k_res, const void* v_res,

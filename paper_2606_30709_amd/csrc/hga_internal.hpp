@@ -89,12 +89,25 @@ hipError_t launch_attend(const hga_plan& plan, const void* q_rot, int q_chunk0, 
                          const int32_t* group_idx, void* out, float* lse, hipEvent_t start,
                          hipEvent_t stop, hipStream_t stream);
 
+// Device scratch the library holds on every device it runs on, for the
+// allocation-free split attention (its partial results): 16 MiB, the most a
+// decode block of 32 query heads over 4 KV heads at d128 uses for its splits.
+constexpr int64_t kStaticScratchBytes = int64_t(16) << 20;
+// Takes the array's device address for `device` (current) once; later calls
+// return at once.
+hipError_t static_scratch_init(int device);
+// The address static_scratch_init recorded for `device`, or null.
+void* static_scratch(int device);
+
 // Attention with each unit's key tiles divided among several workgroups
 // (bf16, r >= 2) whose partial results go to `workspace` and are merged by a
 // second kernel; other configurations, or a workspace too small for two
 // splits, run launch_attend.
 constexpr int kMaxSplit = 16;  // at most the merge kernel's slots
 int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks);
+// Whether launch_attend_split may split these query chunks at all (bf16,
+// several query heads per KV head); otherwise it runs launch_attend.
+bool attend_split_applies(const hga_plan& plan);
 hipError_t launch_attend_split(const hga_plan& plan, const void* q_rot, int q_chunk0,
                                int n_q_chunks, const void* k_res, const void* v_res,
                                int64_t res_tokens, const int32_t* res_slot, const void* k_routed,

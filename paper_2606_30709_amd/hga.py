@@ -18,7 +18,8 @@ __all__ = [
     "HgaError", "HgaParams", "Plan", "WarmCache", "library", "library_path", "F32", "BF16",
     "hga_build_summaries", "hga_route_chunks", "hga_route_groups", "hga_route",
     "hga_build_summaries_qbar", "hga_route_qbar", "hga_gather_kv", "hga_attend",
-    "hga_attend_timed", "hga_attend_split", "hga_attend_split_workspace", "hga_gather_attend",
+    "hga_attend_timed", "hga_attend_split", "hga_attend_split_workspace",
+    "hga_attend_split_static", "hga_static_scratch_bytes", "hga_gather_attend",
     "hga_gather_attend_split", "hga_gather_kv_cached", "hga_attend_backward",
     "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error",
     "hga_version", "EXPORTED_SYMBOLS",
@@ -31,7 +32,8 @@ EXPORTED_SYMBOLS = (
     "hga_plan_create", "hga_plan_destroy", "hga_plan_params", "hga_build_summaries",
     "hga_route_chunks", "hga_route_groups", "hga_route", "hga_build_summaries_qbar",
     "hga_route_qbar", "hga_gather_kv", "hga_attend", "hga_attend_timed", "hga_attend_split",
-    "hga_attend_split_workspace", "hga_gather_attend", "hga_gather_attend_split",
+    "hga_attend_split_workspace", "hga_attend_split_static", "hga_static_scratch_bytes",
+    "hga_gather_attend", "hga_gather_attend_split",
     "hga_gather_kv_cached", "hga_attend_backward", "hga_block_step", "hga_prefill_blocks",
     "hga_status_string",
     "hga_last_error", "hga_version",
@@ -91,6 +93,8 @@ def library() -> ctypes.CDLL:
             "hga_attend_timed": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_split": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, i64,
                                  vp],
+            "hga_attend_split_static": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp,
+                                        vp],
             "hga_gather_attend": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, vp],
             "hga_attend_backward": [vp, vp, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp, vp, vp,
                                     vp],
@@ -107,6 +111,8 @@ def library() -> ctypes.CDLL:
             fn.restype = i32
         lib.hga_attend_split_workspace.argtypes = [vp, i32]
         lib.hga_attend_split_workspace.restype = i64
+        lib.hga_static_scratch_bytes.argtypes = []
+        lib.hga_static_scratch_bytes.restype = i64
         lib.hga_status_string.argtypes = [i32]
         lib.hga_status_string.restype = ctypes.c_char_p
         lib.hga_last_error.argtypes = []
@@ -344,6 +350,22 @@ def hga_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v
         plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
         _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
         _ptr(workspace), nbytes, _stream(stream)))
+
+
+def hga_attend_split_static(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_routed, v_routed,
+                            group_idx, out, lse=None, res_slot=None, stream=None):
+    """hga_attend_split with the library's static per-device scratch as the
+    workspace: allocates nothing."""
+    nq = q_rot.shape[2] // plan.params.chunk
+    _check(library().hga_attend_split_static(
+        plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],
+        _ptr(res_slot), _ptr(k_routed), _ptr(v_routed), _ptr(group_idx), _ptr(out), _ptr(lse),
+        _stream(stream)))
+
+
+def hga_static_scratch_bytes() -> int:
+    """Size of the per-device array hga_attend_split_static uses."""
+    return library().hga_static_scratch_bytes()
 
 
 def hga_gather_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_src, v_src,

@@ -91,6 +91,9 @@ def test_calls_reject_null_plan():
     assert lib.hga_attend_split(None, None, 0, 0, None, None, 0, None, None, None, None, None,
                                 None, None, 0, None) == -1
     assert lib.hga_attend_split_workspace(None, 1) == -1
+    assert lib.hga_attend_split_static(None, None, 0, 0, None, None, 0, None, None, None, None,
+                                       None, None, None) == -1
+    assert lib.hga_static_scratch_bytes() == 16 << 20
     assert lib.hga_gather_attend_split(None, None, 0, 0, None, None, 0, None, None, None, 0, 0,
                                        None, None, None, None, None, None, 0, None) == -1
     assert lib.hga_gather_kv_cached(None, None, 0, None, None, 0, 0, None, None, 0, None, None,
