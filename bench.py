@@ -239,6 +239,28 @@ def cpu_baseline(w, inp, max_seconds: float, block_chunks: int = 64) -> dict:
             "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
+def measured_h2d_bandwidth(sizes=(1 << 20, 64 << 20), reps: int = 20) -> dict:
+    """GB/s of plain host-to-device copies from pinned host memory (the
+    reference for the host-link gathers), per size in bytes: the mean over
+    `reps` copies timed with events on the current stream."""
+    import torch
+    out = {}
+    for n in sizes:
+        src = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+        for _ in range(3):
+            dst.copy_(src, non_blocking=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            dst.copy_(src, non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+        out[f"{n >> 20}MiB"] = round(n * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    return out
+
+
 def measured_copy_bandwidth(nbytes: int = 1 << 30, reps: int = 10) -> float:
     """Achievable HBM bandwidth on this device: GB/s of a streaming copy of
     nbytes (each byte read once and written once), well beyond the 256 MB
@@ -323,6 +345,7 @@ def decode_bench(w, inp, args):
                    "seed": inp["seed"]},
         "pcie_bytes_per_block": pcie,
         "pcie_gbs_at_block_rate": round(pcie / dt / 1e9, 2),
+        "pcie_measured_GB_s": measured_h2d_bandwidth(),
     }
     print(json.dumps(res), flush=True)
 
@@ -339,23 +362,37 @@ def decode_sequence_bench(w, inp, args):
     from paper_2606_30709_amd.pipeline import DecodeSequencePipeline
     slots = args.cache_slots or 8 * w.topk_groups
 
-    def run(cache_slots):
+    schedule = "serial" if args.route_from_q else args.schedule
+    slots_or_none = None if args.no_cache else slots
+
+    def run(cache_slots, sched):
         pipe = DecodeSequencePipeline(w, inp, cache_slots=cache_slots,
                                       qbar_first=not args.route_from_q)
+        overlapped = sched.endswith("overlapped")
+        step = pipe.step_overlapped if overlapped else pipe.step
+        if sched.startswith("graph"):
+            step = pipe.capture(overlapped).replay
         for _ in range(args.warmup):
             pipe.reset_cache()
-            pipe.step()
+            step()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
             pipe.reset_cache()
-            pipe.step()
+            step()
         torch.cuda.synchronize()
         dt = (time.perf_counter() - t0) / args.steps
         routed = int((pipe.group_idx >= 0).sum().item())
         return dt, pipe.pcie_bytes(), routed
 
-    dt, pcie, routed = run(None if args.no_cache else slots)
+    dt, pcie, routed = run(slots_or_none, schedule)
+    descr = {
+        "serial": "route, gather, attend per block on one stream",
+        "overlapped": "gather of block b+1 on a second stream while block b attends",
+        "graph-serial": "the one-stream schedule replayed as a HIP graph",
+        "graph-overlapped": ("gather of block b+1 on a second stream while block b attends, "
+                             "the step replayed as a HIP graph (stream joins as graph edges)"),
+    }
     res = {
         "metric": "routed-attn decode tokens/s (64-token blocks in sequence)",
         "value": round(w.chunk * w.batch * w.decode_blocks / dt, 1), "unit": "tokens/s",
@@ -369,13 +406,19 @@ def decode_sequence_bench(w, inp, args):
                                 f"in pinned host memory"),
                    "seed": inp["seed"],
                    "warm_cache_slots_per_head": None if args.no_cache else slots},
+        "schedule": f"{schedule}: {descr[schedule]}",
         "us_per_block": round(dt * 1e6 / w.decode_blocks, 2),
         "pcie_bytes_per_block": pcie // w.decode_blocks,
+        "pcie_measured_GB_s": measured_h2d_bandwidth(),
         "routed_groups_fetched_from_host": round(
             pcie / (2 * w.group * w.head_dim * w.elem_bytes) / max(routed, 1), 4),
     }
+    if not args.route_from_q:
+        res["other_schedules_us_per_block"] = {
+            sc: round(run(slots_or_none, sc)[0] * 1e6 / w.decode_blocks, 2)
+            for sc in descr if sc != schedule}
     if not args.no_cache:
-        dt0, pcie0, _ = run(None)
+        dt0, pcie0, _ = run(None, schedule)
         res["uncached"] = {"us_per_block": round(dt0 * 1e6 / w.decode_blocks, 2),
                            "pcie_bytes_per_block": pcie0 // w.decode_blocks}
     print(json.dumps(res), flush=True)
@@ -498,6 +541,12 @@ def main():
                     help="decode: hga_route forms q_bar from the query rows and the block's "
                          "summaries follow it (default: hga_build_summaries_qbar first, then "
                          "hga_route_qbar)")
+    ap.add_argument("--schedule", default="graph-overlapped",
+                    choices=("serial", "overlapped", "graph-serial", "graph-overlapped"),
+                    help="decode sequence: route, gather and attend each block on one stream "
+                         "(serial), or block b+1's gather on a second stream while block b "
+                         "attends (overlapped); graph-*: the step replayed as a HIP graph "
+                         "(default graph-overlapped)")
     ap.add_argument("--no-cache", action="store_true",
                     help="decode sequence: gather every block's routed groups from host memory")
     ap.add_argument("--cache-slots", type=int, default=0,

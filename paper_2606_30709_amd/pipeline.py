@@ -405,6 +405,95 @@ class DecodeSequencePipeline:
             hga.hga_build_summaries(self.plan, self.k_res, c, c + 1, self.chunk_sum,
                                     self.group_sum, k_chunk0=k_chunk0, stream=stream)
 
+    def step_overlapped(self, copy_stream=None):
+        """All blocks, with each block's gather (the warm cache's bookkeeping
+        and copies, the misses over the host link) on `copy_stream` while the
+        previous block attends on the current stream (Sec. 4.3: the cold tier
+        feeds the warm one while the hot set computes).  Same calls and
+        results as ``step`` (routing, routed rows, outputs, cache maps): the
+        current stream runs block b+1's summaries and routing before block b's
+        attention; events order gather(b) after routing(b) and before
+        attention(b), and gather(b+2) after attention(b), whose routed buffers
+        (two sets, alternating) it overwrites.  Requires ``qbar_first`` (the
+        block's own chunk summarised before it routes)."""
+        assert self.qbar_first
+        main = torch.cuda.current_stream()
+        side = copy_stream or self._copy_stream()
+        if not hasattr(self, "k_routed2"):
+            self.k_routed2 = torch.empty((2, *self.k_routed.shape), dtype=self.k_routed.dtype,
+                                         device=self.k_routed.device)
+            self.v_routed2 = torch.empty_like(self.k_routed2)
+        ev_route = [torch.cuda.Event() for _ in range(self.n_blocks)]
+        ev_gather = [torch.cuda.Event() for _ in range(self.n_blocks)]
+        ev_attend = [torch.cuda.Event() for _ in range(self.n_blocks)]
+
+        def route(b):
+            c = self.c0 + b
+            k_chunk0 = c - int(self.slot_of[c])
+            hga.hga_build_summaries_qbar(self.plan, self.k_res, k_chunk0, c, c + 1,
+                                         self.chunk_sum, self.group_sum, self.q_blocks[b], c,
+                                         self.qbar, stream=main)
+            hga.hga_route_qbar(self.plan, self.qbar, c, self.chunk_sum, self.group_sum,
+                               self.chunk_idx, self.group_idx[b], stream=main)
+            ev_route[b].record(main)
+
+        def gather(b):
+            c = self.c0 + b
+            side.wait_event(ev_route[b])
+            if b >= 2:
+                side.wait_event(ev_attend[b - 2])
+            kr, vr = self.k_routed2[b % 2], self.v_routed2[b % 2]
+            if self.cache is not None:
+                hga.hga_gather_kv_cached(self.plan, self.group_idx[b], c, self.k_hist,
+                                         self.v_hist, self.cache, kr, vr, self.n_fetched[b],
+                                         src_on_host=True, stream=side)
+            else:
+                hga.hga_gather_kv(self.plan, self.group_idx[b], c, self.k_hist, self.v_hist, kr,
+                                  vr, src_on_host=True, stream=side)
+            ev_gather[b].record(side)
+
+        def attend(b):
+            c = self.c0 + b
+            main.wait_event(ev_gather[b])
+            hga.hga_attend_split(self.plan, self.q_blocks[b], c, self.k_res, self.v_res,
+                                 self.k_routed2[b % 2], self.v_routed2[b % 2], self.group_idx[b],
+                                 self.out[b], self.attend_ws, self.lse[b],
+                                 res_slot=self.res_slot, stream=main)
+            ev_attend[b].record(main)
+
+        route(0)
+        gather(0)
+        for b in range(self.n_blocks):
+            if b + 1 < self.n_blocks:
+                route(b + 1)
+                gather(b + 1)
+            attend(b)
+        # the copy stream's work is joined before the caller's next use
+        main.wait_event(ev_gather[self.n_blocks - 1])
+
+    def capture(self, overlapped: bool = True):
+        """One step (all blocks) recorded as a HIP graph: replaying it
+        launches every block's kernels, and with `overlapped` the two-stream
+        schedule of ``step_overlapped`` with its stream joins as graph edges
+        instead of event waits.  The calls' arguments are fixed at capture
+        (the warm cache's ticks included), so a replay is the step of a fresh
+        sequence after ``reset_cache``.  No call captured here records a
+        memset node."""
+        self.reset_cache()
+        (self.step_overlapped if overlapped else self.step)()   # warm-up, eager
+        torch.cuda.synchronize()
+        self.reset_cache()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            (self.step_overlapped if overlapped else self.step)()
+        torch.cuda.synchronize()
+        return g
+
+    def _copy_stream(self):
+        if not hasattr(self, "_side"):
+            self._side = torch.cuda.Stream()   # default priority
+        return self._side
+
     def reset_cache(self):
         """Empty the warm cache (a new sequence); its tick keeps counting."""
         if self.cache is not None:

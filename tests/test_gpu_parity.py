@@ -873,6 +873,81 @@ def test_warm_cache_gather(hga, slots_per_topk):
             assert got[bb, j] == model.call(bb * Hkv + j, [int(x) for x in gnp[bb, j, 0]], lim, tick)
 
 
+def test_decode_sequence_overlapped_equals_serial(hga):
+    """The two-stream decode schedule (block b+1's gather, through the warm
+    cache or straight from host memory, on a second stream while block b
+    attends) writes exactly what the one-stream schedule writes: every
+    block's routing, output and LSE, the per-block miss counts, the final
+    cache maps and the last block's routed buffers; run twice over the
+    sequence (cold, then warm)."""
+    from paper_2606_30709_amd.pipeline import DecodeSequencePipeline
+    w = W_("decode64k_seq", seq_len=8192 + 16 * 64, needle_depths=(12, 64, 115))
+    inp = W.generate(w)
+    n_slots = 4 * w.topk_groups
+    _say(f"[decode overlap] {w.decode_blocks} blocks, {n_slots} slots")
+    serial = DecodeSequencePipeline(w, inp, cache_slots=n_slots)
+    over = DecodeSequencePipeline(w, inp, plan=serial.plan, cache_slots=n_slots)
+    plain = DecodeSequencePipeline(w, inp, plan=serial.plan)
+    last = w.decode_blocks - 1
+    for rep in range(2):
+        for pipe in (serial, over, plain):
+            pipe.out.fill_(float("nan"))
+            pipe.lse.fill_(float("nan"))
+            pipe.group_idx.fill_(-7)
+        serial.step()
+        over.step_overlapped()
+        plain.step_overlapped()
+        torch.cuda.synchronize()
+        assert torch.equal(serial.group_idx, over.group_idx)
+        assert torch.equal(serial.group_idx, plain.group_idx)
+        for pipe in (over, plain):
+            assert torch.equal(_bits(serial.out), _bits(pipe.out))
+            assert torch.equal(serial.lse, pipe.lse)
+        assert torch.equal(serial.n_fetched, over.n_fetched)
+        assert torch.equal(_bits(serial.k_routed), _bits(over.k_routed2[last % 2]))
+        assert torch.equal(_bits(serial.v_routed), _bits(plain.v_routed2[last % 2]))
+        _say(f"  pass {rep}: {int(over.n_fetched.sum())} groups fetched from host")
+    for name in ("slot_group", "slot_used", "group_slot"):
+        assert torch.equal(getattr(serial.cache, name), getattr(over.cache, name)), name
+    assert not torch.isnan(over.out).any()
+
+
+@pytest.mark.parametrize("overlapped", [True, False])
+def test_decode_sequence_graph_replays_equal_eager(hga, overlapped):
+    """The decode sequence (16 blocks through the warm cache) recorded as a
+    HIP graph: three replays, each after emptying the cache and with eager
+    work of another pipeline in between, write exactly what one eager step
+    from an empty cache writes (routing, outputs, LSE, miss counts, the
+    cache's slot maps)."""
+    from paper_2606_30709_amd.pipeline import DecodeSequencePipeline
+    w = W_("decode64k_seq", seq_len=8192 + 16 * 64, needle_depths=(12, 64, 115))
+    inp = W.generate(w)
+    n_slots = 4 * w.topk_groups
+    _say(f"[decode graph] overlapped={overlapped}")
+    ref = DecodeSequencePipeline(w, inp, cache_slots=n_slots)
+    ref.reset_cache()
+    ref.step()
+    torch.cuda.synchronize()
+    want = {k: getattr(ref, k).clone() for k in ("out", "lse", "group_idx", "n_fetched")}
+    want_maps = {k: getattr(ref.cache, k).clone() for k in ("slot_group", "group_slot")}
+    pipe = DecodeSequencePipeline(w, inp, plan=ref.plan, cache_slots=n_slots)
+    g = pipe.capture(overlapped)
+    for rep in range(3):
+        for name in ("out", "lse"):
+            getattr(pipe, name).fill_(float("nan"))
+        pipe.reset_cache()
+        g.replay()
+        ref.reset_cache()
+        ref.step()                      # eager work between the replays
+        torch.cuda.synchronize()
+        assert torch.equal(_bits(pipe.out), _bits(want["out"])), rep
+        assert torch.equal(pipe.lse, want["lse"]), rep
+        assert torch.equal(pipe.group_idx, want["group_idx"]), rep
+        assert torch.equal(pipe.n_fetched, want["n_fetched"]), rep
+        for k, v in want_maps.items():
+            assert torch.equal(getattr(pipe.cache, k), v), (rep, k)
+
+
 def test_decode_block_parity_reduced(hga):
     w = W_("decode64k", seq_len=8192 + 64, needle_depths=(12, 64, 115))
     _decode_check(hga, w)
