@@ -239,6 +239,22 @@ def cpu_baseline(w, inp, max_seconds: float, block_chunks: int = 64) -> dict:
             "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
+def settle(step, seconds: float) -> int:
+    """Run `step` untimed, in batches of ten with a synchronization after
+    each, until `seconds` of wall time have passed (before the warm-up
+    steps): the GPU's clocks reach their steady state first, so a short timed
+    region does not measure the ramp.  Returns the steps run."""
+    import torch
+    n = 0
+    t_end = time.perf_counter() + seconds
+    while time.perf_counter() < t_end:
+        for _ in range(10):
+            step()
+        n += 10
+        torch.cuda.synchronize()
+    return n
+
+
 def measured_h2d_bandwidth(sizes=(1 << 20, 64 << 20), reps: int = 20) -> dict:
     """GB/s of plain host-to-device copies from pinned host memory (the
     reference for the host-link gathers), per size in bytes: the mean over
@@ -526,6 +542,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="CPU budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--settle-seconds", type=float, default=0.3,
+                    help="untimed steps before the warm-up steps, until this much wall time "
+                         "has passed (clocks at their steady state)")
     ap.add_argument("--dense", action="store_true",
                     help="also time dense causal attention (torch SDPA) on the same Q/K/V; "
                          "on by default for train12k")
@@ -634,9 +653,13 @@ def main():
             lambda: hga.hga_route_qbar(p, pipe.qbar, 0, pipe.chunk_sum, pipe.group_sum,
                                        pipe.chunk_idx, pipe.group_idx, stream=sh)) + tail
 
-    for _ in range(args.warmup):
+    def one_step():
         for f in calls:
             f()
+
+    settle(one_step, args.settle_seconds)
+    for _ in range(args.warmup):
+        one_step()
     torch.cuda.synchronize()
 
     # Timed region: K steps; in a sample of them spread evenly over the
