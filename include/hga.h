@@ -39,7 +39,9 @@
  * - Error strings: hga_last_error() returns the message of the last failing
  *   call on the calling thread.  No C++ exception crosses this interface.
  * - The library keeps no state between calls besides the plan, so calls on
- *   different streams may overlap as long as their buffers do not.
+ *   different streams may overlap as long as their buffers do not -- except
+ *   hga_route_qbar calls on one plan, which may share the plan's routing
+ *   workspace (and hga_attend_split_static calls on one device).
  */
 #ifndef HGA_H
 #define HGA_H
@@ -107,8 +109,9 @@ typedef struct hga_plan hga_plan;
 
 /* Validate `params`, compute the summary phase tables in double precision on
  * the host (stored as fp32) and upload them to the current device.  The plan
- * owns that device memory (a few tens of KiB) and is bound to the device
- * current at creation.  *plan is set only on HGA_OK.  Returns HGA_EINVAL /
+ * owns that device memory (a few tens of KiB) and a routing workspace of
+ * 512 KiB (see hga_route_qbar), and is bound to the device current at
+ * creation.  *plan is set only on HGA_OK.  Returns HGA_EINVAL /
  * HGA_EUNSUPPORTED for bad params before touching the device, HGA_EHIP if
  * there is no usable device. */
 hga_status hga_plan_create(const hga_params* params, hga_plan** plan);
@@ -211,7 +214,12 @@ hga_status hga_build_summaries_qbar(const hga_plan* plan, const void* k_rot, int
  * hga_build_summaries_qbar wrote; chunk_idx and group_idx are exactly what
  * hga_route writes when it computes the same q_bar itself.  qbar is read
  * only.  Arguments, layouts, requirements and errors are those of
- * hga_route. */
+ * hga_route.  A launch of at most 16 query chunks x KV heads x batch with
+ * 256..4096 middle chunks spreads each unit's table scan over several
+ * workgroups whose keys meet in the plan's routing workspace: two such calls
+ * on one plan must not run at the same time (keep a plan's routing calls on
+ * one stream, or use one plan per stream); the workspace is left ready for
+ * the next call. */
 hga_status hga_route_qbar(const hga_plan* plan, const float* qbar, int32_t q_chunk0,
                           int32_t n_q_chunks, const float* chunk_sum, const float* group_sum,
                           int32_t table_chunks, int32_t* chunk_idx, int32_t* group_idx,

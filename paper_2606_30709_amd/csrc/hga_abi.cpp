@@ -233,6 +233,24 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
     }
     pl->phase_group = buf;
     pl->phase_psi = buf + tg.size();
+    // the spread routing form's workspace: keys, then per-unit counters that
+    // start at zero (each call leaves them at zero)
+    void* ws = nullptr;
+    e = hipMalloc(&ws, hga::route_workspace_bytes());
+    if (e == hipSuccess) {
+        pl->route_keys = static_cast<uint64_t*>(ws);
+        pl->route_count = reinterpret_cast<unsigned*>(
+            static_cast<unsigned char*>(ws) +
+            sizeof(uint64_t) * hga::kRouteSpreadUnits * hga::kRouteSpreadCandidates);
+        e = hipMemset(pl->route_count, 0, sizeof(unsigned) * hga::kRouteSpreadUnits);
+        if (e == hipSuccess) e = hipDeviceSynchronize();
+    }
+    if (e != hipSuccess) {
+        (void)hipFree(ws);
+        (void)hipFree(buf);
+        delete pl;
+        return hip_fail(e, "hipMalloc/hipMemset (routing workspace)");
+    }
     *plan = pl;
     return HGA_OK;
 }
@@ -240,6 +258,8 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
 hga_status hga_plan_destroy(hga_plan* plan) {
     if (!plan) return HGA_OK;
     hipError_t e = hipFree(plan->phase_group);
+    const hipError_t e2 = hipFree(plan->route_keys);
+    if (e == hipSuccess) e = e2;
     delete plan;
     if (e != hipSuccess) return hip_fail(e, "hipFree (phase tables)");
     return HGA_OK;

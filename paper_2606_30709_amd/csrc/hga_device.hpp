@@ -137,6 +137,27 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
     return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(x), 63));
 }
 
+// x plus the value DPP control kCtrl moves into this lane (0 where nothing
+// arrives: outside the row, or rows outside kRowMask).
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int add_dpp(int x) {
+    return x + __builtin_amdgcn_update_dpp(0, x, kCtrl, kRowMask, 0xf, true);
+}
+
+// Inclusive prefix sum over the wave's lanes (lane l gets the sum of lanes
+// 0..l): the steps of wave_max_u32 with addition -- shifts by 1, 2, 4, 8
+// scan each 16-lane row, then row 0's total goes into rows 1 and 3 and the
+// total of rows 0..1 into rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan_add(int x) {
+    x = add_dpp<0x111, 0xf>(x);  // row_shr:1
+    x = add_dpp<0x112, 0xf>(x);  // row_shr:2
+    x = add_dpp<0x114, 0xf>(x);  // row_shr:4
+    x = add_dpp<0x118, 0xf>(x);  // row_shr:8
+    x = add_dpp<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+    x = add_dpp<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+    return x;
+}
+
 // Wave-wide maximum of a 64-bit key: the high words first, then the low
 // words of the lanes holding that high word -- read straight from that lane
 // when only one holds it, the usual case.

@@ -13,6 +13,11 @@ struct hga_plan {
     int n_cu;             // compute units of the device
     float* phase_group;   // device [2][group][head_dim/2]: cos then sin of phi_p(o), span = group
     float* phase_psi;     // device [2][chunk/group][head_dim/2]: cos, sin of psi_g theta_p
+    // routing workspace of the spread form (launches of a few units): keys
+    // [kRouteSpreadUnits][kRouteSpreadCandidates], then one counter per unit
+    // (zero between calls)
+    uint64_t* route_keys;
+    unsigned* route_count;
 };
 
 namespace hga {
@@ -21,6 +26,14 @@ namespace hga {
 // beyond 1024 the routing streams the table and keeps no per-candidate list.
 constexpr int kMaxChunkCandidates = 1 << 18;
 constexpr int kMaxTopK = 512;
+// Launches of at most this many units with this many middle chunks or fewer
+// may take the spread routing form, whose keys live in the plan's workspace.
+constexpr int kRouteSpreadUnits = 16;
+constexpr int kRouteSpreadCandidates = 4096;
+inline size_t route_workspace_bytes() {
+    return sizeof(uint64_t) * kRouteSpreadUnits * kRouteSpreadCandidates +
+           sizeof(unsigned) * kRouteSpreadUnits;
+}
 
 // visible-window length W = max(L, force_prev ? 1 : 0)
 inline int recent_window(const hga_params& p) {

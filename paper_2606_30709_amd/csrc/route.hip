@@ -324,12 +324,13 @@ __global__ __launch_bounds__(256) void route_groups_kernel(
 // wave 0's wave_select_topk.  Otherwise thread t holds keys t, t + kThreads,
 // ... in registers and:
 // 1. a lower bound L on the k-th largest score word is found, in one of two
-//    forms.  For k <= kTopW * (waves): each wave hands over its kTopW largest
-//    words (one key removed per round) and wave 0 takes the k-th largest of
-//    those words, each of a different key.  For larger k: each wave finds its
-//    own k-th largest word (bisection on ballot counts; 0 if it holds fewer
-//    than k keys) and L is the largest of them.  Either way at least k keys
-//    have a word >= L, so every key of the top k does;
+//    forms.  For k <= kTopW * (waves): each wave hands over its
+//    ceil(k / waves) largest words (one key removed per round) and wave 0
+//    takes the k-th largest of those words, each of a different key.  For
+//    larger k: each wave finds its own k-th largest word (bisection on ballot
+//    counts; 0 if it holds fewer than k keys) and L is the largest of them.
+//    Either way at least k keys have a word >= L, so every key of the top k
+//    does;
 // 2. the keys with word >= L (usually a few times k) are compacted in
 //    position order, which keeps ids ascending;
 // 3. wave 0 selects the top k of those with wave_select_topk.
@@ -369,17 +370,20 @@ __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int
         hi[i] = static_cast<uint32_t>(key[i] >> 32);  // 0 for no key: never >= a candidate
     }
     // A lower bound on the k-th largest score word.  With k <= kTopW * NW:
-    // each wave hands over its kTopW largest words (one key removed per
-    // round), and the k-th largest of those kTopW * NW words, each of a
+    // each wave hands over its `rounds` largest words (one key removed per
+    // round), and the k-th largest of those rounds * NW words, each of a
     // different key, is found by wave 0.  Otherwise: the largest per-wave
     // k-th largest word.  Either way at least k keys reach the bound, so the
     // exact selection below sees every key of the result.
     constexpr int kTopW = WgSelect<kThreads>::kTopW;
     uint32_t bound = 0;
     if (k <= kTopW * NW) {
+        // rounds: enough words for k candidates (one per key)
+        const int rounds = (k + NW - 1) / NW;
         uint32_t used = 0;  // this thread's keys already handed over
 #pragma unroll
         for (int rr = 0; rr < kTopW; ++rr) {
+            if (rr >= rounds) break;
             uint32_t my = 0;
             int mi = -1;
 #pragma unroll
@@ -388,23 +392,18 @@ __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int
                     my = hi[i];
                     mi = i;
                 }
-            uint32_t m = my;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1) {
-                const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), off));
-                m = o > m ? o : m;
-            }
+            const uint32_t m = wave_max_u32(my);
             const uint64_t holders = __ballot(mi >= 0 && my == m);
             if (lane == static_cast<int>(__builtin_ctzll(holders))) used |= 1u << mi;
             if (lane == 0) S->cand[rr * NW + wave] = m;
         }
         __syncthreads();
         if (wave == 0) {
-            const uint32_t v = lane < kTopW * NW ? S->cand[lane] : 0u;
+            const uint32_t v = lane < rounds * NW ? S->cand[lane] : 0u;
             uint32_t t = 0;
             for (int bit = 31; bit >= 0; --bit) {
                 const uint32_t c = t | (1u << bit);
-                if (__popcll(__ballot(lane < kTopW * NW && v >= c)) >= k) t = c;
+                if (__popcll(__ballot(lane < rounds * NW && v >= c)) >= k) t = c;
             }
             if (lane == 0) S->bound = t;
         }
@@ -439,12 +438,7 @@ __device__ __forceinline__ void wg_select_topk(uint64_t* keys, int n, int k, int
     static_assert(kMaxPer * NW <= 64, "one lane per (pass, wave)");
     if (wave == 0) {
         const int c0 = lane < per * NW ? S->wave_cnt[lane / NW][lane % NW] : 0;
-        int v = c0;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int o = __shfl_up(v, off);
-            if (lane >= off) v += o;
-        }
+        const int v = wave_incl_scan_add(c0);
         if (lane < per * NW) S->offset[lane] = v - c0;
         if (lane == 63) S->n_keep = v;
     }
@@ -498,6 +492,71 @@ __device__ __forceinline__ void wg_mean_rows(const T* rows_lds, int rows, float*
             for (int x = 0; x < NRS; x += 2 * step) v[x] = v[x] + v[x + step];
         out[tid] = v[0] * (1.0f / static_cast<float>(rows));
     }
+}
+
+// Launches with at most this many units route each unit with a whole
+// workgroup (route_wide_kernel, for up to kWideMaxCandidates middle chunks:
+// four keys per thread in its selection); larger ones pack four units per
+// workgroup (route_kernel, up to kPackedMaxCandidates: sixteen keys per
+// lane).  Longer candidate lists take route_long_kernel.
+constexpr int kWideMaxUnits = 128;
+constexpr int kWideMaxCandidates = WgSelect<1024>::kMaxPer * 1024;
+constexpr int kPackedMaxCandidates = 1024;
+
+// Steps 3 and 4 of the whole-workgroup routing, shared by route_wide_kernel
+// and route_spread_kernel: the top K_c of the n chunk keys in L.keys (ids
+// keep_first + m) to chunk_idx, then, with kGroups, the group refinement of
+// the chosen chunks against L.q.  Every thread of the workgroup calls.
+template <int D, bool kGroups>
+__device__ __forceinline__ void wide_select_refine(const WaveLds& L, unsigned char* big, int n,
+                                                   int unit, int bh,
+                                                   const float* __restrict__ group_sum,
+                                                   int table_chunks, int32_t* __restrict__ chunk_idx,
+                                                   int32_t* __restrict__ group_idx, int topk,
+                                                   int topk_groups, int gpc_shift) {
+    constexpr int kThreads = 1024;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int gpc = 1 << gpc_shift;
+    // 3. top-k chunks, ascending, -1 padded (the select's histograms reuse
+    // the table region)
+    auto* S = reinterpret_cast<WgSelect<kThreads>*>(big);
+    const int k = n < topk ? n : topk;
+    int32_t* out = chunk_idx + static_cast<int64_t>(unit) * topk;
+    if (k > 0) wg_select_topk<kThreads>(L.keys, n, k, L.sel, L.scr, S);  // ids keep_first + m
+    if (wave == 0) {
+        for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
+        if constexpr (kGroups)
+            for (int t = lane; t < k; t += 64) L.list[t] = L.sel[t];
+    }
+    if constexpr (!kGroups) return;
+
+    // 4. group refinement (the chunk-only variant keeps every candidate:
+    // ascending, written without scoring)
+    const int ng = k * gpc;
+    int32_t* gout = group_idx + static_cast<int64_t>(unit) * topk_groups;
+    if (ng <= topk_groups) {
+        if (wave == 0)
+            for (int t = lane; t < topk_groups; t += 64)
+                gout[t] = t < ng ? L.sel[t >> gpc_shift] * gpc + (t & (gpc - 1)) : -1;
+        return;
+    }
+    __syncthreads();  // the chunk list is visible to every wave
+    const float* gtab = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
+    for (int m0 = wave * 16; m0 < ng; m0 += 16 * (kThreads / 64)) {
+        const int rem = ng - m0;
+        batch_keys<D, 1>(
+            L.q, gtab,
+            [&](int kk) {
+                const int m = m0 + (kk < rem ? kk : rem - 1);
+                return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1));
+            },
+            rem, L.keys + m0);
+    }
+    __syncthreads();
+    wg_select_topk<kThreads>(L.keys, ng, topk_groups, L.sel, L.scr, S);  // groups of ascending chunks
+    if (wave == 0)
+        for (int t = lane; t < topk_groups; t += 64) gout[t] = L.sel[t];
 }
 
 // Routing of one unit by a whole workgroup of 16 wavefronts, for launches
@@ -631,45 +690,102 @@ __global__ __launch_bounds__(1024) void route_wide_kernel(
         __syncthreads();  // the block is scored before the next one is stored
     }
 
-    // 3. top-k chunks, ascending, -1 padded (the select's histograms reuse
-    // the table region)
-    auto* S = reinterpret_cast<WgSelect<kThreads>*>(big);
-    const int k = n < topk ? n : topk;
-    int32_t* out = chunk_idx + static_cast<int64_t>(unit) * topk;
-    if (k > 0) wg_select_topk<kThreads>(L.keys, n, k, L.sel, L.scr, S);  // ids keep_first + m
-    if (wave == 0) {
-        for (int t = lane; t < topk; t += 64) out[t] = t < k ? L.sel[t] : -1;
-        if constexpr (kGroups)
-            for (int t = lane; t < k; t += 64) L.list[t] = L.sel[t];
-    }
-    if constexpr (!kGroups) return;
+    wide_select_refine<D, kGroups>(L, big, n, unit, bh, group_sum, table_chunks, chunk_idx,
+                                   group_idx, topk, topk_groups, gpc_shift);
+}
 
-    // 4. group refinement (the chunk-only variant keeps every candidate:
-    // ascending, written without scoring)
-    const int ng = k * gpc;
-    int32_t* gout = group_idx + static_cast<int64_t>(unit) * topk_groups;
-    if (ng <= topk_groups) {
-        if (wave == 0)
-            for (int t = lane; t < topk_groups; t += 64)
-                gout[t] = t < ng ? L.sel[t >> gpc_shift] * gpc + (t & (gpc - 1)) : -1;
-        return;
+// Routing from a given q_bar for a launch of a few units (a decode block),
+// each unit's table scan spread over `parts` workgroups: one workgroup reads
+// the table at a single compute unit's bandwidth, which bounds
+// route_wide_kernel there.  Workgroup (unit, p) scores middle chunks
+// [p*kSpreadRows, (p+1)*kSpreadRows) with route_wide_kernel's arithmetic (the
+// same keys, bit for bit) and writes their keys to the plan's routing
+// workspace; the unit's last workgroup to finish -- the one whose increment
+// of the unit's device-scope counter completes it -- reads every key back,
+// resets the counter for the next call, and selects and refines exactly as
+// route_wide_kernel does.  One thread per workgroup makes the increment, an
+// acquire-release atomic at device scope: it publishes the workgroup's keys
+// (ordered before it by the workgroup barrier) and, in the last workgroup,
+// makes every other workgroup's keys visible.
+constexpr int kSpreadRows = 128;
+static_assert(kRouteSpreadCandidates <= kWideMaxCandidates, "the last workgroup's selection");
+
+template <int D, bool kGroups>
+__global__ __launch_bounds__(1024) void route_spread_kernel(
+    const float* __restrict__ qbar, int q_chunk0, int n_q_chunks,
+    const float* __restrict__ chunk_sum, const float* __restrict__ group_sum, int table_chunks,
+    int32_t* __restrict__ chunk_idx, int32_t* __restrict__ group_idx,
+    uint64_t* __restrict__ ws_keys, unsigned* __restrict__ ws_count, int n_kv, int keep_first,
+    int window, int topk, int topk_groups, int gpc_shift, int parts, int big_off) {
+    constexpr int kThreads = 1024;
+    constexpr int F4 = D / 4;                        // float4 per table row
+    constexpr int TS = D + 4;                        // padded LDS row stride (floats)
+    constexpr int PF = kSpreadRows * F4 / kThreads;  // float4 per thread
+    static_assert(PF >= 1 && PF * kThreads == kSpreadRows * F4, "block split");
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __shared__ int s_last;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int unit = blockIdx.x / parts, part = blockIdx.x % parts;
+    const int bh = unit / n_q_chunks, i = unit % n_q_chunks;
+    const int c = q_chunk0 + i;
+    WaveLds L = carve(smem_raw, D, kGroups ? topk : 0,
+                      kGroups && topk_groups > topk ? topk_groups : topk);
+    unsigned char* big = smem_raw + big_off;
+
+    int n = c - window - keep_first;
+    if (n < 0) n = 0;
+    const float* table = chunk_sum + (static_cast<int64_t>(bh) * table_chunks + keep_first) * D;
+    const buf_rsrc t_rsrc = make_rsrc(table, static_cast<uint32_t>(n) * D * sizeof(float));
+    const int r0 = part * kSpreadRows;
+    float4 qin = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (tid < D / 4)
+        qin = *reinterpret_cast<const float4*>(qbar + static_cast<int64_t>(unit) * D + tid * 4);
+    float4 pf[PF];
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+        const int x = tid + u * kThreads;
+        const uint32_t off = (static_cast<uint32_t>(r0 + x / F4) * D + (x % F4) * 4) * sizeof(float);
+        pf[u] = __builtin_bit_cast(float4, buf_load16(t_rsrc, off));  // zeros past row n
     }
-    __syncthreads();  // the chunk list is visible to every wave
-    const float* gtab = group_sum + static_cast<int64_t>(bh) * table_chunks * gpc * D;
-    for (int m0 = wave * 16; m0 < ng; m0 += 16 * (kThreads / 64)) {
-        const int rem = ng - m0;
-        batch_keys<D, 1>(
-            L.q, gtab,
-            [&](int kk) {
-                const int m = m0 + (kk < rem ? kk : rem - 1);
-                return L.list[m >> gpc_shift] * gpc + (m & (gpc - 1));
-            },
-            rem, L.keys + m0);
+    if (tid < D / 4) *reinterpret_cast<float4*>(L.q + tid * 4) = qin;
+    float* s_tab = reinterpret_cast<float*>(big);
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+        const int x = tid + u * kThreads;
+        *reinterpret_cast<float4*>(s_tab + (x / F4) * TS + (x % F4) * 4) = pf[u];
     }
     __syncthreads();
-    wg_select_topk<kThreads>(L.keys, ng, topk_groups, L.sel, L.scr, S);  // groups of ascending chunks
-    if (wave == 0)
-        for (int t = lane; t < topk_groups; t += 64) gout[t] = L.sel[t];
+    // scores of the block's rows: quad rl scores row rl (route_wide_kernel's
+    // per-row arithmetic), keys to the workspace
+    const int qd = lane & 3;
+    const int rl = wave * 16 + (lane >> 2);
+    uint64_t* keys = ws_keys + static_cast<int64_t>(unit) * kRouteSpreadCandidates;
+    if (rl < kSpreadRows) {
+        const float* row = s_tab + rl * TS + qd;
+        float a = 0.f;
+#pragma unroll
+        for (int f = 0; f < F4; ++f) a = fmaf(L.q[4 * f + qd], row[4 * f], a);
+        a = add_quad<0xb1>(a);  // (s0 + s1), (s2 + s3)
+        a = add_quad<0x4e>(a);  // (s0 + s1) + (s2 + s3)
+        const int m = r0 + rl;
+        if (qd == 0 && m < n) keys[m] = select_key(a, keep_first + m);
+    }
+    // The workgroup's keys happen before thread 0's increment (the barrier),
+    // which releases them at device scope; the increment that completes the
+    // count acquires every other workgroup's.
+    __syncthreads();
+    if (tid == 0)
+        s_last = __hip_atomic_fetch_add(ws_count + unit, 1u, __ATOMIC_ACQ_REL,
+                                        __HIP_MEMORY_SCOPE_AGENT) ==
+                 static_cast<unsigned>(parts - 1);
+    __syncthreads();
+    if (!s_last) return;
+    for (int m = tid; m < n; m += kThreads) L.keys[m] = keys[m];
+    if (tid == 0) ws_count[unit] = 0u;  // every workgroup of the unit has counted
+    __syncthreads();
+    wide_select_refine<D, kGroups>(L, big, n, unit, bh, group_sum, table_chunks, chunk_idx,
+                                   group_idx, topk, topk_groups, gpc_shift);
 }
 
 // Routing of units with more middle chunks than the other kernels hold as
@@ -924,14 +1040,6 @@ inline RouteGeom route_geom(const hga_plan& plan, int n_max, bool groups) {
     return g;
 }
 
-// Launches with at most this many units route each unit with a whole
-// workgroup (route_wide_kernel, for up to kWideMaxCandidates middle chunks:
-// four keys per thread in its selection); larger ones pack four units per
-// workgroup (route_kernel, up to kPackedMaxCandidates: sixteen keys per
-// lane).  Longer candidate lists take route_long_kernel.
-constexpr int kWideMaxUnits = 128;
-constexpr int kWideMaxCandidates = WgSelect<1024>::kMaxPer * 1024;
-constexpr int kPackedMaxCandidates = 1024;
 
 // LDS of route_wide_kernel: the WaveLds pieces (keys for the larger
 // candidate list), then one region (at the returned offset) for the staged
@@ -969,6 +1077,24 @@ hipError_t launch_route_t(const hga_plan& plan, const void* q_rot, int q_chunk0,
     const int units = p.batch * p.n_kv_heads * n_q_chunks;
     const int gpc = p.chunk / p.group;
     const int gpc_shift = gpc == 8 ? 3 : (gpc == 4 ? 2 : 1);
+    // a few units with long tables: the scan spread over several workgroups
+    // per unit (q_bar given; the keys in the plan's workspace)
+    if (kQbarIn && units <= kRouteSpreadUnits && n_max >= 2 * kSpreadRows &&
+        n_max <= kRouteSpreadCandidates && plan.route_keys) {
+        const WideGeom wg = route_wide_geom(plan, n_max, kGroups, true);
+        const size_t tab = sizeof(float) * kSpreadRows * (D + 4);
+        const size_t total = wg.big_off + (tab > wg.total - wg.big_off ? tab : wg.total - wg.big_off);
+        if (total + 64 <= static_cast<size_t>(plan.max_lds)) {  // + the static flag
+            const int parts = (n_max + kSpreadRows - 1) / kSpreadRows;
+            hipLaunchKernelGGL((route_spread_kernel<D, kGroups>), dim3(units * parts), dim3(1024),
+                               total, stream, qbar, q_chunk0, n_q_chunks, chunk_sum, group_sum,
+                               table_chunks, chunk_idx, group_idx, plan.route_keys,
+                               plan.route_count, p.n_kv_heads, p.keep_first, recent_window(p),
+                               p.topk_chunks, p.topk_groups, gpc_shift, parts,
+                               static_cast<int>(wg.big_off));
+            return hipGetLastError();
+        }
+    }
     if (units <= kWideMaxUnits && n_max <= kWideMaxCandidates) {
         const WideGeom wg = route_wide_geom(plan, n_max, kGroups, kQbarIn);
         if (wg.total <= static_cast<size_t>(plan.max_lds)) {

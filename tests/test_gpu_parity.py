@@ -985,7 +985,8 @@ def test_decode_block_parity_full(hga):
 def test_prefill_parity_full_size_sampled(hga, key):
     """Full sizes, launched exactly as the benchmark does; the oracle checks
     every summary and query mean, the routing of sampled query chunks, and
-    the attention of sampled units."""
+    the attention of every query chunk of one (batch, KV head) -- or, with
+    four KV heads, of 64 units, each head's first and last chunks included."""
     from paper_2606_30709_amd.pipeline import PrefillPipeline
     w = W.preset(key)
     _say(f"[full] {key}")
@@ -998,7 +999,20 @@ def test_prefill_parity_full_size_sampled(hga, key):
     rng = np.random.default_rng(5)
     nc = w.n_chunks
     chunk_ids = sorted(set([0, 1, 2, 3, nc - 1] + list(rng.choice(nc, 6, replace=False))))
-    units = [(int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads)), c) for c in chunk_ids]
+    if w.n_kv_heads * w.batch > 4:
+        # every query chunk of one (batch, KV head)
+        b0, j0 = int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads))
+        units = [(b0, j0, c) for c in range(nc)]
+    else:
+        # 64 units: the first and last chunks of every KV head, the rest drawn
+        units = sorted(set([(b, j, c) for b in range(w.batch) for j in range(w.n_kv_heads)
+                            for c in (0, 1, nc - 1)]))
+        while len(units) < 64:
+            u = (int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads)),
+                 int(rng.integers(nc)))
+            if u not in units:
+                units.append(u)
+    _say(f"  attention checked on {len(units)} units")
     _oracle_stage_checks(w, inp, pipe, units=units, chunk_ids=chunk_ids)
 
 

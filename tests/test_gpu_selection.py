@@ -14,9 +14,11 @@ The cases reach every selection path of the routing kernels: the packed
 kernel (more than 128 units; register lists up to 1024 candidates, the LDS
 form of its group stage beyond), the wide kernel (at most 128 units, up to
 4096 candidates: wave 0 alone below 257, the workgroup selection with one to
-four keys per thread, both forms of its bound), the long kernel (streaming
-selection beyond those lists, up to the 2^18-candidate limit), and the
-separate group call."""
+four keys per thread, both forms of its bound), the spread form (from q_bar,
+at most 16 units with 256..4096 candidates: the table scan over several
+workgroups per unit, the wide kernel's selection in the last one), the long
+kernel (streaming selection beyond those lists, up to the 2^18-candidate
+limit), and the separate group call."""
 
 from __future__ import annotations
 
@@ -50,8 +52,12 @@ def hga():
 # name: (head_dim, batch, n_kv, n_q_chunks, middle chunks of the last query
 #        chunk, K_c, K_g, group, values)
 CASES = {
-    # wide kernel (<= 128 units)
+    # wide kernel (<= 128 units; from q_bar with 256..4096 candidates only
+    # above 16 units, below that the spread form, whose last workgroup runs
+    # the same selection)
     "wide_wave0_d128": (128, 1, 4, 1, 200, 20, 32, 16, "ties"),
+    "wide_qbar_20_units": (128, 1, 4, 5, 1500, 30, 48, 16, "ties"),
+    "wide_qbar_20_units_d64": (64, 1, 4, 5, 3000, 64, 96, 16, "spread"),
     "wide_per1_d128": (128, 1, 4, 1, 700, 20, 32, 16, "ties"),
     "wide_per1_zero": (128, 1, 4, 1, 700, 20, 32, 16, "zero"),
     "wide_per2_k100_g100": (128, 1, 4, 1, 1500, 100, 100, 16, "ties"),
