@@ -242,14 +242,15 @@ hga_status hga_plan_create(const hga_params* params, hga_plan** plan) {
         pl->route_count = reinterpret_cast<unsigned*>(
             static_cast<unsigned char*>(ws) +
             sizeof(uint64_t) * hga::kRouteSpreadUnits * hga::kRouteSpreadCandidates);
-        e = hipMemset(pl->route_count, 0, sizeof(unsigned) * hga::kRouteSpreadUnits);
-        if (e == hipSuccess) e = hipDeviceSynchronize();
+        // a synchronous copy of zeros (no device-wide synchronisation)
+        const unsigned zeros[hga::kRouteSpreadUnits] = {};
+        e = hipMemcpy(pl->route_count, zeros, sizeof(zeros), hipMemcpyHostToDevice);
     }
     if (e != hipSuccess) {
         (void)hipFree(ws);
         (void)hipFree(buf);
         delete pl;
-        return hip_fail(e, "hipMalloc/hipMemset (routing workspace)");
+        return hip_fail(e, "hipMalloc/hipMemcpy (routing workspace)");
     }
     *plan = pl;
     return HGA_OK;

@@ -217,3 +217,34 @@ def test_candidate_limit_refused_before_launch(hga):
     assert e.value.status == -2
     torch.cuda.synchronize()
     assert bool((ci == -7).all()) and bool((gi == -7).all())
+
+
+def test_spread_route_reuses_the_plan_workspace(hga):
+    """hga_route_qbar's spread form (at most 16 units, 256..4096 candidates)
+    meets each unit's keys in the plan's workspace and leaves its counters at
+    zero: successive calls on one plan, with different unit and candidate
+    counts and inputs, each equal the oracle's lowest-index top-k exactly."""
+    d, B, H, K_c, K_g, group = 128, 1, 4, 20, 32, 16
+    F, L, W = 1, 0, 1
+    gpc = 64 // group
+    plan = hga.Plan(batch=B, n_q_heads=H, n_kv_heads=H, head_dim=d, group=group, keep_first=F,
+                    keep_last=L, force_prev=1, topk_chunks=K_c, topk_groups=K_g,
+                    dtype=hga.BF16, rope_base=1e6)
+    for call, (nq, n_last, mode) in enumerate([(1, 700, "ties"), (4, 3000, "spread"),
+                                                (2, 300, "ties"), (1, 4000, "zero"),
+                                                (3, 1500, "ramp")]):
+        c_last = n_last + W + F
+        c0 = c_last - nq + 1
+        T = c_last + 1
+        _say(f"[spread reuse] call {call}: units {B * H * nq} middle {n_last} {mode}")
+        rng = np.random.default_rng(1000 + call)
+        cs, gs, qb = _tables(rng, mode, B, H, T, gpc, nq, d)
+        ids = list(range(c0, c0 + nq))
+        want_c = O.route_chunks(qb, cs, ids, F, L, 1, K_c)
+        want_g = O.route_groups(qb, want_c, gs, gpc, K_g)
+        ci = torch.full((B, H, nq, K_c), -7, dtype=torch.int32, device="cuda")
+        gi = torch.full((B, H, nq, K_g), -7, dtype=torch.int32, device="cuda")
+        hga.hga_route_qbar(plan, _dev(qb), c0, _dev(cs), _dev(gs), ci, gi)
+        torch.cuda.synchronize()
+        assert np.array_equal(ci.cpu().numpy(), want_c), f"call {call}: chunk_idx"
+        assert np.array_equal(gi.cpu().numpy(), want_g), f"call {call}: group_idx"
