@@ -16,9 +16,10 @@
 //
 // Fused work item: (unit, part): a workgroup of NW wavefronts takes NW query
 // tiles of 32 rows of the unit's r*64 (as the forward packs them).  Per 64-key tile
-// the workgroup stages K and V row-major and K transposed in LDS; per 32-key
-// sub-tile each wavefront computes, for its own 32 queries,
-//   S^T = K.Q^T and dP^T = V.dO^T   (B operands: the wave's Q, dO rows in LDS),
+// the workgroup stages K and V row-major in LDS; per 32-key sub-tile each
+// wavefront computes, for its own 32 queries,
+//   S^T = K.Q^T and dP^T = V.dO^T   (B operands: the wave's Q, dO rows, read
+//                                    from LDS into registers once),
 //   P^T, dS^T elementwise           (each lane owns one query column),
 //   dQ += dS.K                      (A = the lane's own dS values, in registers),
 // and writes dS^T and P^T to its LDS scratch.  The key gradients of the
@@ -31,8 +32,8 @@
 //
 // A product's contraction index may be permuted as long as both operands use
 // the same permutation: dQ's A operand is the lane's own dS^T column (keys in
-// the order of the accumulator layout) and its B operand reads K^T in that
-// same key order.
+// the order of the accumulator layout) and its B operand takes K^T in that
+// same key order, by transpose reads of the row-major K tile (k_tr4).
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -52,11 +53,9 @@ constexpr int SCR = 40;   // row stride (bf16) of the 32 x 32 scratch tiles
 template <int D, int NW>
 struct BwdLayout {
     static constexpr int KS = D + 8;        // row stride (bf16) of K, V, Q, dO tiles
-    static constexpr int TS = KT + 4;       // row stride (bf16) of the K^T tile
     static constexpr int kK = 0;
     static constexpr int kV = kK + KT * KS * 2;
-    static constexpr int kKT = kV + KT * KS * 2;
-    static constexpr int kQ = kKT + D * TS * 2;                  // NW x (Q, dO) rows
+    static constexpr int kQ = kV + KT * KS * 2;                  // NW x (Q, dO) rows
     static constexpr int kScr = kQ + NW * 2 * 32 * KS * 2;       // NW x 2 buffers x (dS^T, P^T)
     static constexpr int kTok = kScr + NW * 4 * 32 * SCR * 2;    // 2 x (tile row -> token)
     static constexpr int kGid = kTok + 2 * KT * 4;
@@ -69,6 +68,23 @@ __device__ __forceinline__ bf16x8_t frag(const bf16_t* p) {
 
 __device__ __forceinline__ bf16x4_t frag4(const bf16_t* p) {
     return *reinterpret_cast<const bf16x4_t*>(p);
+}
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+
+// Four keys of one dimension from a row-major K tile in LDS (row stride ks
+// elements), by gfx950's transpose read ds_read_b64_tr_b16: within each
+// 16-lane group, lane i receives element i%4 of the 8-byte reads of lanes
+// 4j + i/4, j = 0..3.  Lane r of the group reads row k0 + r/4, dimensions
+// d0 + 16*(group & 1) + 4*(r%4) .. +3, so lane i of group g receives keys
+// k0 .. k0+3 of dimension d0 + 16*(g & 1) + i: for the 32 lanes of a half,
+// dimension d0 + (lane % 32).
+__device__ __forceinline__ bf16x4_t k_tr4(const bf16_t* sk, int ks, int k0, int d0) {
+    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+    const bf16_t* p = sk + (k0 + (r >> 2)) * ks + d0 + (g & 1) * 16 + (r & 3) * 4;
+    return __builtin_bit_cast(bf16x4_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                            (lds_i16x4_t*)(reinterpret_cast<uintptr_t>(p))));
 }
 
 // 16-bit element e of a 16-byte vector, and its value as a float when it is
@@ -131,7 +147,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     extern __shared__ __align__(16) unsigned char smem[];
     bf16_t* sK = reinterpret_cast<bf16_t*>(smem + Lay::kK);
     bf16_t* sV = reinterpret_cast<bf16_t*>(smem + Lay::kV);
-    bf16_t* sKT = reinterpret_cast<bf16_t*>(smem + Lay::kKT);
     bf16_t* sQall = reinterpret_cast<bf16_t*>(smem + Lay::kQ);
     bf16_t* scr_all = reinterpret_cast<bf16_t*>(smem + Lay::kScr);
     int* s_tok_all = reinterpret_cast<int*>(smem + Lay::kTok);
@@ -217,6 +232,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
         }
     }
 
+    // B fragments of S^T = K.Q^T and dP^T = V.dO^T (the lane's query row,
+    // dimensions kk*16 + half*8 .. +7), the same for every key tile: read
+    // from LDS once
+    bf16x8_t qf[NKS], gf[NKS];
+#pragma unroll
+    for (int kk = 0; kk < NKS; ++kk) {
+        qf[kk] = frag(sQ + col * Lay::KS + kk * 16 + half * 8);
+        gf[kk] = frag(sG + col * Lay::KS + kk * 16 + half * 8);
+    }
+
     f32x16_t dqacc[NDT];
 #pragma unroll
     for (int nb = 0; nb < NDT; ++nb)
@@ -237,7 +262,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
     auto scratch = [&](int w, int x) { return scr_all + (w * 2 + x) * 2 * 32 * SCR; };
 
     for (int tile = 0; tile < n_tiles; ++tile) {
-        // Stage K, V row-major and K transposed; the token of each tile row
+        // Stage K and V row-major (K^T operands are transpose reads of K); the token of each tile row
         // (-1: a routed row to skip, staged as zeros) goes to the token table
         // of the tile's parity.  Every wave has passed the previous tile's
         // last barrier, after which only the token table of that tile's
@@ -267,8 +292,6 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
                 const int cv = pv * VPT + u;
                 *reinterpret_cast<vec16*>(sK + row * Lay::KS + cv * 8) = kx[u];
                 *reinterpret_cast<vec16*>(sV + row * Lay::KS + cv * 8) = vx[u];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) sKT[(cv * 8 + e) * Lay::TS + row] = elem16(kx[u], e);
             }
         }
         lds_barrier();
@@ -286,10 +309,10 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 #pragma unroll
                 for (int kk = 0; kk < NKS; ++kk) {
                     const int off = kk * 16 + half * 8;
-                    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        frag(sK + krow * Lay::KS + off), frag(sQ + col * Lay::KS + off), sacc, 0, 0, 0);
-                    pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        frag(sV + krow * Lay::KS + off), frag(sG + col * Lay::KS + off), pacc, 0, 0, 0);
+                    sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag(sK + krow * Lay::KS + off),
+                                                                   qf[kk], sacc, 0, 0, 0);
+                    pacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(frag(sV + krow * Lay::KS + off),
+                                                                   gf[kk], pacc, 0, 0, 0);
                 }
                 // P^T, dS^T: lane (half, col) holds keys st*32 + kl, kl below;
                 // element e of fragment kap is e' = kap*8 + e of the accumulator
@@ -310,13 +333,15 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
                 }
                 // dQ += dS.K: k-slot half*8 + e of fragment kap is key
                 // st*32 + kap*16 + (e/4)*8 + half*4 + e%4, so the B operand
-                // is two 4-key runs of the K^T row of dimension nb*32 + col.
+                // is two 4-key runs of dimension nb*32 + col, transpose-read
+                // from the row-major K tile.
 #pragma unroll
                 for (int kap = 0; kap < 2; ++kap)
 #pragma unroll
                     for (int nb = 0; nb < NDT; ++nb) {
-                        const bf16_t* kp = sKT + (nb * 32 + col) * Lay::TS + st * 32 + kap * 16 + half * 4;
-                        const bf16x4_t lo = frag4(kp), hi = frag4(kp + 8);
+                        const int k0 = st * 32 + kap * 16 + half * 4;
+                        const bf16x4_t lo = k_tr4(sK, Lay::KS, k0, nb * 32);
+                        const bf16x4_t hi = k_tr4(sK, Lay::KS, k0 + 8, nb * 32);
                         const bf16x8_t bf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
                         dqacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dsf[kap], bf, dqacc[nb], 0, 0, 0);
                     }
