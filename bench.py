@@ -6,8 +6,9 @@ group summaries, chunk routing, group refinement, gather of the routed K/V,
 and exact attention (inputs already resident in HBM).  By default a step is
 three C-ABI calls: hga_build_summaries_qbar (summaries and the routing query
 means in one launch), hga_route_qbar (chunk and group selection) and
-hga_gather_attend (the attention stages each routed group's rows from the
-resident K/V and writes them to the routed buffers, the gather's output).
+hga_gather_attend (the attention gathers each routed group's rows from the
+resident K/V straight into its LDS tiles; with --routed-out it also writes
+them to the routed buffers, the standalone gather's output).
 --route fused / separate use hga_route or the two routing calls instead,
 --gather separate uses hga_gather_kv + hga_attend (identical results).  The
 default workload is the largest single-GPU prefill, the Qwen3-30B-A3B
@@ -58,9 +59,10 @@ GATHER_STAGES = {
 ATTENTION_STAGES = ("attend", "gather_attend")
 
 
-def algorithmic_bytes(w, n_valid_rows: int) -> dict:
+def algorithmic_bytes(w, n_valid_rows: int, routed_out: bool = False) -> dict:
     """Bytes each kernel must move at least once per step (compulsory
-    traffic).  n_valid_rows = routed token rows (all heads, all chunks)."""
+    traffic).  n_valid_rows = routed token rows (all heads, all chunks);
+    routed_out: the fused gather + attention also writes the routed rows."""
     B, Hq, Hkv, d, N, C, G = (w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.seq_len,
                               w.chunk, w.group)
     e = w.elem_bytes
@@ -82,10 +84,12 @@ def algorithmic_bytes(w, n_valid_rows: int) -> dict:
         "gather_kv": 4 * routed + B * Hkv * nc * w.topk_groups * 4,
         "attend": q_tok + 2 * kv_tok + 2 * routed + q_tok + B * Hq * N * 4,
         # the routed rows are rows of the resident K/V, which is read once
-        # as a whole (every chunk is some unit's current chunk); they are
-        # written once to the routed buffers and never read back
+        # as a whole (every chunk is some unit's current chunk); with
+        # routed_out they are written once to the routed buffers and never
+        # read back
         "gather_attend": (q_tok + 2 * kv_tok + q_tok + B * Hq * N * 4 +
-                          2 * routed + B * Hkv * nc * w.topk_groups * 4),
+                          (2 * routed if routed_out else 0) +
+                          B * Hkv * nc * w.topk_groups * 4),
     }
 
 
@@ -129,10 +133,11 @@ def attend_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str, workload_key: str):
+def measured_traffic(kernel: str, workload_key: str, routed_out: bool = False):
     """HBM bytes per launch of the attention kernel (`kernel`: attend or
-    gather_attend) from the committed counter summary, or None when there is
-    none or the kernel source changed since the counters were taken."""
+    gather_attend, the latter with or without the routed-buffer writes) from
+    the committed counter summary, or None when there is none, it covers the
+    other form, or the kernel source changed since the counters were taken."""
     try:
         vals = {}
         with open(traffic_file(kernel, workload_key)) as f:
@@ -144,20 +149,22 @@ def measured_traffic(kernel: str, workload_key: str):
             return None
         if vals.get("workload") != workload_key:
             return None
+        if kernel == "gather_attend" and vals.get("routed_out") != str(int(routed_out)):
+            return None
         return int(float(vals["traffic_bytes_per_launch"]))
     except (OSError, KeyError, ValueError):
         return None
 
 
-def probe_traffic(w, inp, gather_mode: str):
+def probe_traffic(w, inp, gather_mode: str, routed_out: bool):
     """For counter collection: the pipeline once, the attention call 5 times
-    (hga_gather_attend, or hga_attend with gather_mode "separate"), then 5
-    plain device copies of COPY_BYTES (the calibration for FETCH_SIZE and
-    WRITE_SIZE)."""
+    (hga_gather_attend, with or without the routed-buffer writes, or
+    hga_attend with gather_mode "separate"), then 5 plain device copies of
+    COPY_BYTES (the calibration for FETCH_SIZE and WRITE_SIZE)."""
     import torch
 
     from paper_2606_30709_amd.pipeline import PrefillPipeline
-    pipe = PrefillPipeline(w, inp, gather_mode=gather_mode)
+    pipe = PrefillPipeline(w, inp, gather_mode=gather_mode, routed_out=routed_out)
     pipe.step()
     for _ in range(5):
         if gather_mode == "fused":
@@ -171,6 +178,7 @@ def probe_traffic(w, inp, gather_mode: str):
     torch.cuda.synchronize()
     print(json.dumps({"probe": "traffic", "workload": w.key, "copy_bytes": COPY_BYTES,
                       "kernel": "gather_attend" if gather_mode == "fused" else "attend",
+                      "routed_out": int(pipe.routed_out),
                       "kernel_source_sha256": attend_source_hash()}), flush=True)
 
 
@@ -553,9 +561,13 @@ def main():
                          "hga_build_summaries + hga_route; separate: hga_build_summaries + "
                          "hga_route_chunks + hga_route_groups (identical results)")
     ap.add_argument("--gather", choices=("fused", "separate"), default="fused",
-                    help="fused: hga_gather_attend (the attention stages the routed rows and "
-                         "writes the routed buffers); separate: hga_gather_kv + hga_attend "
-                         "(identical results)")
+                    help="fused: hga_gather_attend (the attention stages the routed rows from "
+                         "the resident K/V); separate: hga_gather_kv + hga_attend (identical "
+                         "results)")
+    ap.add_argument("--routed-out", action="store_true",
+                    help="fused gather: also write the gathered rows to the routed buffers "
+                         "(k_routed, v_routed; bit-identical outputs); by default they stay in "
+                         "the attention's LDS tiles")
     ap.add_argument("--route-from-q", action="store_true",
                     help="decode: hga_route forms q_bar from the query rows and the block's "
                          "summaries follow it (default: hga_build_summaries_qbar first, then "
@@ -608,9 +620,10 @@ def main():
         backward_bench(w, inp, args)
         return
     if args.probe_traffic:
-        probe_traffic(w, inp, args.gather)
+        probe_traffic(w, inp, args.gather, args.routed_out)
         return
-    pipe = PrefillPipeline(w, inp, route_mode=args.route, gather_mode=args.gather)
+    pipe = PrefillPipeline(w, inp, route_mode=args.route, gather_mode=args.gather,
+                           routed_out=args.routed_out)
     stream = torch.cuda.current_stream()
     sh = stream.cuda_stream
     p = pipe.plan
@@ -621,9 +634,12 @@ def main():
                                        pipe.v_routed, stream=sh)
     if args.gather == "fused":
         # the dominant kernel's own dispatch records e0/e1 when given
+        # with --routed-out the gathered rows are also written to the routed
+        # buffers; by default they stay in the attention's LDS tiles
+        kr, vr = (pipe.k_routed, pipe.v_routed) if args.routed_out else (None, None)
         attend_timed = lambda e0, e1: hga.hga_gather_attend(
-            p, pipe.q, 0, pipe.k, pipe.v, pipe.group_idx, pipe.k_routed, pipe.v_routed, pipe.out,
-            pipe.lse, start_event=e0, stop_event=e1, stream=sh)
+            p, pipe.q, 0, pipe.k, pipe.v, pipe.group_idx, kr, vr, pipe.out, pipe.lse,
+            start_event=e0, stop_event=e1, stream=sh)
         tail = (lambda: attend_timed(None, None),)
     else:
         attend_timed = lambda e0, e1: hga.hga_attend_timed(
@@ -713,7 +729,7 @@ def main():
     tokens = w.batch * w.seq_len
     gi = pipe.group_idx.cpu().numpy()
     n_valid_rows = int((gi >= 0).sum()) * w.group
-    abytes = algorithmic_bytes(w, n_valid_rows)
+    abytes = algorithmic_bytes(w, n_valid_rows, pipe.routed_out)
     flops = attention_flops(w, gi)
 
     # achievable HBM bandwidth on this device, measured by a plain copy
@@ -753,8 +769,8 @@ def main():
                     "copy_measured_GB_s": round(copy_gbs, 1),
                     "frac_of_copy": round(achieved / copy_gbs, 4)}
     roofline.update({
-                "traffic": (measured_traffic(dominant, w.key) if dominant in ATTENTION_STAGES
-                            else None),
+                "traffic": (measured_traffic(dominant, w.key, pipe.routed_out)
+                            if dominant in ATTENTION_STAGES else None),
                 "alg_bytes_per_launch": abytes[dominant],
                 "mean_launch_us": round(stage_ms[dominant] * 1e3, 2),
                 "timed_launches": len(timed_steps) if dominant == att_name else KB})
@@ -785,6 +801,8 @@ def main():
         "stages": stages,
         "route_calls": args.route,
         "gather_calls": args.gather,
+        "routed_kv": ("written to the routed buffers" if pipe.routed_out else
+                      "gathered into the attention's LDS tiles only (not written)"),
         "roofline": roofline,
         "device": torch.cuda.get_device_properties(0).gcnArchName,
     }

@@ -441,7 +441,9 @@ hga_status hga_attend_backward(const hga_plan* plan, const void* q_rot, int32_t 
  *   src_on_host   0: device memory; 1: pinned, mapped host memory
  *                 (hipHostMalloc), read through its device mapping
  * Other arguments as hga_gather_kv and hga_attend_split; k_routed/v_routed
- * must not overlap any input. */
+ * must not overlap any input.  k_routed = v_routed = NULL: the routed rows
+ * are gathered into the kernel's tiles only and not written out (out and
+ * lse unchanged); exactly one of them NULL is HGA_EINVAL. */
 hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                                    int32_t n_q_chunks, const void* k_res, const void* v_res,
                                    int64_t res_tokens, const int32_t* res_slot,
@@ -464,7 +466,14 @@ hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int3
  * the attention kernel's dispatch as in hga_attend_timed (for the fp32 plan
  * dtype the gather runs as its own kernel first, outside the events).
  * Arguments, layouts, requirements and errors are those of the two calls;
- * k_routed/v_routed must not overlap any input. */
+ * k_routed/v_routed must not overlap any input.
+ * k_routed = v_routed = NULL: the gather's rows go to the attention's
+ * on-chip tiles only and are not written to memory (for a caller that needs
+ * the output, not the gathered copies: no routed-buffer traffic, 2 bytes x
+ * head_dim x 2 per routed row and unit); out and lse are bit-identical to
+ * the call with buffers (for the fp32 plan dtype the attention kernel then
+ * reads the routed rows from k_res/v_res itself, and no gather kernel runs).
+ * Exactly one of them NULL is HGA_EINVAL. */
 hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk0,
                              int32_t n_q_chunks, const void* k_res, const void* v_res,
                              int64_t res_tokens, const int32_t* group_idx, void* k_routed,

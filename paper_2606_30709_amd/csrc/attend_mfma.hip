@@ -461,10 +461,11 @@ __device__ __forceinline__ void finish_rows(f32x16_t (&oacc)[D / 32], float m_ru
 // with the first tiles, then the key tiles stream through the ring.
 // kGather: the routed rows are copied straight from the resident K/V (rows
 // g*G .. g*G+G-1 of each routed group g, zeros for a padded or future group,
-// as the gather step defines them), and the unit's first workgroup writes
-// every routed tile it staged to k_routed / v_routed (with two or more
-// workgroups per unit the first writes K and the second V), so the call also
-// produces the gather step's output.  Otherwise the routed rows are
+// as the gather step defines them), and when k_routed / v_routed are given
+// the unit's first workgroup writes every routed tile it staged to them
+// (with two or more workgroups per unit the first writes K and the second
+// V), so the call also produces the gather step's output; when they are
+// null the gathered rows live in LDS only.  Otherwise the routed rows are
 // read from k_routed / v_routed.
 // With kGather the routed rows come from k_src / v_src (src_tokens rows per
 // head: the resident K/V itself for the prefill layout, or the history in
@@ -674,8 +675,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
     auto store16_nt = [](unsigned char* p, const vec16& x) {
         __builtin_nontemporal_store(__builtin_bit_cast(u32x4, x), reinterpret_cast<u32x4*>(p));
     };
-    const bool write_k = kGather && part == 0;
-    const bool write_v = kGather && part == (wg_div.d == 1 ? 0 : 1);
+    // (no routed buffers given: the routed rows are gathered into LDS only)
+    const bool write_k = kGather && k_routed != nullptr && part == 0;
+    const bool write_v = kGather && v_routed != nullptr && part == (wg_div.d == 1 ? 0 : 1);
     auto write_routed = [&](int tile, int stage) {
         const int rt0 = (tile - 1 - n_vis) * KT;
         const unsigned char* sk = smem + stage * kStageBytes;
@@ -1003,7 +1005,8 @@ hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chu
                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                               const void* v_routed, const int32_t* group_idx, void* out,
                               float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
-                              hipStream_t stream);
+                              hipStream_t stream, const void* k_src = nullptr,
+                              const void* v_src = nullptr, int64_t src_tokens = 0);
 
 int64_t attend_split_bytes_per_split(const hga_plan& plan, int n_q_chunks) {
     const hga_params& p = plan.p;
@@ -1069,12 +1072,16 @@ hipError_t launch_gather_attend_split(const hga_plan& plan, const void* q_rot, i
                                       int64_t workspace_bytes, hipStream_t stream) {
     const hga_params& p = plan.p;
     if (p.dtype == HGA_F32) {
-        hipError_t e = launch_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_src, v_src,
-                                        src_tokens, k_routed, v_routed, stream);
-        if (e != hipSuccess) return e;
+        // the gather kernel, then the attention reading its output; without
+        // routed buffers the attention reads the routed rows from k_src/v_src
+        if (k_routed) {
+            const hipError_t e = launch_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_src,
+                                                  v_src, src_tokens, k_routed, v_routed, stream);
+            if (e != hipSuccess) return e;
+        }
         return launch_attend_valu(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
                                   res_slot, k_routed, v_routed, group_idx, out, lse, nullptr,
-                                  nullptr, stream);
+                                  nullptr, stream, k_src, v_src, src_tokens);
     }
     const int n_split = choose_splits(plan, q_chunk0, n_q_chunks, workspace_bytes);
     if (n_split <= 1)
@@ -1110,13 +1117,17 @@ hipError_t launch_gather_attend(const hga_plan& plan, const void* q_rot, int q_c
                                 void* v_routed, void* out, float* lse, hipEvent_t ev_start,
                                 hipEvent_t ev_stop, hipStream_t stream) {
     if (plan.p.dtype == HGA_F32) {
-        // fp32: the gather kernel, then the attention kernel reading its output
-        hipError_t e = launch_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_res, v_res,
-                                        res_tokens, k_routed, v_routed, stream);
-        if (e != hipSuccess) return e;
+        // fp32: the gather kernel, then the attention kernel reading its
+        // output; without routed buffers the attention kernel reads each
+        // routed row from the resident K/V itself
+        if (k_routed) {
+            const hipError_t e = launch_gather_kv(plan, group_idx, q_chunk0, n_q_chunks, k_res,
+                                                  v_res, res_tokens, k_routed, v_routed, stream);
+            if (e != hipSuccess) return e;
+        }
         return launch_attend_valu(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
                                   nullptr, k_routed, v_routed, group_idx, out, lse, ev_start,
-                                  ev_stop, stream);
+                                  ev_stop, stream, k_res, v_res, res_tokens);
     }
     return launch_mfma_any<true>(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens,
                                  nullptr, k_routed, v_routed, group_idx, out, lse, ev_start,

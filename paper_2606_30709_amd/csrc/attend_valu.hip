@@ -28,7 +28,8 @@ __global__ __launch_bounds__(64 * kSplit) void attend_valu_kernel(
     const float* __restrict__ v_res, int64_t res_tokens, const int32_t* __restrict__ res_slot,
     const float* __restrict__ k_routed, const float* __restrict__ v_routed,
     const int32_t* __restrict__ group_idx, float* __restrict__ out, float* __restrict__ lse,
-    int n_q_heads, int n_kv, int chunk, int group, int keep_first, int window, int topk_groups) {
+    int n_q_heads, int n_kv, int chunk, int group, int keep_first, int window, int topk_groups,
+    const float* __restrict__ k_src, const float* __restrict__ v_src, int64_t src_tokens) {
     extern __shared__ __align__(16) float smem_f[];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     float* s_k = smem_f + wave * (2 * kTile * D + kTile);  // [kTile][D]
@@ -81,9 +82,11 @@ __global__ __launch_bounds__(64 * kSplit) void attend_valu_kernel(
         } else if (tile < n_vis_tiles + n_rt_tiles) {
             kind = kTileRouted;
             row0 = (tile - n_vis_tiles) * kTile;
-            const int64_t off = (unit * routed_rows + row0) * D;
-            ksrc = k_routed + off;
-            vsrc = v_routed + off;
+            if (k_routed) {
+                const int64_t off = (unit * routed_rows + row0) * D;
+                ksrc = k_routed + off;
+                vsrc = v_routed + off;
+            }
         } else {
             kind = kTileCurrent;
             row0 = (tile - n_vis_tiles - n_rt_tiles) * kTile;
@@ -105,8 +108,18 @@ __global__ __launch_bounds__(64 * kSplit) void attend_valu_kernel(
                     ok = g >= 0 && g < c * gpc;
                 }
             }
-            s_k[rr * D + e] = ok ? ksrc[rr * D + e] : 0.f;
-            s_v[rr * D + e] = ok ? vsrc[rr * D + e] : 0.f;
+            const float* kp = ksrc ? ksrc + rr * D + e : nullptr;
+            const float* vp = vsrc ? vsrc + rr * D + e : nullptr;
+            if (!ksrc && ok) {
+                // no routed buffers: routed row R of group gi[R / G] is row
+                // g*G + R % G of the routed-row source (the gather's rule)
+                const int row = row0 + rr;
+                const int64_t tok = static_cast<int64_t>(gi[row / group]) * group + row % group;
+                kp = k_src + (static_cast<int64_t>(bh) * src_tokens + tok) * D + e;
+                vp = v_src + (static_cast<int64_t>(bh) * src_tokens + tok) * D + e;
+            }
+            s_k[rr * D + e] = ok ? *kp : 0.f;
+            s_v[rr * D + e] = ok ? *vp : 0.f;
             if (e == 0) s_valid[rr] = ok;
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -181,7 +194,8 @@ hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chu
                               int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                               const void* v_routed, const int32_t* group_idx, void* out,
                               float* lse, hipEvent_t ev_start, hipEvent_t ev_stop,
-                              hipStream_t stream) {
+                              hipStream_t stream, const void* k_src, const void* v_src,
+                              int64_t src_tokens) {
     const hga_params& p = plan.p;
     const int r = p.n_q_heads / p.n_kv_heads;
     dim3 grid(n_q_chunks * r, p.batch * p.n_kv_heads);
@@ -205,7 +219,9 @@ hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chu
                               static_cast<const float*>(k_routed),                              \
                               static_cast<const float*>(v_routed), group_idx,                   \
                               static_cast<float*>(out), lse, p.n_q_heads, p.n_kv_heads,         \
-                              p.chunk, p.group, p.keep_first, recent_window(p), p.topk_groups); \
+                              p.chunk, p.group, p.keep_first, recent_window(p), p.topk_groups,  \
+                              static_cast<const float*>(k_src), static_cast<const float*>(v_src), \
+                              src_tokens);                                                      \
     } while (0)
     if (p.head_dim == 64)
         HGA_VALU(64);

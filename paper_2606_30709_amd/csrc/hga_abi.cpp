@@ -543,7 +543,7 @@ hga_status check_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk
                         int32_t n_q_chunks, const void* k_res, const void* v_res,
                         int64_t res_tokens, const int32_t* res_slot, const void* k_routed,
                         const void* v_routed, const int32_t* group_idx, const void* out,
-                        const float* lse) {
+                        const float* lse, bool routed_optional = false) {
     const hga_params& p = plan->p;
     if (!res_slot && (static_cast<int64_t>(q_chunk0) + n_q_chunks) * p.chunk > res_tokens)
         return fail(HGA_EINVAL, "without res_slot the resident K/V must cover chunks up to %d "
@@ -567,8 +567,14 @@ hga_status check_attend(const hga_plan* plan, const void* q_rot, int32_t q_chunk
     HGA_TRY(check_tensor(q_rot, "q_rot"));
     HGA_TRY(check_tensor(k_res, "k_res"));
     HGA_TRY(check_tensor(v_res, "v_res"));
-    HGA_TRY(check_tensor(k_routed, "k_routed"));
-    HGA_TRY(check_tensor(v_routed, "v_routed"));
+    if (routed_optional && !k_routed && !v_routed) {
+        // the gather forms without routed buffers: the rows stay on chip
+    } else {
+        if (routed_optional && (!k_routed || !v_routed))
+            return fail(HGA_EINVAL, "k_routed and v_routed must both be given or both be NULL");
+        HGA_TRY(check_tensor(k_routed, "k_routed"));
+        HGA_TRY(check_tensor(v_routed, "v_routed"));
+    }
     HGA_TRY(check_index(group_idx, "group_idx"));
     HGA_TRY(check_tensor(out, "out"));
     if (lse && !aligned(lse, 4)) return fail(HGA_EALIGN, "lse is not 4-byte aligned");
@@ -669,7 +675,7 @@ hga_status hga_gather_attend_split(const hga_plan* plan, const void* q_rot, int3
     if (src_on_host != 0 && src_on_host != 1) return fail(HGA_EINVAL, "src_on_host must be 0 or 1");
     if (n_q_chunks == 0) return HGA_OK;
     HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, res_slot,
-                         k_routed, v_routed, group_idx, out, lse));
+                         k_routed, v_routed, group_idx, out, lse, true));
     const hga_params& p = plan->p;
     const int64_t need = static_cast<int64_t>(q_chunk0 + n_q_chunks - 1) * p.chunk;
     if (src_tokens < need)
@@ -732,7 +738,7 @@ hga_status hga_gather_attend(const hga_plan* plan, const void* q_rot, int32_t q_
         return fail(HGA_EINVAL, "q_chunk0, n_q_chunks and res_tokens must be >= 0");
     if (n_q_chunks == 0) return HGA_OK;
     HGA_TRY(check_attend(plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res, res_tokens, nullptr,
-                         k_routed, v_routed, group_idx, out, lse));
+                         k_routed, v_routed, group_idx, out, lse, true));
     clear_stale_error();
     return launched(hga::launch_gather_attend(*plan, q_rot, q_chunk0, n_q_chunks, k_res, v_res,
                                               res_tokens, group_idx, k_routed, v_routed, out, lse,

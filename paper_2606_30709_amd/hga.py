@@ -372,7 +372,8 @@ def hga_gather_attend_split(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, k_sr
                             group_idx, k_routed, v_routed, out, workspace, lse=None,
                             res_slot=None, src_on_host=False, stream=None):
     """hga_gather_kv (from k_src/v_src [B, Hkv, src_tokens, d], device or
-    pinned host) + hga_attend_split in one pass; k_routed/v_routed written."""
+    pinned host) + hga_attend_split in one pass; k_routed/v_routed written
+    (or both None: gathered on chip only)."""
     nq = q_rot.shape[2] // plan.params.chunk
     nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(library().hga_gather_attend_split(
@@ -397,8 +398,9 @@ def hga_gather_attend(plan: Plan, q_rot, q_chunk0: int, k_res, v_res, group_idx,
                       v_routed, out, lse=None, start_event=None, stop_event=None, stream=None):
     """hga_gather_kv + hga_attend in one pass (prefill layout: k_res/v_res
     [B, Hkv, res_tokens, d] indexed by token); k_routed/v_routed
-    [B, Hkv, n_q_chunks, K_g*G, d] are written.  start/stop_event: recorded
-    torch.cuda.Event objects or None."""
+    [B, Hkv, n_q_chunks, K_g*G, d] are written, or both None: the routed rows
+    are gathered on chip only.  start/stop_event: recorded torch.cuda.Event
+    objects or None."""
     nq = q_rot.shape[2] // plan.params.chunk
     _check(library().hga_gather_attend(
         plan.handle, _ptr(q_rot), q_chunk0, nq, _ptr(k_res), _ptr(v_res), k_res.shape[2],

@@ -47,13 +47,17 @@ def to_device(arr: np.ndarray, dtype: str, device="cuda", pin=False) -> torch.Te
 
 class PrefillPipeline:
     def __init__(self, w, inputs: dict, device="cuda", plan: hga.Plan | None = None,
-                 route_mode: str = "qbar", gather_mode: str = "fused"):
+                 route_mode: str = "qbar", gather_mode: str = "fused", routed_out: bool = True):
+        """routed_out: with the fused gather, also write the gathered rows to
+        k_routed/v_routed (False: they stay on chip; the separate gather
+        always writes them)."""
         assert not w.decode_block
         assert route_mode in ("fused", "separate", "qbar")
         assert gather_mode in ("fused", "separate")
         self.w = w
         self.route_mode = route_mode
         self.gather_mode = gather_mode
+        self.routed_out = routed_out or gather_mode == "separate"
         self.plan = plan or hga.Plan.for_workload(w)
         B, Hkv, d, C, G = w.batch, w.n_kv_heads, w.head_dim, w.chunk, w.group
         nc = w.n_chunks
@@ -104,9 +108,10 @@ class PrefillPipeline:
                        self.group_idx, self.out, self.lse, stream=stream)
 
     def gather_attend(self, stream=None, start_event=None, stop_event=None):
-        hga.hga_gather_attend(self.plan, self.q, 0, self.k, self.v, self.group_idx,
-                              self.k_routed, self.v_routed, self.out, self.lse,
-                              start_event=start_event, stop_event=stop_event, stream=stream)
+        kr, vr = (self.k_routed, self.v_routed) if self.routed_out else (None, None)
+        hga.hga_gather_attend(self.plan, self.q, 0, self.k, self.v, self.group_idx, kr, vr,
+                              self.out, self.lse, start_event=start_event,
+                              stop_event=stop_event, stream=stream)
 
     def backward(self, dout, stream=None):
         """Gradients of the attention of the last ``step`` for output gradient

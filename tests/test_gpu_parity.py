@@ -149,7 +149,11 @@ def _oracle_stage_checks(w, inp, pipe, units=None, chunk_ids=None):
                                 f"group_idx[{b},{j},{c}]")
     _say(f"  {w.key}: chunk selections {rep_c}, group selections {rep_g}")
 
-    # gather: bit-exact on the GPU's group selection
+    # gather: bit-exact on the GPU's group selection (when the step kept the
+    # routed rows on chip, the standalone gather writes them for the check)
+    if not pipe.routed_out:
+        pipe.gather()
+        torch.cuda.synchronize()
     kb = inp["k"]
     vb = inp["v"]
     sel = [(b, j, c) for b in range(w.batch) for j in range(w.n_kv_heads) for c in ids]
@@ -292,18 +296,22 @@ def _bits(t):
 
 def _gather_attend_both_ways(hga, plan, w, q, q_chunk0, k, v, gi):
     """hga_gather_kv + hga_attend and hga_gather_attend on the same inputs,
-    every output pre-filled with NaN so that an unwritten element shows."""
+    every output pre-filled with NaN so that an unwritten element shows; and
+    hga_gather_attend without routed buffers (rows gathered on chip only),
+    whose out and lse must be the same bits."""
     B, Hkv, d, G = w.batch, w.n_kv_heads, w.head_dim, w.group
     nq = gi.shape[2]
     outs = []
-    for fused in (False, True):
+    for mode in ("separate", "fused", "fused_no_routed"):
         kr = torch.full((B, Hkv, nq, w.topk_groups * G, d), float("nan"), dtype=k.dtype,
                         device="cuda")
         vr = torch.full_like(kr, float("nan"))
         out = torch.full_like(q, float("nan"))
         lse = torch.full(q.shape[:3], float("nan"), device="cuda")
-        if fused:
+        if mode == "fused":
             hga.hga_gather_attend(plan, q, q_chunk0, k, v, gi, kr, vr, out, lse)
+        elif mode == "fused_no_routed":
+            hga.hga_gather_attend(plan, q, q_chunk0, k, v, gi, None, None, out, lse)
         else:
             hga.hga_gather_kv(plan, gi, q_chunk0, k, v, kr, vr)
             hga.hga_attend(plan, q, q_chunk0, k, v, kr, vr, gi, out, lse)
@@ -312,6 +320,10 @@ def _gather_attend_both_ways(hga, plan, w, q, q_chunk0, k, v, gi):
     for a, b, name in zip(outs[0], outs[1], ("k_routed", "v_routed", "out", "lse")):
         assert torch.equal(_bits(a), _bits(b)), name
     assert not torch.isnan(outs[1][2]).any()
+    for a, b, name in zip(outs[1][2:], outs[2][2:], ("out", "lse")):
+        assert torch.equal(_bits(a), _bits(b)), f"{name} without routed buffers"
+    # nothing was written to the routed buffers of the third call
+    assert torch.isnan(outs[2][0]).all() and torch.isnan(outs[2][1]).all()
 
 
 @pytest.mark.parametrize("key", list(FUSED_CASES))
@@ -751,6 +763,16 @@ def test_decode_fused_gather_equals_separate(hga):
                 a, b = getattr(fused, name), getattr(sep, name)
                 assert torch.equal(_bits(a), _bits(b)), name
             assert not torch.isnan(fused.out).any()
+            # without routed buffers: the same output and LSE bits
+            out2 = torch.full_like(fused.out, float("nan"))
+            lse2 = torch.full_like(fused.lse, float("nan"))
+            hga.hga_gather_attend_split(fused.plan, fused.q, fused.c, fused.k_res, fused.v_res,
+                                        fused.k_hist, fused.v_hist, fused.group_idx, None, None,
+                                        out2, fused.attend_ws, lse2, res_slot=fused.res_slot,
+                                        src_on_host=True)
+            torch.cuda.synchronize()
+            assert torch.equal(_bits(out2), _bits(fused.out))
+            assert torch.equal(lse2, fused.lse)
 
 
 class _LruModel:
@@ -991,7 +1013,7 @@ def test_prefill_parity_full_size_sampled(hga, key):
     w = W.preset(key)
     _say(f"[full] {key}")
     inp = W.generate(w)
-    pipe = PrefillPipeline(w, inp)
+    pipe = PrefillPipeline(w, inp, routed_out=False)  # the benchmark's form
     pipe.out.fill_(float("nan"))
     pipe.step()
     torch.cuda.synchronize()
@@ -1062,6 +1084,18 @@ def test_argument_errors_launch_nothing(hga):
                                      1024, 1, gi.data_ptr(), kr.data_ptr(), kr.data_ptr(),
                                      q.data_ptr(), None, None, 0, None)
     assert st == -1 and "pinned" in hga.hga_last_error()
+    # the routed buffers of the fused gathers: both or neither
+    kk = torch.zeros(1, 1, 1024, 64, device=dev)
+    for kr_p, vr_p in ((kr.data_ptr(), None), (None, kr.data_ptr())):
+        st = lib.hga_gather_attend(plan.handle, q.data_ptr(), 0, 16, kk.data_ptr(),
+                                   kk.data_ptr(), 1024, gi.data_ptr(), kr_p, vr_p, q.data_ptr(),
+                                   None, None, None, None)
+        assert st == -1 and "both" in hga.hga_last_error()
+        st = lib.hga_gather_attend_split(plan.handle, q.data_ptr(), 0, 16, kk.data_ptr(),
+                                         kk.data_ptr(), 1024, None, kk.data_ptr(), kk.data_ptr(),
+                                         1024, 0, gi.data_ptr(), kr_p, vr_p, q.data_ptr(), None,
+                                         None, 0, None)
+        assert st == -1 and "both" in hga.hga_last_error()
     # empty ranges are no-ops
     hga.hga_build_summaries(plan, k, 3, 3, cs, gs)
     torch.cuda.synchronize()
