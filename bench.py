@@ -242,8 +242,10 @@ def cpu_baseline(w, inp, max_seconds: float, block_chunks: int = 64) -> dict:
         threads = max(threads, int(pool.get("num_threads", 1)))
     return {"value": tokens / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{done} pieces of {block_chunks} query chunks of one (batch, KV head) "
-                      f"({chunks} of the layer's {w.n_chunks * len(units)} unit-chunks, blocks "
-                      f"spread over the sequence), five stages, float64 NumPy, {dt:.1f} s",
+                      f"({chunks} unit-chunks, {chunks / (w.n_chunks * len(units)):.2f} of the "
+                      f"layer's {w.n_chunks * len(units)}: the {len(pieces)} pieces in turn, "
+                      f"blocks spread over the sequence), five stages, float64 NumPy, "
+                      f"{dt:.1f} s",
             "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
