@@ -403,11 +403,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 template <int D>
 struct DqLayout {
     static constexpr int KS = D + 8;
-    static constexpr int TS = KT + 4;
     static constexpr int kK = 0;
     static constexpr int kV = kK + KT * KS * 2;
-    static constexpr int kKT = kV + KT * KS * 2;
-    static constexpr int kTok = kKT + D * TS * 2;
+    static constexpr int kTok = kV + KT * KS * 2;
     static constexpr int kGid = kTok + KT * 4;
     static constexpr int kBytes = kGid + kMaxTopK * 4;
 };
@@ -429,7 +427,6 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
     extern __shared__ __align__(16) unsigned char smem[];
     bf16_t* sK = reinterpret_cast<bf16_t*>(smem + Lay::kK);
     bf16_t* sV = reinterpret_cast<bf16_t*>(smem + Lay::kV);
-    bf16_t* sKT = reinterpret_cast<bf16_t*>(smem + Lay::kKT);
     int* s_tok = reinterpret_cast<int*>(smem + Lay::kTok);
     int* s_gid = reinterpret_cast<int*>(smem + Lay::kGid);
 
@@ -523,8 +520,6 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
             const int cv = pv * VPT + u;
             *reinterpret_cast<vec16*>(sK + srow * Lay::KS + cv * 8) = kx[u];
             *reinterpret_cast<vec16*>(sV + srow * Lay::KS + cv * 8) = vx[u];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) sKT[(cv * 8 + e) * Lay::TS + srow] = elem16(kx[u], e);
         }
         lds_barrier();
         if (tile + 1 < n_tiles) fetch(tile + 1);
@@ -555,12 +550,16 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
                 const float p = __builtin_amdgcn_exp2f(ok ? sacc[e] * scale2 - lse2 : -INFINITY);
                 dsf[e >> 3][e & 7] = static_cast<__bf16>(p * (pacc[e] - dsum));
             }
+            // dQ += dS.K: the B operand (keys in dS's k-slot order, dimension
+            // nb*32 + col) is two 4-key runs transpose-read from the K rows
 #pragma unroll
             for (int kap = 0; kap < 2; ++kap)
 #pragma unroll
                 for (int nb = 0; nb < NDT; ++nb) {
-                    const bf16_t* kp = sKT + (nb * 32 + col) * Lay::TS + st * 32 + kap * 16 + half * 4;
-                    const bf16x8_t bf = __builtin_shufflevector(frag4(kp), frag4(kp + 8), 0, 1, 2, 3, 4, 5, 6, 7);
+                    const int k0 = st * 32 + kap * 16 + half * 4;
+                    const bf16x8_t bf = __builtin_shufflevector(k_tr4(sK, Lay::KS, k0, nb * 32),
+                                                                k_tr4(sK, Lay::KS, k0 + 8, nb * 32),
+                                                                0, 1, 2, 3, 4, 5, 6, 7);
                     dqacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dsf[kap], bf, dqacc[nb], 0, 0, 0);
                 }
         }
@@ -614,16 +613,14 @@ __global__ __launch_bounds__(256) void attend_bwd_dsum_kernel(const bf16_t* __re
 // with one tile per workgroup two workgroups share a CU, and their waves,
 // not held together by a common barrier, hide each other's LDS and matrix
 // latencies.  The cost is S computed twice.  The unit's query rows pass in
-// 32-row tiles through two LDS buffers (Q, dO row-major for S and dP,
-// transposed for the B operands of dK and dV, -lse in log2 units and D_i,
-// which a pre-pass computes once per row).
+// 32-row tiles through two LDS buffers (Q, dO row-major, -lse in log2 units
+// and D_i, which a pre-pass computes once per row); the B operands of dK and
+// dV (Q^T, dO^T) are transpose reads of the same rows (k_tr4).
 template <int D>
 struct KvLayout {
     static constexpr int KS = D + 8;       // row stride (bf16) of the Q, dO rows
-    static constexpr int QS = 32 + 4;      // row stride (bf16) of Q^T, dO^T
     static constexpr int kQ = 0;           // per buffer: Q rows, dO rows
-    static constexpr int kQT = kQ + 2 * 32 * KS * 2;    // Q^T, dO^T
-    static constexpr int kStat = kQT + 2 * D * QS * 2;  // lse2[32], dsum[32]
+    static constexpr int kStat = kQ + 2 * 32 * KS * 2;  // lse2[32], dsum[32]
     static constexpr int kBuf = kStat + 64 * 4;
     static constexpr int kTok = 2 * kBuf;               // up to 4 sub-tiles x 32 key tokens
     static constexpr int kBytes = kTok + 4 * 32 * 4;
@@ -726,8 +723,6 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
         unsigned char* base = smem + buf * Lay::kBuf;
         bf16_t* sQ = reinterpret_cast<bf16_t*>(base + Lay::kQ);
         bf16_t* sG = sQ + 32 * Lay::KS;
-        bf16_t* sQT = reinterpret_cast<bf16_t*>(base + Lay::kQT);
-        bf16_t* sGT = sQT + D * Lay::QS;
         float* s_stat = reinterpret_cast<float*>(base + Lay::kStat);
         if (sput) {
 #pragma unroll
@@ -735,11 +730,6 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
                 const int cv = u * TPR + sp;
                 store16(sQ + sm * Lay::KS + cv * 8, qx[u]);
                 store16(sG + sm * Lay::KS + cv * 8, gx[u]);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    sQT[(cv * 8 + e) * Lay::QS + sm] = elem16(qx[u], e);
-                    sGT[(cv * 8 + e) * Lay::QS + sm] = elem16(gx[u], e);
-                }
             }
         }
         if (sp == 0) {
@@ -758,8 +748,6 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
             const unsigned char* base = smem + buf * Lay::kBuf;
             const bf16_t* sQ = reinterpret_cast<const bf16_t*>(base + Lay::kQ);
             const bf16_t* sG = sQ + 32 * Lay::KS;
-            const bf16_t* sQT = reinterpret_cast<const bf16_t*>(base + Lay::kQT);
-            const bf16_t* sGT = sQT + D * Lay::QS;
             const float* s_stat = reinterpret_cast<const float*>(base + Lay::kStat);
             // S[query][key] (and dP for role 0): lane (half, col = key) holds
             // queries 8*(e/4) + 4*half + e%4
@@ -808,14 +796,18 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
                     for (int x = 0; x < 4; ++x) af[g4 >> 1][(g4 & 1) * 4 + x] = static_cast<__bf16>(p[x]);
                 }
             }
-            // role 0: dK[key][d] += dS^T.Q; role 1: dV[key][d] += P^T.dO
-            const bf16_t* sXT = role == 0 ? sQT : sGT;
+            // role 0: dK[key][d] += dS^T.Q; role 1: dV[key][d] += P^T.dO.  The
+            // B operand (query k-slots as in af, dimension nb*32 + col) is
+            // two 4-query runs transpose-read from the row-major Q or dO rows.
+            const bf16_t* sX = role == 0 ? sQ : sG;
 #pragma unroll
             for (int kap = 0; kap < 2; ++kap)
 #pragma unroll
                 for (int nb = 0; nb < NDT; ++nb) {
-                    const bf16_t* xp = sXT + (nb * 32 + col) * Lay::QS + kap * 16 + half * 4;
-                    const bf16x8_t bx = __builtin_shufflevector(frag4(xp), frag4(xp + 8), 0, 1, 2, 3, 4, 5, 6, 7);
+                    const int q0 = kap * 16 + half * 4;
+                    const bf16x8_t bx = __builtin_shufflevector(k_tr4(sX, Lay::KS, q0, nb * 32),
+                                                                k_tr4(sX, Lay::KS, q0 + 8, nb * 32),
+                                                                0, 1, 2, 3, 4, 5, 6, 7);
                     acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kap], bx, acc[nb], 0, 0, 0);
                 }
         }
