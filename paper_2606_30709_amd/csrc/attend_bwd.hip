@@ -403,9 +403,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 template <int D>
 struct DqLayout {
     static constexpr int KS = D + 8;
+    static constexpr int TS = KT + 4;
     static constexpr int kK = 0;
     static constexpr int kV = kK + KT * KS * 2;
-    static constexpr int kTok = kV + KT * KS * 2;
+    static constexpr int kKT = kV + KT * KS * 2;
+    static constexpr int kTok = kKT + D * TS * 2;
     static constexpr int kGid = kTok + KT * 4;
     static constexpr int kBytes = kGid + kMaxTopK * 4;
 };
@@ -427,6 +429,7 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
     extern __shared__ __align__(16) unsigned char smem[];
     bf16_t* sK = reinterpret_cast<bf16_t*>(smem + Lay::kK);
     bf16_t* sV = reinterpret_cast<bf16_t*>(smem + Lay::kV);
+    bf16_t* sKT = reinterpret_cast<bf16_t*>(smem + Lay::kKT);
     int* s_tok = reinterpret_cast<int*>(smem + Lay::kTok);
     int* s_gid = reinterpret_cast<int*>(smem + Lay::kGid);
 
@@ -493,7 +496,10 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
     const bf16_t* vbase = v_res + static_cast<int64_t>(bh) * res_tokens * D;
     const int lim = c * gpc;
 
-    // the next tile's rows are fetched into registers while this one is used
+    // The next tile's rows are fetched into registers while this one is
+    // used.  K is also staged transposed (K^T rows, one 16-bit write per
+    // element): the eight query-tile waves all read K^T for dQ, so one copy
+    // per tile costs less than a transpose read per wave (measured).
     const int srow = tid % KT, pv = tid / KT;
     vec16 kx[VPT], vx[VPT];
     int stok = -1;
@@ -520,6 +526,8 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
             const int cv = pv * VPT + u;
             *reinterpret_cast<vec16*>(sK + srow * Lay::KS + cv * 8) = kx[u];
             *reinterpret_cast<vec16*>(sV + srow * Lay::KS + cv * 8) = vx[u];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sKT[(cv * 8 + e) * Lay::TS + srow] = elem16(kx[u], e);
         }
         lds_barrier();
         if (tile + 1 < n_tiles) fetch(tile + 1);
@@ -550,16 +558,12 @@ __global__ __launch_bounds__(NW * 64) void attend_bwd_dq_kernel(
                 const float p = __builtin_amdgcn_exp2f(ok ? sacc[e] * scale2 - lse2 : -INFINITY);
                 dsf[e >> 3][e & 7] = static_cast<__bf16>(p * (pacc[e] - dsum));
             }
-            // dQ += dS.K: the B operand (keys in dS's k-slot order, dimension
-            // nb*32 + col) is two 4-key runs transpose-read from the K rows
 #pragma unroll
             for (int kap = 0; kap < 2; ++kap)
 #pragma unroll
                 for (int nb = 0; nb < NDT; ++nb) {
-                    const int k0 = st * 32 + kap * 16 + half * 4;
-                    const bf16x8_t bf = __builtin_shufflevector(k_tr4(sK, Lay::KS, k0, nb * 32),
-                                                                k_tr4(sK, Lay::KS, k0 + 8, nb * 32),
-                                                                0, 1, 2, 3, 4, 5, 6, 7);
+                    const bf16_t* kp = sKT + (nb * 32 + col) * Lay::TS + st * 32 + kap * 16 + half * 4;
+                    const bf16x8_t bf = __builtin_shufflevector(frag4(kp), frag4(kp + 8), 0, 1, 2, 3, 4, 5, 6, 7);
                     dqacc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(dsf[kap], bf, dqacc[nb], 0, 0, 0);
                 }
         }
