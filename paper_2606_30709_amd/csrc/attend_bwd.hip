@@ -111,6 +111,11 @@ __device__ __forceinline__ void lds_barrier() {
 
 constexpr int kXcds = 8;  // XCDs of the chip; workgroups are dealt to them in turn
 
+template <bool B>
+struct BoolTag {
+    static constexpr bool value = B;
+};
+
 // Logical work item of this workgroup: consecutive items on one XCD, so the
 // workgroups of one unit (which read the same key tiles or query rows) share
 // that XCD's L2.
@@ -745,6 +750,12 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
     fetch(0);
     put(0);
     lds_barrier();
+    // The masks (causal on the current chunk, -inf for a skipped key row)
+    // cost three vector instructions per score; most waves have neither, so
+    // the query-tile loop exists in two forms and each wave takes its own
+    // (the forms execute the same barriers).
+    auto qtiles = [&](auto mask_tag) {
+    constexpr bool kMask = decltype(mask_tag)::value;
     for (int qt = 0; qt < nq; ++qt) {
         const int buf = qt & 1;
         if (qt + 1 < nq) fetch(qt + 1);
@@ -781,12 +792,14 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
 #pragma unroll
             for (int g4 = 0; g4 < 4; ++g4) {
                 const float4 l4 = *reinterpret_cast<const float4*>(s_stat + g4 * 8 + half * 4);
-                const float nl[4] = {l4.x + kbias, l4.y + kbias, l4.z + kbias, l4.w + kbias};
+                const float nl[4] = {kMask ? l4.x + kbias : l4.x, kMask ? l4.y + kbias : l4.y,
+                                     kMask ? l4.z + kbias : l4.z, kMask ? l4.w + kbias : l4.w};
                 float p[4];
 #pragma unroll
                 for (int x = 0; x < 4; ++x) {
                     float a = fmaf(sacc[g4 * 4 + x], scale2, nl[x]);
-                    if (current) a = kr <= buf * 32 + g4 * 8 + half * 4 + x ? a : -INFINITY;
+                    if (kMask && current)
+                        a = kr <= buf * 32 + g4 * 8 + half * 4 + x ? a : -INFINITY;
                     p[x] = __builtin_amdgcn_exp2f(a);
                 }
                 if (role == 0) {
@@ -818,6 +831,11 @@ __global__ __launch_bounds__(NSUB * 128) __attribute__((amdgpu_waves_per_eu(2, 2
         if (qt + 1 < nq) put(buf ^ 1);
         lds_barrier();
     }
+    };
+    if (current || __builtin_amdgcn_ballot_w64(tok < 0) != 0)
+        qtiles(BoolTag<true>{});
+    else
+        qtiles(BoolTag<false>{});
 
     // acc[nb][e]: key 8*(e/4) + 4*half + e%4 of the sub-tile, dimension nb*32 + col
     if (kactive) {
