@@ -539,6 +539,23 @@ hga_status hga_prefill_blocks(const hga_plan* plan, const void* q_blocks, int32_
                               void* k_routed, void* v_routed, void* out, float* lse,
                               void* workspace, int64_t workspace_bytes, void* stream);
 
+/* The closed chunks that query chunk c sees besides its own (Sec. 3.3,
+ * deterministic visibility): the first min(keep_first, c) chunks and the
+ * recent window [max(0, c - W), c), W = max(keep_last, force_prev), in
+ * ascending order, without repeats.  These are the chunks the attention
+ * reads from the resident K/V for c (through res_slot when one is given),
+ * so a caller that keeps a compact resident set takes it from here rather
+ * than restating the rule.  Host-only: validates params as hga_plan_create
+ * does, touches no device.
+ *   params  the routing parameters (hf_pairs_* are not used)
+ *   c       query chunk, >= 0
+ *   chunks  out, int32[cap] (NULL when cap = 0): the ids, ascending
+ *   cap     capacity of chunks
+ * Returns the number of visible chunks (which may exceed cap: then only the
+ * first cap are written), or a negative hga_status for invalid params or
+ * c < 0. */
+int32_t hga_visible_chunks(const hga_params* params, int32_t c, int32_t* chunks, int32_t cap);
+
 /* Static description of a status code (never NULL). */
 const char* hga_status_string(int32_t status);
 

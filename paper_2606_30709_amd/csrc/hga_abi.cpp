@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "hga.h"
+#include "attend_common.hpp"
 #include "hga_internal.hpp"
 
 namespace {
@@ -170,6 +171,17 @@ void clear_stale_error() { (void)hipGetLastError(); }
 extern "C" {
 
 int32_t hga_version(void) { return (1 << 16) | 0; }
+
+int32_t hga_visible_chunks(const hga_params* params, int32_t c, int32_t* chunks, int32_t cap) {
+    HGA_TRY(validate_params(params));
+    if (c < 0 || cap < 0) return fail(HGA_EINVAL, "c and cap must be >= 0");
+    if (cap > 0 && !chunks) return fail(HGA_EINVAL, "chunks is NULL");
+    // the enumeration the attention kernels use
+    const hga::VisibleChunks vis(c, params->keep_first, hga::recent_window(*params));
+    for (int idx = 0; idx < vis.count && idx < cap; ++idx) chunks[idx] = vis.chunk(idx);
+    clear_stale_error();
+    return vis.count;
+}
 
 const char* hga_status_string(int32_t status) {
     switch (status) {

@@ -22,7 +22,7 @@ __all__ = [
     "hga_attend_split_static", "hga_static_scratch_bytes", "hga_gather_attend",
     "hga_gather_attend_split", "hga_gather_kv_cached", "hga_attend_backward",
     "hga_block_step", "hga_prefill_blocks", "hga_status_string", "hga_last_error",
-    "hga_version", "EXPORTED_SYMBOLS",
+    "hga_version", "hga_visible_chunks", "EXPORTED_SYMBOLS",
 ]
 
 F32, BF16 = 0, 1
@@ -36,7 +36,7 @@ EXPORTED_SYMBOLS = (
     "hga_gather_attend", "hga_gather_attend_split",
     "hga_gather_kv_cached", "hga_attend_backward", "hga_block_step", "hga_prefill_blocks",
     "hga_status_string",
-    "hga_last_error", "hga_version",
+    "hga_last_error", "hga_version", "hga_visible_chunks",
 )
 
 
@@ -119,6 +119,8 @@ def library() -> ctypes.CDLL:
         lib.hga_last_error.restype = ctypes.c_char_p
         lib.hga_version.argtypes = []
         lib.hga_version.restype = i32
+        lib.hga_visible_chunks.argtypes = [ctypes.POINTER(HgaParams), i32, vp, i32]
+        lib.hga_visible_chunks.restype = i32
         _LIB = lib
     return _LIB
 
@@ -133,6 +135,18 @@ def hga_last_error() -> str:
 
 def hga_version() -> int:
     return library().hga_version()
+
+
+def hga_visible_chunks(params: HgaParams, c: int) -> list:
+    """The closed chunks query chunk c sees besides its own, ascending (the
+    library's enumeration; host only)."""
+    n = library().hga_visible_chunks(ctypes.byref(params), c, None, 0)
+    if n < 0:
+        raise HgaError(n, hga_last_error())
+    buf = (ctypes.c_int32 * max(n, 1))()
+    _check(min(0, library().hga_visible_chunks(ctypes.byref(params), c,
+                                               ctypes.cast(buf, ctypes.c_void_p), n)))
+    return list(buf[:n])
 
 
 def _check(status: int):

@@ -211,9 +211,9 @@ class DecodePipeline:
         # cold tier: the history in pinned host memory
         self.k_hist = k_all[:, :, :hist].contiguous().pin_memory()
         self.v_hist = v_all[:, :, :hist].contiguous().pin_memory()
-        # hot tier: first F chunks, the recent window, then the current block
-        window = max(w.keep_last, 1 if w.force_prev else 0)
-        hot = sorted(set(range(min(w.keep_first, c))) | set(range(max(0, c - window), c)))
+        # hot tier: the chunks the block sees besides its own (the library's
+        # visibility rule: first F chunks, the recent window), then the block
+        hot = hga.hga_visible_chunks(self.plan.params, c)
         self.hot_chunks = hot + [c]
         slot = np.full(c + 1, -1, dtype=np.int32)
         for s, cc in enumerate(self.hot_chunks):
@@ -344,9 +344,10 @@ class DecodeSequencePipeline:
         v_all = to_device(inputs["v"], w.dtype, "cpu")
         self.k_hist = k_all.contiguous().pin_memory()      # cold tier: every token
         self.v_hist = v_all.contiguous().pin_memory()
-        window = max(w.keep_last, 1 if w.force_prev else 0)
-        hot = sorted(set(range(min(w.keep_first, self.c0))) |
-                     set(range(max(0, self.c0 - window), c_end)))
+        # hot tier: every chunk some block sees besides its own (the
+        # library's visibility rule), and the blocks' own chunks
+        hot = sorted(set(range(self.c0, c_end)).union(
+            *(hga.hga_visible_chunks(self.plan.params, c) for c in range(self.c0, c_end))))
         slot = np.full(c_end, -1, dtype=np.int32)
         for s, cc in enumerate(hot):
             slot[cc] = s

@@ -118,3 +118,32 @@ def test_valid_plan_without_device_reports_hip_error():
     h = ctypes.c_void_p()
     assert lib.hga_plan_create(ctypes.byref(p), ctypes.byref(h)) == -4
     assert h.value is None
+
+
+@pytest.mark.parametrize("keep_first,keep_last,force_prev", [
+    (1, 0, 1), (1, 0, 0), (2, 8, 1), (0, 3, 0), (4, 2, 1), (0, 0, 0), (3, 1, 0)])
+def test_visible_chunks_follow_the_oracle(keep_first, keep_last, force_prev):
+    """hga_visible_chunks (the enumeration the attention kernels use, host
+    only) lists exactly the oracle's deterministic visible chunks D_c
+    (Sec. 3.3) for every query chunk, and honours its capacity."""
+    from oracle import hga_oracle as O
+    p = _params(keep_first=keep_first, keep_last=keep_last, force_prev=force_prev)
+    lib = hga.library()
+    for c in range(0, 40):
+        D, _ = O.visibility(c, keep_first, keep_last, force_prev)
+        assert hga.hga_visible_chunks(p, c) == D, c
+        if D:
+            buf = (ctypes.c_int32 * 1)(-7)
+            assert lib.hga_visible_chunks(ctypes.byref(p), c, ctypes.cast(buf, ctypes.c_void_p),
+                                          1) == len(D)
+            assert buf[0] == D[0]
+
+
+def test_visible_chunks_reject_bad_input():
+    lib = hga.library()
+    p = _params()
+    assert lib.hga_visible_chunks(ctypes.byref(p), -1, None, 0) == -1
+    assert lib.hga_visible_chunks(ctypes.byref(p), 5, None, 3) == -1   # cap without a buffer
+    bad = _params(head_dim=96)
+    assert lib.hga_visible_chunks(ctypes.byref(bad), 5, None, 0) == -2
+    assert lib.hga_visible_chunks(None, 5, None, 0) == -1
