@@ -547,8 +547,16 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(D == 64
                                     static_cast<uint32_t>(src_tokens * kRowBytes));
     const u32x4 rv_src = rsrc_words(v_src + static_cast<int64_t>(bh) * src_tokens * D,
                                     static_cast<uint32_t>(src_tokens * kRowBytes));
-    const u32x4 rk_rt = rsrc_words(k_routed + unit * routed_rows * D, routed_rows * kRowBytes);
-    const u32x4 rv_rt = rsrc_words(v_routed + unit * routed_rows * D, routed_rows * kRowBytes);
+    // The routed buffers may be null (the gather form keeping the rows on
+    // chip): their unit offsets are taken as integers, and the buffers are
+    // only accessed when given.
+    const int64_t rt_off = unit * routed_rows * static_cast<int64_t>(kRowBytes);
+    const u32x4 rk_rt = rsrc_words(reinterpret_cast<const void*>(
+                                       reinterpret_cast<uintptr_t>(k_routed) + rt_off),
+                                   routed_rows * kRowBytes);
+    const u32x4 rv_rt = rsrc_words(reinterpret_cast<const void*>(
+                                       reinterpret_cast<uintptr_t>(v_routed) + rt_off),
+                                   routed_rows * kRowBytes);
 
     // The unit's group ids into LDS.
     {
