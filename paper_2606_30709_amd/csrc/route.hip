@@ -15,11 +15,12 @@
 namespace hga {
 namespace {
 
-// Chunk-summary rows staged per LDS block: for D = 64 one block covers the
-// middle chunks of every query chunk up to 128 chunks in, so short contexts
-// need a single round trip for the table; D = 128 rows stay at 64 per block
-// (measured faster: half the registers and LDS per block).
-constexpr int table_rows(int d) { return d == 64 ? 128 : 64; }
+// Chunk-summary rows staged per LDS block, 64 at either head size: one row
+// per lane of the scoring wavefront.  Taller blocks (128 rows at D = 64, one
+// round trip for contexts up to 128 chunks) were measured slower: twice the
+// prefetch registers and LDS per block, and a longer first load before the
+// first scores.
+constexpr int table_rows(int) { return 64; }
 
 __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_wave_barrier();
@@ -150,6 +151,7 @@ __global__ __launch_bounds__(256) void route_kernel(
     constexpr int TS = D + 4;               // padded LDS row stride (floats)
     constexpr int F4 = D / 4;               // float4 per table row
     constexpr int PF = TB * F4 / kThreads;  // float4 per thread per table block
+    static_assert(PF >= 1 && PF * kThreads == TB * F4, "table block split");
     extern __shared__ __align__(16) unsigned char smem_raw[];
     float* s_tab = reinterpret_cast<float*>(smem_raw);
     unsigned char* wave_base = smem_raw + align16(sizeof(float) * TB * TS);
