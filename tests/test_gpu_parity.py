@@ -508,6 +508,49 @@ def test_attend_split_matches_oracle(hga, key):
         assert torch.equal(_bits(out), _bits(po)) and torch.equal(lse, pl)
 
 
+@pytest.mark.parametrize("key", ["qwen_4k_ragged", "gqa3_d64", "f32_d128_gqa", "mha_d128"])
+def test_gather_attend_split_without_routed_buffers(hga, key):
+    """hga_gather_attend_split from device-resident sources, on prefill-layout
+    query blocks: the routed rows it writes are hga_gather_kv's, and with
+    both routed buffers NULL (rows gathered on chip only) its output and LSE
+    are the same bits, also with padded and out-of-range group ids."""
+    from paper_2606_30709_amd.pipeline import PrefillPipeline
+    w = SPLIT_CASES[key]
+    _say(f"[gather-attend-split, no routed buffers] {key}")
+    pipe = PrefillPipeline(w, W.generate(w), gather_mode="separate")
+    pipe.summaries()
+    pipe.route()
+    pipe.gather()
+    torch.cuda.synchronize()
+    C = w.chunk
+    planted = pipe.group_idx.clone()
+    c = w.n_chunks - 1
+    planted[0, 0, c, 0] = -1
+    planted[0, w.n_kv_heads - 1, c, w.topk_groups - 1] = 10 ** 6
+    for gi_all, c0, n in ((pipe.group_idx, 0, 1), (pipe.group_idx, w.n_chunks // 3, 3),
+                          (planted, c, 1)):
+        q = pipe.q[:, :, c0 * C:(c0 + n) * C].contiguous()
+        gi = gi_all[:, :, c0:c0 + n].contiguous()
+        ws = torch.empty(hga.hga_attend_split_workspace(pipe.plan, n) // 4,
+                         dtype=torch.float32, device="cuda")
+        kr = torch.full_like(pipe.k_routed[:, :, c0:c0 + n], float("nan"))
+        vr = torch.full_like(kr, float("nan"))
+        outs = []
+        for routed in ((kr, vr), (None, None)):
+            out = torch.full_like(q, float("nan"))
+            lse = torch.full(q.shape[:3], float("nan"), device="cuda")
+            hga.hga_gather_attend_split(pipe.plan, q, c0, pipe.k, pipe.v, pipe.k, pipe.v, gi,
+                                        routed[0], routed[1], out, ws, lse)
+            torch.cuda.synchronize()
+            outs.append((out, lse))
+        if gi_all is pipe.group_idx:  # the separate gather ran on these ids
+            assert torch.equal(_bits(kr), _bits(pipe.k_routed[:, :, c0:c0 + n]))
+            assert torch.equal(_bits(vr), _bits(pipe.v_routed[:, :, c0:c0 + n]))
+        (o1, l1), (o2, l2) = outs
+        assert not torch.isnan(o1).any() and not torch.isnan(l1).any()
+        assert torch.equal(_bits(o1), _bits(o2)) and torch.equal(l1, l2)
+
+
 def test_gather_attend_full_size(hga):
     """The fused call equals the two calls at the full prefill sizes."""
     from paper_2606_30709_amd.pipeline import PrefillPipeline
