@@ -337,8 +337,15 @@ def dense_comparator(w, pipe, reps: int = 20):
         return {"available": False, "reason": str(e).splitlines()[0][:200]}
     ms = e0.elapsed_time(e1) / reps
     del out
-    return {"available": True, "kernel": "torch SDPA (flash / memory-efficient), causal",
-            "ms": round(ms, 4), "tokens_per_s": round(w.batch * w.seq_len / (ms * 1e-3), 1)}
+    # 4*d FLOPs per visible (query, key) pair, N(N+1)/2 pairs per query head
+    flops = 4.0 * w.head_dim * w.batch * w.n_q_heads * w.seq_len * (w.seq_len + 1) / 2
+    tflops = flops / (ms * 1e-3) / 1e12
+    out = {"available": True, "kernel": "torch SDPA (flash / memory-efficient), causal",
+           "ms": round(ms, 4), "tokens_per_s": round(w.batch * w.seq_len / (ms * 1e-3), 1),
+           "TFLOP_s": round(tflops, 1)}
+    if w.dtype == "bf16":
+        out["mfma_frac"] = round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)
+    return out
 
 
 def decode_bench(w, inp, args):
