@@ -310,6 +310,13 @@ def measured_copy_bandwidth(nbytes: int = 1 << 30, reps: int = 10) -> float:
     return 2 * nbytes / sec / 1e9
 
 
+def dense_causal_flops(w) -> float:
+    """FLOPs of dense causal attention over the workload's Q/K/V: 4*d per
+    visible (query, key) pair (two d-long products, a multiply and an add
+    each), N(N+1)/2 pairs per query head."""
+    return 4.0 * w.head_dim * w.batch * w.n_q_heads * w.seq_len * (w.seq_len + 1) / 2
+
+
 def dense_comparator(w, pipe, reps: int = 20):
     """Dense causal attention over the same Q/K/V with PyTorch's fused SDPA
     (a comparator only: flash or memory-efficient kernels, never the
@@ -337,9 +344,7 @@ def dense_comparator(w, pipe, reps: int = 20):
         return {"available": False, "reason": str(e).splitlines()[0][:200]}
     ms = e0.elapsed_time(e1) / reps
     del out
-    # 4*d FLOPs per visible (query, key) pair, N(N+1)/2 pairs per query head
-    flops = 4.0 * w.head_dim * w.batch * w.n_q_heads * w.seq_len * (w.seq_len + 1) / 2
-    tflops = flops / (ms * 1e-3) / 1e12
+    tflops = dense_causal_flops(w) / (ms * 1e-3) / 1e12
     out = {"available": True, "kernel": "torch SDPA (flash / memory-efficient), causal",
            "ms": round(ms, 4), "tokens_per_s": round(w.batch * w.seq_len / (ms * 1e-3), 1),
            "TFLOP_s": round(tflops, 1)}

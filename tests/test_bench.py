@@ -97,3 +97,11 @@ def test_bench_line_contract():
         assert k in rf, k
     assert rf["bound"] in ("hbm", "mfma", "alu")
     assert 0 < rf["frac"] < 1 and abs(rf["achieved"] / rf["peak"] - rf["frac"]) < 1e-3
+
+
+def test_dense_causal_flops_count_every_causal_pair():
+    """4*d FLOPs per (query, key) pair with key <= query, counted one pair at
+    a time on a small shape."""
+    w = W.preset("tiny").with_(batch=2, n_q_heads=4, n_kv_heads=2, seq_len=3 * 64)
+    pairs = sum(1 for qi in range(w.seq_len) for ki in range(w.seq_len) if ki <= qi)
+    assert bench.dense_causal_flops(w) == 4.0 * w.head_dim * w.batch * w.n_q_heads * pairs
