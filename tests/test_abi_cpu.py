@@ -32,6 +32,21 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, n), n
 
 
+def test_library_exports_nothing_undeclared():
+    """Every hga_ function in the library's dynamic symbol table is declared
+    in the header (no undocumented entry points)."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--defined-only", hga.library_path()], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines()
+                if len(l.split()) == 3 and l.split()[1] == "T" and l.split()[-1].startswith("hga_")}
+    assert exported == set(_declared_functions())
+
+
 def test_status_strings_and_version():
     for st in (0, -1, -2, -3, -4):
         assert hga.hga_status_string(st).startswith("HGA_")
