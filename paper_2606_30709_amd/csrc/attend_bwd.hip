@@ -860,16 +860,16 @@ hipError_t launch_bwd_split_t(const hga_plan& plan, const void* q_rot, int q_chu
                               const void* dout, float* dq, float* dk, float* dv, hipStream_t stream) {
     const hga_params& p = plan.p;
     constexpr int kSub = 2;  // 32-key sub-tiles per key-side workgroup (one tile)
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_bwd_dq_kernel<D, kNwDq>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, DqLayout<D>::kBytes);
+    static std::atomic<uint64_t> configured{0};  // per instantiation and device
+    const hipError_t ce = once_per_device(configured, plan.device, [] {
+        const hipError_t e = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&attend_bwd_dq_kernel<D, kNwDq>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, DqLayout<D>::kBytes);
         if (e != hipSuccess) return e;
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_bwd_kv_kernel<D, kSub>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, KvLayout<D>::kBytes);
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+        return hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_bwd_kv_kernel<D, kSub>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, KvLayout<D>::kBytes);
+    });
+    if (ce != hipSuccess) return ce;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int group_shift = p.group == 8 ? 3 : (p.group == 16 ? 4 : 5);
     const int window = recent_window(p);
@@ -916,14 +916,12 @@ hipError_t launch_bwd_t(const hga_plan& plan, const void* q_rot, int q_chunk0, i
                         const void* dout, float* dq, float* dk, float* dv, hipStream_t stream) {
     const hga_params& p = plan.p;
     constexpr int kLds = BwdLayout<D, NW>::kBytes;
-    static bool configured = false;
-    if (!configured) {
-        const hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&attend_bwd_kernel<D, NW>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    static std::atomic<uint64_t> configured{0};  // per instantiation and device
+    const hipError_t ce = once_per_device(configured, plan.device, [] {
+        return hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_bwd_kernel<D, NW>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
+    });
+    if (ce != hipSuccess) return ce;
     const int r = p.n_q_heads / p.n_kv_heads;
     const int wg_per_unit = (2 * r + NW - 1) / NW;
     const int64_t items = static_cast<int64_t>(p.batch) * p.n_kv_heads * n_q_chunks * wg_per_unit;

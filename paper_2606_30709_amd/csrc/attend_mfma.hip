@@ -887,14 +887,13 @@ hipError_t launch_mfma_t(const hga_plan& plan, hipStream_t stream, hipEvent_t ev
         src_tokens = res_tokens;
     }
     constexpr uint32_t kLds = Layout<D, NS>::kBytes;
-    static bool configured = false;  // per instantiation (the limit is a function attribute)
-    if (!configured) {
-        const hipError_t e = hipFuncSetAttribute(
+    static std::atomic<uint64_t> configured{0};  // per instantiation and device
+    const hipError_t ce = once_per_device(configured, plan.device, [] {
+        return hipFuncSetAttribute(
             reinterpret_cast<const void*>(&attend_mfma_kernel<D, KS, NS, NW, kGather, kSplit>),
             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+    });
+    if (ce != hipSuccess) return ce;
     const int grid = (n_items + kXcds - 1) / kXcds * kXcds;
     hipExtLaunchKernelGGL((attend_mfma_kernel<D, KS, NS, NW, kGather, kSplit>), dim3(grid),
                           dim3(NW * 64), kLds, stream, ev_start, ev_stop, 0, q_rot, q_chunk0,

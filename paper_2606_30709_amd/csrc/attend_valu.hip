@@ -204,14 +204,13 @@ hipError_t launch_attend_valu(const hga_plan& plan, const void* q_rot, int q_chu
     const size_t lds = tiles > merge ? tiles : merge;
 #define HGA_VALU(DD)                                                                            \
     do {                                                                                        \
-        static bool configured = false;                                                         \
-        if (!configured) {                                                                      \
-            const hipError_t e = hipFuncSetAttribute(                                           \
-                reinterpret_cast<const void*>(&attend_valu_kernel<DD>),                         \
-                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));            \
-            if (e != hipSuccess) return e;                                                      \
-            configured = true;                                                                  \
-        }                                                                                       \
+        static std::atomic<uint64_t> configured{0}; /* per kernel and device */                \
+        const hipError_t ce = once_per_device(configured, plan.device, [&] {                   \
+            return hipFuncSetAttribute(reinterpret_cast<const void*>(&attend_valu_kernel<DD>),  \
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,              \
+                                       static_cast<int>(lds));                                  \
+        });                                                                                     \
+        if (ce != hipSuccess) return ce;                                                        \
         hipExtLaunchKernelGGL((attend_valu_kernel<DD>), grid, dim3(64 * kSplit), lds, stream,   \
                               ev_start, ev_stop, 0, static_cast<const float*>(q_rot), q_chunk0, \
                               n_q_chunks, static_cast<const float*>(k_res),                     \

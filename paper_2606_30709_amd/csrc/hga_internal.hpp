@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "hga.h"
 
 struct hga_plan {
@@ -33,6 +35,19 @@ constexpr int kRouteSpreadCandidates = 4096;
 inline size_t route_workspace_bytes() {
     return sizeof(uint64_t) * kRouteSpreadUnits * kRouteSpreadCandidates +
            sizeof(unsigned) * kRouteSpreadUnits;
+}
+
+// Runs `set` (a kernel's one-time attribute setting, e.g. its dynamic LDS
+// limit) once per device: function attributes belong to the kernel on each
+// device, so a process that launches on several devices sets them on each.
+// `done` holds one bit per device id below 64 (larger ids set every time).
+template <typename F>
+inline hipError_t once_per_device(std::atomic<uint64_t>& done, int device, F set) {
+    const uint64_t bit = device >= 0 && device < 64 ? uint64_t(1) << device : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    const hipError_t e = set();
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+    return e;
 }
 
 // visible-window length W = max(L, force_prev ? 1 : 0)
